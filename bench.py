@@ -1,0 +1,287 @@
+#!/usr/bin/env python3
+"""Benchmark of the GETT contraction library on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-report]
+                    [--no-cpu-baseline]
+
+A step is one contraction C <- alpha*A*B + beta*C of the headline workload
+(bw4x3_fp32: C[a,b,c,d] = A[a,e,b] * B[e,d,c], a..d = 112, e = 16,
+alpha 1.5, beta 1) with inputs already resident in device memory.  W untimed
+steps, then K timed steps between device synchronisations; one JSON line on
+stdout.  The line also carries:
+  roofline      the kernel's algorithmic bytes (or flops) per launch over its
+                average launch time (HIP events on the launch stream), against
+                MI355X's published peak;
+  cpu_baseline  the oracle (plain C, fp64, all host threads) on a bounded
+                sample of the same workload;
+  workloads     every workload with cold-cache kernel times (minimum and
+                median over runs, each after a 1 GiB cache flush), GFLOP/s,
+                GB/s, fraction of its bound, and an equal-size GEMM (torch ->
+                hipBLASLt/rocBLAS) timed the same way (Sec. 7: the GEMM of
+                sizes S_Im x S_In x S_Ik).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import workloads as wl  # noqa: E402
+
+PEAK = {"hbm_GBs": 8000.0, "f32_TFLOPs": 157.3, "f64_TFLOPs": 78.6}
+HEADLINE = "bw4x3_fp32"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_1607_00145_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def bound_of(w) -> str:
+    ai = wl.flop_count(w) / wl.algorithmic_bytes(w)
+    ridge = (PEAK["f32_TFLOPs"] if w.dtype == "f32" else PEAK["f64_TFLOPs"]) * 1e3 / PEAK["hbm_GBs"]
+    return "mfma" if ai > ridge else "hbm"
+
+
+class Problem:
+    """One workload on the device, planned."""
+
+    def __init__(self, w, dev):
+        import torch
+
+        import paper_1607_00145_amd as g
+        self.w, self.g, self.dev = w, g, dev
+        A, B, Cin = wl.make_inputs(w)
+        self.host = (A, B, Cin)
+        flat = lambda t: torch.from_numpy(np.asfortranarray(t).reshape(-1, order="F")).to(dev)
+        self.A, self.B = flat(A), flat(B)
+        self.C0 = flat(Cin) if Cin is not None else None
+        self.C = self.C0.clone() if Cin is not None else torch.zeros(w.numel("C"), dtype=self.A.dtype,
+                                                                     device=dev)
+        dt = g.GETT_FLOAT32 if w.dtype == "f32" else g.GETT_FLOAT64
+        st, self.h = g.gett_plan(dt, w.modes_C, w.shape("C"), None, w.modes_A, w.shape("A"), None,
+                                 w.modes_B, w.shape("B"), None, 0)
+        if st != 0:
+            raise RuntimeError(f"gett_plan: {g.gett_status_string(st)}")
+        self.plan = json.loads(g.gett_plan_describe(self.h))
+
+    def launch(self, stream):
+        st = self.g.gett_contract(self.h, self.w.alpha, self.A.data_ptr(), self.B.data_ptr(),
+                                  self.w.beta, self.C.data_ptr(), stream.cuda_stream)
+        if st != 0:
+            raise RuntimeError(f"gett_contract: {self.g.gett_status_string(st)}")
+
+    def close(self):
+        self.g.gett_destroy(self.h)
+
+
+def time_launches(fn, n, stream, flush=None):
+    """Per-launch HIP event times (ms) on `stream`, optionally after a flush."""
+    import torch
+    ts = []
+    for _ in range(n):
+        if flush is not None:
+            flush()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        e1.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return ts
+
+
+def cpu_baseline(w, target_s=15.0):
+    """The oracle on a bounded, evenly spaced sample of C's elements."""
+    import oracle
+    A, B, Cin = wl.make_inputs(w)
+    nC = w.numel("C")
+    flops_per_elem = wl.flop_count(w) / nC
+    threads = oracle.max_threads()
+    # calibrate on a small sample, then size the measured sample to ~target_s
+    n0 = min(nC, 200_000)
+    pts = np.linspace(0, nC - 1, n0).astype(np.int64)
+    t = time.perf_counter()
+    oracle.contract(w.modes_C, w.modes_A, w.modes_B, A, B, w.alpha, w.beta, Cin,
+                    shape_C=w.shape("C"), points=pts)
+    dt0 = time.perf_counter() - t
+    n = int(min(nC, max(n0, n0 * target_s / max(dt0, 1e-6))))
+    pts = np.linspace(0, nC - 1, n).astype(np.int64)
+    t = time.perf_counter()
+    oracle.contract(w.modes_C, w.modes_A, w.modes_B, A, B, w.alpha, w.beta, Cin,
+                    shape_C=w.shape("C"), points=pts)
+    dt = time.perf_counter() - t
+    return {"value": round(flops_per_elem * n / dt / 1e9, 4), "unit": "GFLOP/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{n} of {nC} elements of C ({w.name}), evenly spaced; {dt:.1f} s"}
+
+
+def traffic_for(kernel_name: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary, or None
+    when it was measured on other kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        d = json.load(open(path))
+    except Exception:
+        return None
+    if d.get("source_hash") != kernel_source_hash():
+        return None
+    return d.get("bytes_per_launch")
+
+
+def report_workload(w, dev, stream, runs, flush):
+    import torch
+    p = Problem(w, dev)
+    flops = wl.flop_count(w)
+    nbytes = wl.algorithmic_bytes(w)
+    for _ in range(3):
+        p.launch(stream)
+    ts = time_launches(lambda: p.launch(stream), runs, stream, flush)
+    tmin, tmed = min(ts), statistics.median(ts)
+    bound = bound_of(w)
+    peak_f = (PEAK["f32_TFLOPs"] if w.dtype == "f32" else PEAK["f64_TFLOPs"]) * 1e12
+    rec = {"workload": w.name, "expression": w.expression(), "dtype": w.dtype,
+           "bound": bound, "ms_min": round(tmin, 5), "ms_median": round(tmed, 5),
+           "gflops": round(flops / (tmin * 1e-3) / 1e9, 1),
+           "gbs": round(nbytes / (tmin * 1e-3) / 1e9, 1)}
+    rec["frac_mfma_peak"] = round(flops / (tmin * 1e-3) / peak_f, 4)
+    rec["frac_hbm_peak"] = round(nbytes / (tmin * 1e-3) / (PEAK["hbm_GBs"] * 1e9), 4)
+    rec["frac_of_bound"] = rec["frac_mfma_peak"] if bound == "mfma" else rec["frac_hbm_peak"]
+    rec["plan"] = {k: p.plan[k] for k in ("swapped", "merges", "x_order", "y_order", "k_order",
+                                           "gather_x", "gather_y", "c_vector")}
+    rec["plan"]["tile"] = [p.plan["tile"]["mt"], p.plan["tile"]["nt"], p.plan["tile"]["kt"]]
+    rec["plan"]["workgroups"] = p.plan["grid"]["workgroups"]
+    p.close()
+    # equal-size GEMM (Sec. 7): S_Im x S_Ik times S_Ik x S_In with the same alpha, beta
+    M, N, K = p.plan["size_x"], p.plan["size_y"], p.plan["size_k"]
+    del p
+    torch.cuda.empty_cache()
+    dt = torch.float32 if w.dtype == "f32" else torch.float64
+    torch.backends.cuda.matmul.allow_tf32 = False
+    a = torch.randn(M, K, dtype=dt, device=dev)
+    b = torch.randn(K, N, dtype=dt, device=dev)
+    c = torch.randn(M, N, dtype=dt, device=dev)
+    if w.beta != 0:
+        fn = lambda: torch.addmm(c, a, b, beta=w.beta, alpha=w.alpha, out=c)
+    else:
+        fn = lambda: torch.mm(a, b, out=c)
+    for _ in range(3):
+        fn()
+    gts = time_launches(fn, runs, stream, flush)
+    gmin = min(gts)
+    rec["gemm_ms_min"] = round(gmin, 5)
+    rec["gemm_gflops"] = round(flops / (gmin * 1e-3) / 1e9, 1)
+    rec["vs_equal_size_gemm"] = round(gmin / tmin, 4)
+    del a, b, c
+    torch.cuda.empty_cache()
+    return rec
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=HEADLINE, choices=[w.name for w in wl.WORKLOADS])
+    ap.add_argument("--report-runs", type=int, default=20)
+    ap.add_argument("--no-report", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the contraction is built and timed on a single "
+              "MI355X; --gpus above 1 is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    import paper_1607_00145_amd as g
+    g.load_library()   # fails loudly when the HIP library is not built
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    w = wl.BY_NAME[args.workload]
+
+    # ---- headline: K back-to-back steps, inputs resident ----
+    p = Problem(w, dev)
+    log(f"[bench] {w.name}: plan {json.dumps({k: p.plan[k] for k in ('tile', 'kbox', 'grid')})}")
+    for _ in range(args.warmup):
+        p.launch(stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        p.launch(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed / args.steps * 1e3
+    flops = wl.flop_count(w)
+    value = flops * args.steps / elapsed / 1e9
+    # live per-launch kernel time (HIP events on the launch stream)
+    ev = time_launches(lambda: p.launch(stream), max(20, min(args.steps, 200)), stream)
+    kavg = statistics.mean(ev)
+    bound = bound_of(w)
+    if bound == "hbm":
+        per_launch = wl.algorithmic_bytes(w)
+        roof = {"bound": "hbm", "achieved": round(per_launch / (kavg * 1e-3) / 1e9, 1),
+                "peak": PEAK["hbm_GBs"], "unit": "GB/s"}
+    else:
+        per_launch = flops
+        pk = PEAK["f32_TFLOPs"] if w.dtype == "f32" else PEAK["f64_TFLOPs"]
+        roof = {"bound": "mfma", "achieved": round(per_launch / (kavg * 1e-3) / 1e12, 2),
+                "peak": pk, "unit": "TFLOP/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = traffic_for("gett_macro_kernel", w.name)
+    roof["kernel_ms_avg"] = round(kavg, 5)
+    p.close()
+    del p
+    torch.cuda.empty_cache()
+
+    out = {"metric": "GFLOP/s", "value": round(value, 1), "unit": "GFLOP/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": w.dtype, "data": "synthetic (seeded PCG64, workloads module)",
+           "config": {"workload": w.name, "expression": w.expression(),
+                      "extents": w.extents, "alpha": w.alpha, "beta": w.beta,
+                      "layout": "column-major", "parallelism": "single GPU"},
+           "roofline": roof}
+
+    # ---- per-workload cold-cache report ----
+    if not args.no_report:
+        flush_buf = torch.empty(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
+        flush = lambda: flush_buf.zero_()
+        reps = []
+        for ww in wl.WORKLOADS:
+            log(f"[bench] report {ww.name}")
+            reps.append(report_workload(ww, dev, stream, args.report_runs, flush))
+        out["workloads"] = reps
+        del flush_buf
+        torch.cuda.empty_cache()
+
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle)")
+        out["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,144 @@
+/*
+ * gett.h -- C interface of the MI355X (gfx950) GETT tensor-contraction library.
+ *
+ * The library computes the dense tensor contraction of Sec. 2.2, Eq. 3:
+ *
+ *     C_{Pi_C(I_m u I_n)} <- alpha * A_{Pi_A(I_m u I_k)} * B_{Pi_B(I_n u I_k)}
+ *                            + beta * C_{Pi_C(I_m u I_n)}
+ *
+ * where I_m are the free indices of A (they appear in A and C), I_n the free
+ * indices of B (they appear in B and C) and I_k the contracted indices (they
+ * appear in A and B, not in C).  The sum over I_k is implicit (Einstein
+ * notation, Sec. 2.2).  The method is GETT (Sec. 3): sub-tensors of A and B
+ * are gathered ("packed", Sec. 3.2, Eq. 9-10) into on-chip memory and
+ * multiplied by a GEMM-like macro-kernel (Sec. 3.1, Listing 4); the result is
+ * scaled and written through C's own index permutation (Eq. 11).  No copy of
+ * any operand is made in device memory (Sec. 1: no auxiliary memory).
+ *
+ * Usage: gett_plan() once per contraction shape (host only, makes no HIP
+ * call), gett_contract() any number of times (asynchronous on a stream),
+ * gett_destroy() at the end.
+ *
+ * All functions have C linkage, throw nothing and report errors by status.
+ */
+#ifndef GETT_H
+#define GETT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Maximum number of modes of one tensor. */
+#define GETT_MAX_RANK 12
+
+/* Element type of A, B and C (Table II: --floatType=[s,d]).  Products and
+ * sums are formed in the same type (fp32 or fp64 matrix-core arithmetic). */
+typedef enum {
+    GETT_FLOAT32 = 0,
+    GETT_FLOAT64 = 1
+} gett_dtype_t;
+
+typedef enum {
+    GETT_SUCCESS = 0,
+    /* null pointer, unknown dtype, negative extent, stride < 1, C aliasing
+     * A or B, pointer not aligned to the element size */
+    GETT_ERROR_INVALID_VALUE = 1,
+    /* malformed mode string; an index that appears in only one tensor, in
+     * all three (Sec. 2.2, footnote 9) or twice in one; extents that differ
+     * between tensors */
+    GETT_ERROR_INVALID_INDICES = 2,
+    /* rank above GETT_MAX_RANK; C strides that may map two elements of C to
+     * one address; a tensor whose largest element offset reaches 2^31 */
+    GETT_ERROR_NOT_SUPPORTED = 3,
+    /* a HIP runtime call (kernel launch) failed */
+    GETT_ERROR_HIP = 4,
+    /* host memory allocation failed */
+    GETT_ERROR_ALLOC = 5
+} gett_status_t;
+
+/* Opaque, immutable plan (host memory only). */
+typedef struct gett_plan_s *gett_plan_t;
+
+/* Flags for gett_plan(). */
+#define GETT_FLAG_NONE 0u
+/* Keep A as the row operand of the macro-kernel even when C's stride-one
+ * index belongs to A (by default the operands are exchanged so that C's
+ * stride-one index runs along the macro-kernel's columns, the direction in
+ * which its results are stored contiguously). */
+#define GETT_FLAG_NO_SWAP 1u
+/* Use element-wise gathers for A and B and element-wise C accesses even
+ * where 16-byte vector accesses are possible (a slower reference variant). */
+#define GETT_FLAG_SCALAR 2u
+
+/*
+ * gett_plan -- analyse a contraction and choose its kernel (Sec. 3.2-3.3).
+ *
+ *   plan       out: the new plan; set to NULL on any failure.
+ *   dtype      element type of all three tensors.
+ *   modes_X    index names of tensor X in storage order: comma separated
+ *              ("m1,k1,m2,k2"; a trailing comma marks a single multi-letter
+ *              name, "m1,") or, without commas, one character per index
+ *              ("akc").  Names are labels only; which set an index belongs to
+ *              follows from where it occurs (Sec. 2.2).  "" is a scalar.
+ *   extent_X   extent of each mode of X (>= 0); may be NULL for a scalar.
+ *   stride_X   stride of each mode of X in elements (>= 1), or NULL for the
+ *              Fortran layout of Sec. 2.2 (first index stride-one, dense).
+ *   flags      GETT_FLAG_* bits.
+ *
+ * Extent-1 indices are dropped; consecutive indices of one set that are
+ * adjacent in memory in every tensor holding them are merged into one
+ * super-index (Sec. 6, footnote 18).  An empty I_m, I_n or I_k acts as one
+ * index of extent 1.  A zero extent gives an empty sum (C <- beta * C) or an
+ * empty C.  No HIP call is made; the plan holds no device memory.
+ */
+gett_status_t gett_plan(gett_plan_t *plan, gett_dtype_t dtype,
+                        const char *modes_C, const int64_t *extent_C, const int64_t *stride_C,
+                        const char *modes_A, const int64_t *extent_A, const int64_t *stride_A,
+                        const char *modes_B, const int64_t *extent_B, const int64_t *stride_B,
+                        uint32_t flags);
+
+/*
+ * gett_contract -- C <- alpha * A * B + beta * C on the GPU (Listing 4).
+ *
+ *   plan     a plan from gett_plan().
+ *   alpha    scale of the product (converted to the plan's dtype).
+ *   A, B     device pointers to element [0,...,0] of A and B, laid out as
+ *            the plan's extents and strides describe.  Not read when alpha
+ *            is 0 or the contracted size is 0.
+ *   beta     scale of the old C.  beta == 0: C is not read, so NaN or Inf in
+ *            C does not propagate (BLAS convention).
+ *   C        device pointer to element [0,...,0] of C; must not overlap A
+ *            or B.
+ *   stream   a hipStream_t (NULL: the default stream).
+ *
+ * The call only enqueues work on `stream` and returns; the kernel arguments
+ * are copied at launch, so the plan may be destroyed as soon as the call
+ * returns.  A plan may be used from several host threads and streams at
+ * once.  Pointers must be aligned to the element size; 16-byte aligned
+ * pointers enable vector accesses.
+ */
+gett_status_t gett_contract(const gett_plan_t plan, double alpha, const void *A, const void *B,
+                            double beta, void *C, void *stream);
+
+/* gett_destroy -- free a plan.  NULL is accepted and ignored. */
+gett_status_t gett_destroy(gett_plan_t plan);
+
+/* gett_status_string -- static text for a status code. */
+const char *gett_status_string(gett_status_t status);
+
+/*
+ * gett_plan_describe -- the plan's decisions as a JSON object (static storage
+ * owned by the plan, valid until gett_destroy): index sets, merged
+ * super-indices, operand exchange, loop order, stride-one choices, gather
+ * modes, tile sizes, grid and the flop / byte counts of Eq. 12-14.
+ * Returns "" for NULL.
+ */
+const char *gett_plan_describe(const gett_plan_t plan);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GETT_H */

@@ -1,0 +1,481 @@
+// analyse.cpp -- descriptor analyser: the host-side stand-in for the paper's
+// code generator (Sec. 3.2-3.3, Sec. 6).  Runs once per contraction shape and
+// makes no HIP call.
+//
+//   1. parse and validate the three mode lists (Sec. 2.2, footnote 9);
+//   2. classify indices into I_m, I_n, I_k (Listing 5: I_m = A ∩ C,
+//      I_n = B ∩ C, I_k = A ∩ B);
+//   3. drop extent-1 indices and merge indices of one set that are adjacent
+//      in memory in every tensor holding them into super-indices (Sec. 6,
+//      footnote 18, applied to strides so that it also covers non-dense
+//      views);
+//   4. choose the row and column operands of the macro-kernel: C's
+//      stride-one index goes to the column side, where the kernel stores C
+//      contiguously (the operand exchange of Listing 7, mirrored for the
+//      MFMA result layout);
+//   5. order every set so each operand's stride-one index leads where
+//      possible (Sec. 3.2.1: keep the stride-one index inside the packed
+//      sub-tensor);
+//   6. choose the tile shape and the K box -- a sub-tensor of fixed shape
+//      over the contracted indices, splitting one index into blocks
+//      (Sec. 3.2.1, Examples 1-2: index reinterpretation) -- and the gather
+//      mode of each operand.
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <new>
+#include <sstream>
+
+#include "plan.hpp"
+#include "tiles.hpp"
+
+namespace gett {
+namespace {
+
+gett_status_t parse_modes(const char *s, std::vector<std::string> &out)
+{
+    out.clear();
+    if (!s) return GETT_ERROR_INVALID_VALUE;
+    if (!strchr(s, ',')) {
+        for (const char *p = s; *p; ++p)
+            if (*p != ' ') out.push_back(std::string(1, *p));
+        return GETT_SUCCESS;
+    }
+    std::string cur;
+    for (const char *p = s;; ++p) {
+        if (*p == ',' || *p == 0) {
+            if (cur.empty()) {
+                if (*p == 0 && !out.empty()) break;   // one trailing comma
+                return GETT_ERROR_INVALID_INDICES;
+            }
+            out.push_back(cur);
+            cur.clear();
+            if (*p == 0) break;
+        } else if (*p != ' ') {
+            cur.push_back(*p);
+        }
+    }
+    return GETT_SUCCESS;
+}
+
+struct Tensor {
+    std::vector<std::string> modes;
+    std::vector<int64_t> ext, str;
+    int find(const std::string &n) const
+    {
+        for (size_t i = 0; i < modes.size(); ++i)
+            if (modes[i] == n) return (int)i;
+        return -1;
+    }
+};
+
+gett_status_t load_tensor(const char *m, const int64_t *e, const int64_t *s, Tensor &t)
+{
+    gett_status_t st = parse_modes(m, t.modes);
+    if (st != GETT_SUCCESS) return st;
+    const size_t n = t.modes.size();
+    if (n > GETT_MAX_RANK) return GETT_ERROR_NOT_SUPPORTED;
+    if (n && !e) return GETT_ERROR_INVALID_VALUE;
+    for (size_t i = 0; i < n; ++i)
+        for (size_t j = i + 1; j < n; ++j)
+            if (t.modes[i] == t.modes[j]) return GETT_ERROR_INVALID_INDICES;
+    t.ext.assign(e, e + n);
+    for (int64_t v : t.ext)
+        if (v < 0 || v > INT32_MAX) return GETT_ERROR_INVALID_VALUE;
+    if (s) {
+        t.str.assign(s, s + n);
+    } else {   // Fortran layout: the first index is stride-one (Sec. 2.2)
+        t.str.resize(n);
+        int64_t acc = 1;
+        for (size_t i = 0; i < n; ++i) {
+            t.str[i] = acc;
+            acc *= std::max<int64_t>(t.ext[i], 1);
+        }
+    }
+    for (size_t i = 0; i < n; ++i) {
+        if (t.str[i] < 0) return GETT_ERROR_INVALID_VALUE;
+        if (t.ext[i] > 1 && t.str[i] < 1) return GETT_ERROR_INVALID_VALUE;
+    }
+    return GETT_SUCCESS;
+}
+
+int64_t max_offset(const Tensor &t)
+{
+    int64_t m = 0;
+    for (size_t i = 0; i < t.modes.size(); ++i) {
+        if (t.ext[i] <= 1) continue;
+        if (t.str[i] >= INT32_MAX) return INT64_MAX;
+        m += (t.ext[i] - 1) * t.str[i];
+        if (m >= INT32_MAX) return INT64_MAX;
+    }
+    return m;
+}
+
+// Strides that may send two elements of C to one address are refused:
+// sorted by stride, each index must step over the whole span of the
+// previous ones.
+bool c_is_injective(const Tensor &c)
+{
+    std::vector<std::pair<int64_t, int64_t>> v;   // (stride, extent)
+    for (size_t i = 0; i < c.modes.size(); ++i)
+        if (c.ext[i] > 1) v.push_back({c.str[i], c.ext[i]});
+    std::sort(v.begin(), v.end());
+    int64_t span = 1;   // one past the largest offset reachable so far
+    for (auto &p : v) {
+        if (p.first < span) return false;
+        span = p.first * (p.second - 1) + span;
+    }
+    return true;
+}
+
+// Merge p then q (p fastest) when q follows p in memory in every tensor that
+// holds them (Sec. 6, footnote 18).
+void merge_set(std::vector<Index> &set, bool useA, bool useB, bool useC,
+               std::vector<std::string> &log)
+{
+    bool changed = true;
+    while (changed) {
+        changed = false;
+        for (size_t p = 0; p < set.size() && !changed; ++p)
+            for (size_t q = 0; q < set.size() && !changed; ++q) {
+                if (p == q) continue;
+                const Index &P = set[p], &Q = set[q];
+                auto follows = [&](int64_t sp, int64_t sq) { return sq == sp * P.extent; };
+                if (useA && !follows(P.strA, Q.strA)) continue;
+                if (useB && !follows(P.strB, Q.strB)) continue;
+                if (useC && !follows(P.strC, Q.strC)) continue;
+                Index M = P;
+                M.name = "(" + P.name + "," + Q.name + ")";
+                M.extent = P.extent * Q.extent;
+                log.push_back(M.name);
+                set[p] = M;
+                set.erase(set.begin() + q);
+                changed = true;
+            }
+    }
+}
+
+const TileShape &tile_shape(gett_dtype_t dt, int t)
+{
+    return dt == GETT_FLOAT32 ? kTilesF32[t] : kTilesF64[t];
+}
+int num_tiles(gett_dtype_t dt) { return dt == GETT_FLOAT32 ? kNumTilesF32 : kNumTilesF64; }
+
+void json_set(std::ostringstream &o, const char *key, const std::vector<Index> &set, bool A, bool B,
+              bool C)
+{
+    o << "\"" << key << "\":[";
+    for (size_t i = 0; i < set.size(); ++i) {
+        const Index &x = set[i];
+        o << (i ? "," : "") << "{\"name\":\"" << x.name << "\",\"extent\":" << x.extent;
+        if (A) o << ",\"strideA\":" << x.strA;
+        if (B) o << ",\"strideB\":" << x.strB;
+        if (C) o << ",\"strideC\":" << x.strC;
+        o << "}";
+    }
+    o << "]";
+}
+
+const char *mode_name(int m)
+{
+    return m == kGatherRowVec ? "row-vector" : m == kGatherKVec ? "k-vector" : "scalar";
+}
+
+}  // namespace
+
+gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, const int64_t *eC,
+                      const int64_t *sC, const char *mA, const int64_t *eA, const int64_t *sA,
+                      const char *mB, const int64_t *eB, const int64_t *sB, uint32_t flags)
+{
+    if (dtype != GETT_FLOAT32 && dtype != GETT_FLOAT64) return GETT_ERROR_INVALID_VALUE;
+    Tensor A, B, C;
+    gett_status_t st;
+    if ((st = load_tensor(mC, eC, sC, C)) != GETT_SUCCESS) return st;
+    if ((st = load_tensor(mA, eA, sA, A)) != GETT_SUCCESS) return st;
+    if ((st = load_tensor(mB, eB, sB, B)) != GETT_SUCCESS) return st;
+
+    Analysis an;
+    // ---- classification (Sec. 2.2; Listing 5: the three intersections) ----
+    for (size_t i = 0; i < C.modes.size(); ++i) {
+        const int ia = A.find(C.modes[i]), ib = B.find(C.modes[i]);
+        if ((ia >= 0) == (ib >= 0)) return GETT_ERROR_INVALID_INDICES;   // in both or neither
+        Index x;
+        x.name = C.modes[i];
+        x.extent = C.ext[i];
+        x.strC = C.str[i];
+        if (ia >= 0) {
+            if (A.ext[ia] != C.ext[i]) return GETT_ERROR_INVALID_INDICES;
+            x.strA = A.str[ia];
+            an.Im.push_back(x);
+        } else {
+            if (B.ext[ib] != C.ext[i]) return GETT_ERROR_INVALID_INDICES;
+            x.strB = B.str[ib];
+            an.In.push_back(x);
+        }
+    }
+    for (size_t i = 0; i < A.modes.size(); ++i) {
+        if (C.find(A.modes[i]) >= 0) continue;
+        const int ib = B.find(A.modes[i]);
+        if (ib < 0) return GETT_ERROR_INVALID_INDICES;
+        if (B.ext[ib] != A.ext[i]) return GETT_ERROR_INVALID_INDICES;
+        Index x;
+        x.name = A.modes[i];
+        x.extent = A.ext[i];
+        x.strA = A.str[i];
+        x.strB = B.str[ib];
+        an.Ik.push_back(x);
+    }
+    for (size_t i = 0; i < B.modes.size(); ++i)
+        if (C.find(B.modes[i]) < 0 && A.find(B.modes[i]) < 0) return GETT_ERROR_INVALID_INDICES;
+
+    an.maxOffA = max_offset(A);
+    an.maxOffB = max_offset(B);
+    an.maxOffC = max_offset(C);
+    if (an.maxOffA >= INT32_MAX || an.maxOffB >= INT32_MAX || an.maxOffC >= INT32_MAX)
+        return GETT_ERROR_NOT_SUPPORTED;
+    if (!c_is_injective(C)) return GETT_ERROR_NOT_SUPPORTED;
+
+    for (auto &x : an.Im) { an.sizeM *= x.extent; }
+    for (auto &x : an.In) { an.sizeN *= x.extent; }
+    for (auto &x : an.Ik) { an.sizeK *= x.extent; }
+    an.emptyC = an.sizeM == 0 || an.sizeN == 0;
+    an.emptySum = an.sizeK == 0;
+
+    // ---- drop extent-1 indices, merge (footnote 18) ----
+    auto drop1 = [](std::vector<Index> &s) {
+        s.erase(std::remove_if(s.begin(), s.end(), [](const Index &x) { return x.extent == 1; }),
+                s.end());
+    };
+    drop1(an.Im);
+    drop1(an.In);
+    drop1(an.Ik);
+    if (!an.emptyC && !an.emptySum) {
+        merge_set(an.Im, true, false, true, an.merges);
+        merge_set(an.In, false, true, true, an.merges);
+        merge_set(an.Ik, true, true, false, an.merges);
+    }
+
+    // ---- operand roles: C's stride-one index on the column (y) side ----
+    bool swap = false;
+    {
+        int64_t best = INT64_MAX;
+        int where = 0;   // 1: I_m, 2: I_n
+        for (auto &x : an.Im)
+            if (x.strC < best) { best = x.strC; where = 1; }
+        for (auto &x : an.In)
+            if (x.strC < best) { best = x.strC; where = 2; }
+        swap = where == 1 && !(flags & GETT_FLAG_NO_SWAP);
+    }
+    an.swapped = swap;
+    std::vector<Index> Ix = swap ? an.In : an.Im;
+    std::vector<Index> Iy = swap ? an.Im : an.In;
+    std::vector<Index> Ik = an.Ik;
+    auto sX = [swap](const Index &x) { return swap ? x.strB : x.strA; };
+    auto sY = [swap](const Index &x) { return swap ? x.strA : x.strB; };
+
+    // ---- loop orders (stride-one index first where it helps) ----
+    std::stable_sort(Iy.begin(), Iy.end(), [](const Index &a, const Index &b) { return a.strC < b.strC; });
+    std::stable_sort(Ix.begin(), Ix.end(), [&](const Index &a, const Index &b) { return sX(a) < sX(b); });
+    {
+        int64_t minX = INT64_MAX, minY = INT64_MAX;
+        bool xInK = false, yInK = false;
+        for (auto &x : Ix) if (sX(x) < minX) { minX = sX(x); xInK = false; }
+        for (auto &x : Ik) if (sX(x) < minX) { minX = sX(x); xInK = true; }
+        for (auto &x : Iy) if (sY(x) < minY) { minY = sY(x); yInK = false; }
+        for (auto &x : Ik) if (sY(x) < minY) { minY = sY(x); yInK = true; }
+        const bool byY = !xInK && yInK;
+        std::stable_sort(Ik.begin(), Ik.end(), [&](const Index &a, const Index &b) {
+            return byY ? sY(a) < sY(b) : sX(a) < sX(b);
+        });
+    }
+    // An empty set acts as one index of extent 1 (Sec. 2.2 assumes non-empty sets).
+    auto virt = [](std::vector<Index> &s) {
+        if (s.empty()) {
+            Index v;
+            v.name = "1";
+            s.push_back(v);
+        }
+    };
+    virt(Ix);
+    virt(Iy);
+    virt(Ik);
+    if ((int)Ix.size() > kMaxDims || (int)Iy.size() > kMaxDims || (int)Ik.size() > kMaxDims)
+        return GETT_ERROR_NOT_SUPPORTED;
+
+    // ---- tile shape ----
+    const int VW = dtype == GETT_FLOAT32 ? 4 : 2;
+    const int64_t sizeX = swap ? an.sizeN : an.sizeM;
+    const int64_t sizeY = swap ? an.sizeM : an.sizeN;
+    int tile = 0;
+    {
+        const TileShape &t0 = tile_shape(dtype, 0);
+        const int64_t wg0 = ((sizeX + t0.mt - 1) / t0.mt) * ((sizeY + t0.nt - 1) / t0.nt);
+        if (wg0 < 256 && num_tiles(dtype) > 1) tile = 1;
+    }
+    const TileShape &ts = tile_shape(dtype, tile);
+
+    // ---- K box: whole leading contracted indices, then a block of one ----
+    int kj = 0;
+    int64_t prefix = 1;
+    const int nk = (int)Ik.size();
+    while (kj < nk - 1 && prefix * Ik[kj].extent <= ts.kt) {
+        prefix *= Ik[kj].extent;
+        ++kj;
+    }
+    int64_t tj = std::min<int64_t>(Ik[kj].extent, ts.kt / prefix);
+    if (tj < 1) tj = 1;
+    // Prefer a block length that divides the index (no ragged last block)
+    // unless that would lose more than half of the box.
+    {
+        int64_t best = tj;
+        for (int64_t t = tj; t >= 1; --t)
+            if (Ik[kj].extent % t == 0) { best = t; break; }
+        if (best * 2 > tj) tj = best;
+    }
+    // A contracted stride-one run gathered as vectors needs whole vectors per block.
+    auto kvec_ok = [&](auto strOf) {
+        if (strOf(Ik[0]) != 1) return false;
+        if (Ik[0].extent % VW) return false;
+        for (size_t i = 1; i < Ik.size(); ++i)
+            if (strOf(Ik[i]) % VW) return false;
+        return true;
+    };
+    const bool wantKvec = !(flags & GETT_FLAG_SCALAR) && (kvec_ok(sX) || kvec_ok(sY));
+    if (wantKvec && kj == 0 && tj % VW) {
+        const int64_t t2 = (tj / VW) * VW;
+        if (t2 >= VW) {
+            tj = t2;
+            while (Ik[0].extent % tj && tj > VW) tj -= VW;   // keep it dividing when possible
+        }
+    }
+    const int64_t kbox = prefix * tj;
+    const int64_t nblk = (Ik[kj].extent + tj - 1) / tj;
+    int64_t nsteps = nblk;
+    for (int i = kj + 1; i < nk; ++i) nsteps *= Ik[i].extent;
+    if (an.emptySum) nsteps = 0;
+
+    // ---- gather modes ----
+    auto row_vec_ok = [&](const std::vector<Index> &I, auto strOf) {
+        if (strOf(I[0]) != 1 || I[0].extent % VW) return false;
+        for (size_t i = 1; i < I.size(); ++i)
+            if (strOf(I[i]) % VW) return false;
+        for (auto &k : Ik)
+            if (strOf(k) % VW) return false;
+        return true;
+    };
+    auto k_vec_ok = [&](const std::vector<Index> &I, auto strOf) {
+        if (!kvec_ok(strOf)) return false;
+        if (kj == 0 && (tj % VW)) return false;
+        for (auto &x : I)
+            if (strOf(x) % VW) return false;
+        return true;
+    };
+    int xmode = kGatherScalar, ymode = kGatherScalar;
+    if (!(flags & GETT_FLAG_SCALAR)) {
+        if (row_vec_ok(Ix, sX)) xmode = kGatherRowVec;
+        else if (k_vec_ok(Ix, sX)) xmode = kGatherKVec;
+        if (row_vec_ok(Iy, sY)) ymode = kGatherRowVec;
+        else if (k_vec_ok(Iy, sY)) ymode = kGatherKVec;
+    }
+    bool cvec = !(flags & GETT_FLAG_SCALAR) && Iy[0].strC == 1 && Iy[0].extent % VW == 0;
+    for (auto &x : Ix) if (x.strC % VW) cvec = false;
+    for (size_t i = 1; i < Iy.size(); ++i) if (Iy[i].strC % VW) cvec = false;
+
+    // ---- descriptor ----
+    KDesc d;
+    memset(&d, 0, sizeof(d));
+    d.sizeX = sizeX;
+    d.sizeY = sizeY;
+    d.nx = (int)Ix.size();
+    d.ny = (int)Iy.size();
+    for (int i = 0; i < d.nx; ++i) {
+        d.extX[i] = (int32_t)Ix[i].extent;
+        d.strXop[i] = sX(Ix[i]);
+        d.strCx[i] = Ix[i].strC;
+    }
+    for (int i = 0; i < d.ny; ++i) {
+        d.extY[i] = (int32_t)Iy[i].extent;
+        d.strYop[i] = sY(Iy[i]);
+        d.strCy[i] = Iy[i].strC;
+    }
+    d.nk = nk;
+    for (int i = 0; i < nk; ++i) {
+        d.extK[i] = (int32_t)Ik[i].extent;
+        d.strXk[i] = sX(Ik[i]);
+        d.strYk[i] = sY(Ik[i]);
+    }
+    d.kj = kj;
+    d.tj = (int32_t)tj;
+    d.kbox = (int32_t)kbox;
+    d.nblk = (int32_t)std::max<int64_t>(nblk, 1);
+    d.nsteps = nsteps;
+    const int64_t tilesX = (sizeX + ts.mt - 1) / ts.mt;
+    const int64_t tilesY = (sizeY + ts.nt - 1) / ts.nt;
+    if (!an.emptyC && (tilesX * tilesY * ts.wm * ts.wn * 64 >= (int64_t)UINT32_MAX || sizeX >= INT32_MAX ||
+                       sizeY >= INT32_MAX || nsteps >= INT32_MAX))
+        return GETT_ERROR_NOT_SUPPORTED;
+    d.tilesX = (int32_t)tilesX;
+    d.tilesY = (int32_t)tilesY;
+    d.group = (int32_t)std::max<int64_t>(1, std::min<int64_t>(8, tilesX));
+    d.cvec = cvec ? 1 : 0;
+    d.xscalar_kfast = sX(Ik[0]) < sX(Ix[0]) ? 1 : 0;
+    d.yscalar_kfast = sY(Ik[0]) < sY(Iy[0]) ? 1 : 0;
+
+    plan.dtype = dtype;
+    plan.flags = flags;
+    plan.an = an;
+    plan.desc = d;
+    plan.descScalar = d;
+    plan.descScalar.cvec = 0;
+    plan.tile = tile;
+    plan.xmode = xmode;
+    plan.ymode = ymode;
+    const double item = dtype == GETT_FLOAT32 ? 4.0 : 8.0;
+    plan.flops = 2.0 * (double)an.sizeM * (double)an.sizeN * (double)an.sizeK;
+    const double nA = (double)an.sizeM * an.sizeK, nB = (double)an.sizeN * an.sizeK,
+                 nC = (double)an.sizeM * an.sizeN;
+    plan.bytesAlgo = item * (nA + nB + nC);
+
+    // ---- description ----
+    std::ostringstream o;
+    o << "{\"dtype\":\"" << (dtype == GETT_FLOAT32 ? "f32" : "f64") << "\",";
+    json_set(o, "I_m", an.Im, true, false, true);
+    o << ",";
+    json_set(o, "I_n", an.In, false, true, true);
+    o << ",";
+    json_set(o, "I_k", an.Ik, true, true, false);
+    o << ",\"merges\":[";
+    for (size_t i = 0; i < an.merges.size(); ++i) o << (i ? "," : "") << "\"" << an.merges[i] << "\"";
+    o << "],\"swapped\":" << (swap ? "true" : "false");
+    o << ",\"row_operand\":\"" << (swap ? "B" : "A") << "\",\"col_operand\":\"" << (swap ? "A" : "B")
+      << "\"";
+    auto names = [&](const char *key, const std::vector<Index> &s) {
+        o << ",\"" << key << "\":[";
+        for (size_t i = 0; i < s.size(); ++i) o << (i ? "," : "") << "\"" << s[i].name << "\"";
+        o << "]";
+    };
+    names("x_order", Ix);
+    names("y_order", Iy);
+    names("k_order", Ik);
+    o << ",\"size_x\":" << sizeX << ",\"size_y\":" << sizeY << ",\"size_k\":" << an.sizeK;
+    o << ",\"tile\":{\"id\":" << tile << ",\"mt\":" << ts.mt << ",\"nt\":" << ts.nt << ",\"kt\":" << ts.kt
+      << ",\"waves\":[" << ts.wm << "," << ts.wn << "]}";
+    o << ",\"kbox\":{\"kj\":" << kj << ",\"tj\":" << tj << ",\"elements\":" << kbox << ",\"blocks\":" << nblk
+      << ",\"steps\":" << nsteps << "}";
+    o << ",\"gather_x\":\"" << mode_name(xmode) << "\",\"gather_y\":\"" << mode_name(ymode)
+      << "\",\"c_vector\":" << (cvec ? "true" : "false");
+    o << ",\"grid\":{\"tiles_x\":" << tilesX << ",\"tiles_y\":" << tilesY << ",\"workgroups\":"
+      << tilesX * tilesY << ",\"threads\":" << ts.wm * ts.wn * 64 << "}";
+    o << ",\"empty_c\":" << (an.emptyC ? "true" : "false") << ",\"empty_sum\":"
+      << (an.emptySum ? "true" : "false");
+    char buf[64];
+    snprintf(buf, sizeof buf, "%.17g", plan.flops);
+    o << ",\"flops\":" << buf;
+    snprintf(buf, sizeof buf, "%.17g", plan.bytesAlgo);
+    o << ",\"bytes_min\":" << buf << "}";
+    plan.text = o.str();
+    return GETT_SUCCESS;
+}
+
+}  // namespace gett

@@ -1,0 +1,386 @@
+// kernel.hpp -- the GETT macro-kernel for gfx950 (device code).
+//
+// One workgroup computes an MT x NT tile of the matrix view C[x][y]
+// (Listing 4: the grid replaces the n- and m-loops (1) and (4); the in-kernel
+// loop over K boxes is the k-loop (2)).  Per K box:
+//   pack   -- X's MT x kbox sub-tensor and Y's NT x kbox sub-tensor are
+//             gathered from device memory straight into LDS (Eq. 9-10: the
+//             packing is a transposition into a fixed layout [k][row]); the
+//             loads run along each operand's stride-one index;
+//   macro  -- every wavefront multiplies its part of the packed tiles with
+//             MFMA 16x16x4 instructions, accumulating in registers (the
+//             register-resident C~ of Sec. 3.1);
+// and after the last box
+//   unpack -- C(x,y) <- alpha * acc + beta * C(x,y) through C's own strides
+//             (Eq. 11); C is not read when beta == 0.
+//
+// Register tile of a wavefront.  Lane l (l16 = l % 16, g = l / 16) of an
+// MFMA 16x16x4 supplies row l16 of the A-operand and column l16 of the
+// B-operand at contracted position g, and receives results for rows
+// 4g..4g+3 of column l16.  The kernel lets one 16-byte LDS read per lane
+// feed VW blocks at once (VW = 4 for fp32, 2 for fp64): within a group of
+// 16*VW rows, MFMA row r of block i is tile row VW*r + i (same for columns).
+// A lane then owns VW consecutive columns of C for each of its rows, which
+// the epilogue writes as one 16-byte vector; with the operands arranged so
+// that C's stride-one index runs along y, 16 lanes store 256 contiguous bytes.
+// The contracted positions used by lane group g at MFMA step s are
+// 4s + g for both operands, so each product pairs matching indices.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "desc.hpp"
+
+namespace gett {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef double f64x2 __attribute__((ext_vector_type(2)));
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+template <typename T> struct Traits;
+template <> struct Traits<float> {
+    typedef f32x4 vec;   // 16-byte vector
+    typedef f32x4 acc;   // 16x16 MFMA accumulator slice of one lane
+    static constexpr int VW = 4;
+};
+template <> struct Traits<double> {
+    typedef f64x2 vec;
+    typedef f64x4 acc;
+    static constexpr int VW = 2;
+};
+
+__device__ __forceinline__ f32x4 mfma16x16x4(float a, float b, f32x4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f64x4 mfma16x16x4(double a, double b, f64x4 c)
+{
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+
+constexpr int kInvalidK = 0x7fffffff;
+
+// Map the hardware workgroup id to a tile.  Workgroups are dealt round-robin
+// to the 8 XCDs (each with its own L2); renumber so that consecutive logical
+// tiles run on one XCD, then walk tiles in bands of `group` x-tiles so that
+// neighbours share operand rows/columns in L2.
+__device__ __forceinline__ void tile_of_block(const KDesc &d, int &tx, int &ty)
+{
+    const int nwg = (int)gridDim.x;
+    const int bid = (int)blockIdx.x;
+    const int full = nwg & ~7;
+    int logical = bid;
+    if (bid < full) logical = (bid & 7) * (full >> 3) + (bid >> 3);
+    const int band = d.group * d.tilesY;
+    const int first = (logical / band) * d.group;
+    const int gsz = min(d.tilesX - first, d.group);
+    const int in = logical - (logical / band) * band;
+    tx = first + in % gsz;
+    ty = in / gsz;
+}
+
+// Origin of K box `s`: block `s % nblk` of index kj, then one point of each
+// later contracted index (first one fastest).  Returns the origin offsets in
+// X and Y and the number of valid positions left along index kj.
+__device__ __forceinline__ int box_origin(const KDesc &d, uint32_t s, int64_t &ox, int64_t &oy)
+{
+    const uint32_t nb = (uint32_t)d.nblk;
+    const uint32_t rest0 = s / nb;
+    const int blk = (int)(s - rest0 * nb);
+    uint32_t rest = rest0;
+    ox = (int64_t)blk * d.tj * d.strXk[d.kj];
+    oy = (int64_t)blk * d.tj * d.strYk[d.kj];
+    for (int i = d.kj + 1; i < d.nk; ++i) {
+        const uint32_t e = (uint32_t)d.extK[i];
+        const uint32_t q = rest / e;
+        const uint32_t c = rest - q * e;
+        rest = q;
+        ox += (int64_t)c * d.strXk[i];
+        oy += (int64_t)c * d.strYk[i];
+    }
+    return d.extK[d.kj] - blk * d.tj;
+}
+
+// Per-thread description of the part of one operand tile it gathers.
+template <typename T, int ROWS, int KT, int MODE, int NTH>
+struct Gather {
+    static constexpr int VW = Traits<T>::VW;
+    static constexpr int PITCH = ROWS + VW;   // LDS row pitch (elements) of the [k][row] layout
+    static constexpr int W = (MODE == kGatherScalar) ? 1 : VW;
+    static constexpr int ITEMS = ROWS * KT / W;
+    static constexpr int NI = ITEMS / NTH;
+    static_assert(ITEMS % NTH == 0, "tile must split evenly over the workgroup");
+    typedef typename Traits<T>::vec vec;
+
+    int64_t goff[NI];   // element offset in the operand (without the box origin)
+    int kc[NI];         // position along index kj inside the box; kInvalidK: never valid
+    int lds[NI];        // destination element in the LDS tile
+    T val[NI][W];       // staged values
+
+    // rowoff: LDS table of operand offsets per tile row (-1 = outside the tensor)
+    // koff/kco: LDS tables of offsets / kj-positions per box element
+    __device__ __forceinline__ void setup(int tid, const int64_t *rowoff, const int64_t *koff,
+                                          const int *kco, int kfast)
+    {
+#pragma unroll
+        for (int it = 0; it < NI; ++it) {
+            const int i = tid + it * NTH;
+            int r, kk;
+            if (MODE == kGatherRowVec) {
+                r = (i % (ROWS / VW)) * VW;
+                kk = i / (ROWS / VW);
+            } else if (MODE == kGatherKVec) {
+                kk = (i % (KT / VW)) * VW;
+                r = i / (KT / VW);
+            } else if (kfast) {
+                kk = i % KT;
+                r = i / KT;
+            } else {
+                r = i % ROWS;
+                kk = i / ROWS;
+            }
+            const int64_t ro = rowoff[r];
+            goff[it] = (ro < 0 ? 0 : ro) + koff[kk];
+            kc[it] = ro < 0 ? kInvalidK : kco[kk];
+            lds[it] = kk * PITCH + r;
+        }
+    }
+
+    __device__ __forceinline__ void load(const T *__restrict__ p, int64_t base, int limit)
+    {
+#pragma unroll
+        for (int it = 0; it < NI; ++it) {
+            if (kc[it] < limit) {
+                if (W == 1) {
+                    val[it][0] = p[base + goff[it]];
+                } else {
+                    const vec v = *reinterpret_cast<const vec *>(p + base + goff[it]);
+#pragma unroll
+                    for (int e = 0; e < W; ++e) val[it][e] = v[e];
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < W; ++e) val[it][e] = T(0);
+            }
+        }
+    }
+
+    __device__ __forceinline__ void store(T *tile) const
+    {
+#pragma unroll
+        for (int it = 0; it < NI; ++it) {
+            if (MODE == kGatherRowVec) {
+                vec v;
+#pragma unroll
+                for (int e = 0; e < W; ++e) v[e] = val[it][e];
+                *reinterpret_cast<vec *>(tile + lds[it]) = v;
+            } else if (MODE == kGatherKVec) {
+#pragma unroll
+                for (int e = 0; e < W; ++e) tile[lds[it] + e * PITCH] = val[it][e];
+            } else {
+                tile[lds[it]] = val[it][0];
+            }
+        }
+    }
+};
+
+template <typename T, int MT, int NT, int KT, int WM, int WN, int XMODE, int YMODE>
+__global__ void __launch_bounds__(WM *WN * 64)
+gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
+                  T *__restrict__ C, const T alpha, const T beta)
+{
+    constexpr int NTH = WM * WN * 64;
+    constexpr int VW = Traits<T>::VW;
+    constexpr int WTM = MT / WM;            // wave tile rows
+    constexpr int WTN = NT / WN;            // wave tile columns
+    constexpr int RG = WTM / (16 * VW);     // row groups per wave
+    constexpr int CG = WTN / (16 * VW);     // column groups per wave
+    static_assert(RG >= 1 && CG >= 1 && WTM % (16 * VW) == 0 && WTN % (16 * VW) == 0,
+                  "wave tile must be a multiple of 16*VW in both directions");
+    static_assert(KT % 4 == 0, "K tile must be a multiple of the MFMA depth");
+    typedef Gather<T, MT, KT, XMODE, NTH> GX;
+    typedef Gather<T, NT, KT, YMODE, NTH> GY;
+    typedef typename Traits<T>::vec vec;
+    typedef typename Traits<T>::acc accv;
+
+    __shared__ __attribute__((aligned(16))) T xs[2][KT * GX::PITCH];
+    __shared__ __attribute__((aligned(16))) T ys[2][KT * GY::PITCH];
+    __shared__ int64_t rowX[MT], rowY[NT], offCx[MT], offCy[NT];
+    __shared__ int64_t kX[KT], kY[KT];
+    __shared__ int kco[KT];
+
+    const int tid = (int)threadIdx.x;
+    int tx, ty;
+    tile_of_block(d, tx, ty);
+
+    // ---- identify_subtensor: offsets of this tile's rows, columns, box ----
+    for (int r = tid; r < MT; r += NTH) {
+        uint32_t x = (uint32_t)tx * MT + r;
+        int64_t ox = -1, oc = -1;
+        if ((int64_t)x < d.sizeX) {
+            ox = 0;
+            oc = 0;
+            for (int i = 0; i < d.nx; ++i) {
+                const uint32_t e = (uint32_t)d.extX[i];
+                const uint32_t q = x / e;
+                const uint32_t id = x - q * e;
+                x = q;
+                ox += (int64_t)id * d.strXop[i];
+                oc += (int64_t)id * d.strCx[i];
+            }
+        }
+        rowX[r] = ox;
+        offCx[r] = oc;
+    }
+    for (int r = tid; r < NT; r += NTH) {
+        uint32_t y = (uint32_t)ty * NT + r;
+        int64_t oy = -1, oc = -1;
+        if ((int64_t)y < d.sizeY) {
+            oy = 0;
+            oc = 0;
+            for (int i = 0; i < d.ny; ++i) {
+                const uint32_t e = (uint32_t)d.extY[i];
+                const uint32_t q = y / e;
+                const uint32_t id = y - q * e;
+                y = q;
+                oy += (int64_t)id * d.strYop[i];
+                oc += (int64_t)id * d.strCy[i];
+            }
+        }
+        rowY[r] = oy;
+        offCy[r] = oc;
+    }
+    for (int kk = tid; kk < KT; kk += NTH) {
+        int64_t ox = 0, oy = 0;
+        int pos = kInvalidK;
+        if (kk < d.kbox) {
+            uint32_t k = (uint32_t)kk;
+            for (int i = 0; i < d.kj; ++i) {
+                const uint32_t e = (uint32_t)d.extK[i];
+                const uint32_t q = k / e;
+                const uint32_t id = k - q * e;
+                k = q;
+                ox += (int64_t)id * d.strXk[i];
+                oy += (int64_t)id * d.strYk[i];
+            }
+            pos = (int)k;   // position along index kj, < tj
+            ox += (int64_t)k * d.strXk[d.kj];
+            oy += (int64_t)k * d.strYk[d.kj];
+        }
+        kX[kk] = ox;
+        kY[kk] = oy;
+        kco[kk] = pos;
+    }
+    __syncthreads();
+
+    GX gx;
+    GY gy;
+    gx.setup(tid, rowX, kX, kco, d.xscalar_kfast);
+    gy.setup(tid, rowY, kY, kco, d.yscalar_kfast);
+
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave % WM;
+    const int wn = wave / WM;
+    const int l16 = lane & 15;
+    const int g = lane >> 4;
+
+    accv acc[RG * VW][CG * VW];
+#pragma unroll
+    for (int a = 0; a < RG * VW; ++a)
+#pragma unroll
+        for (int b = 0; b < CG * VW; ++b)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[a][b][r] = T(0);
+
+    const uint32_t nsteps = (uint32_t)d.nsteps;
+    if (nsteps > 0) {
+        int64_t ox, oy;
+        const int lim = box_origin(d, 0, ox, oy);
+        gx.load(X, ox, lim);
+        gy.load(Y, oy, lim);
+        gx.store(xs[0]);
+        gy.store(ys[0]);
+    }
+    __syncthreads();
+
+    for (uint32_t s = 0; s < nsteps; ++s) {
+        const int buf = (int)(s & 1);
+        const bool more = s + 1 < nsteps;
+        if (more) {
+            int64_t ox, oy;
+            const int lim = box_origin(d, s + 1, ox, oy);
+            gx.load(X, ox, lim);
+            gy.load(Y, oy, lim);
+        }
+        const T *xt = xs[buf] + wm * WTM + VW * l16;
+        const T *yt = ys[buf] + wn * WTN + VW * l16;
+#pragma unroll
+        for (int ks = 0; ks < KT / 4; ++ks) {
+            const int k = 4 * ks + g;
+            vec av[RG], bv[CG];
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg)
+                av[rg] = *reinterpret_cast<const vec *>(xt + k * GX::PITCH + rg * 16 * VW);
+#pragma unroll
+            for (int cg = 0; cg < CG; ++cg)
+                bv[cg] = *reinterpret_cast<const vec *>(yt + k * GY::PITCH + cg * 16 * VW);
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+                for (int i = 0; i < VW; ++i)
+#pragma unroll
+                    for (int cg = 0; cg < CG; ++cg)
+#pragma unroll
+                        for (int j = 0; j < VW; ++j)
+                            acc[rg * VW + i][cg * VW + j] =
+                                mfma16x16x4(av[rg][i], bv[cg][j], acc[rg * VW + i][cg * VW + j]);
+        }
+        if (more) {
+            gx.store(xs[buf ^ 1]);
+            gy.store(ys[buf ^ 1]);
+        }
+        __syncthreads();
+    }
+
+    // ---- unpack: C <- alpha * acc + beta * C through C's strides (Eq. 11) ----
+    const bool readC = beta != T(0);
+#pragma unroll
+    for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+        for (int i = 0; i < VW; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int xl = wm * WTM + rg * 16 * VW + VW * (4 * g + r) + i;
+                const int64_t ox = offCx[xl];
+                if (ox < 0) continue;
+#pragma unroll
+                for (int cg = 0; cg < CG; ++cg) {
+                    const int yl = wn * WTN + cg * 16 * VW + VW * l16;
+                    if (d.cvec) {
+                        const int64_t oy = offCy[yl];
+                        if (oy < 0) continue;
+                        T *p = C + ox + oy;
+                        vec cv;
+                        if (readC) cv = *reinterpret_cast<const vec *>(p);
+#pragma unroll
+                        for (int j = 0; j < VW; ++j) {
+                            const T a = alpha * acc[rg * VW + i][cg * VW + j][r];
+                            cv[j] = readC ? a + beta * cv[j] : a;
+                        }
+                        *reinterpret_cast<vec *>(p) = cv;
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < VW; ++j) {
+                            const int64_t oy = offCy[yl + j];
+                            if (oy < 0) continue;
+                            T *p = C + ox + oy;
+                            const T a = alpha * acc[rg * VW + i][cg * VW + j][r];
+                            *p = readC ? a + beta * (*p) : a;
+                        }
+                    }
+                }
+            }
+}
+
+}  // namespace gett

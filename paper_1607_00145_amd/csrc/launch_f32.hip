@@ -1,0 +1,16 @@
+// launch_f32.hip -- fp32 instantiations of the macro-kernel.
+#include "launch.hpp"
+
+namespace gett {
+
+LaunchFn launch_fn_f32(int tile, int xm, int ym)
+{
+    static_assert(kNumTilesF32 == 2, "update the tile switch");
+    switch (tile) {
+    case 0: return pick_modes<float, 0>(xm, ym);
+    case 1: return pick_modes<float, 1>(xm, ym);
+    }
+    return nullptr;
+}
+
+}  // namespace gett

@@ -1,0 +1,16 @@
+// launch_f64.hip -- fp64 instantiations of the macro-kernel.
+#include "launch.hpp"
+
+namespace gett {
+
+LaunchFn launch_fn_f64(int tile, int xm, int ym)
+{
+    static_assert(kNumTilesF64 == 2, "update the tile switch");
+    switch (tile) {
+    case 0: return pick_modes<double, 0>(xm, ym);
+    case 1: return pick_modes<double, 1>(xm, ym);
+    }
+    return nullptr;
+}
+
+}  // namespace gett

@@ -1,0 +1,59 @@
+// plan.hpp -- host-side plan object and the analyser's interface.
+#pragma once
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/gett.h"
+#include "desc.hpp"
+
+namespace gett {
+
+// One (possibly merged) index after analysis.
+struct Index {
+    std::string name;     // "a", or "(a,b)" for a merged super-index
+    int64_t extent = 1;
+    int64_t strA = 0, strB = 0, strC = 0;   // 0 where the tensor lacks the index
+};
+
+struct Analysis {
+    std::vector<Index> Im, In, Ik;   // after dropping extent-1 indices and merging
+    std::vector<std::string> merges; // text of each merge performed
+    bool swapped = false;            // X = B, Y = A
+    int64_t sizeM = 1, sizeN = 1, sizeK = 1;
+    bool emptyC = false;             // some extent of C is 0: nothing to do
+    bool emptySum = false;           // some contracted extent is 0: C <- beta * C
+    int64_t maxOffA = 0, maxOffB = 0, maxOffC = 0;   // largest element offsets
+};
+
+typedef hipError_t (*LaunchFn)(const KDesc &, const void *, const void *, void *, double, double,
+                               hipStream_t);
+
+}  // namespace gett
+
+struct gett_plan_s {
+    gett_dtype_t dtype;
+    uint32_t flags;
+    gett::Analysis an;
+    gett::KDesc desc;        // preferred kernel descriptor
+    gett::KDesc descScalar;  // the same work with scalar gathers and C accesses
+    int tile;                // index into the tile table of the dtype
+    int xmode, ymode;        // gather modes of the preferred kernel
+    double flops;            // 2 * S_Im * S_In * S_Ik (Eq. 14)
+    double bytesAlgo;        // |A| + |B| + |C| (+|C| when beta may be read)
+    std::string text;        // JSON description
+};
+
+namespace gett {
+
+// Analyse and fill a plan; returns a status (the plan is unusable on error).
+gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, const int64_t *eC,
+                      const int64_t *sC, const char *mA, const int64_t *eA, const int64_t *sA,
+                      const char *mB, const int64_t *eB, const int64_t *sB, uint32_t flags);
+
+// Launch table lookup (defined with the kernel instantiations).
+LaunchFn launch_fn(gett_dtype_t dtype, int tile, int xmode, int ymode);
+
+}  // namespace gett

@@ -1,0 +1,229 @@
+"""Host-side tests of the C interface: the library loads, exports every symbol
+the header declares, and the analyser's decisions follow the paper.  No GPU
+call is made here (gett_plan is host-only; contract calls either return
+before any launch or use the launch fault hook)."""
+import json
+import os
+import re
+import subprocess
+import sys
+
+import pytest
+
+import paper_1607_00145_amd as g
+import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+GOLDEN = os.path.join(ROOT, "tests", "golden")
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "gett.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gett_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = g.load_library()
+    names = declared_functions()
+    assert names == sorted(["gett_plan", "gett_contract", "gett_destroy", "gett_status_string",
+                            "gett_plan_describe"])
+    for n in names:
+        assert hasattr(lib, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", g.LIB_PATH], capture_output=True,
+                         text=True).stdout
+    for n in names:
+        assert re.search(rf"\bT {n}\b", out), n
+
+
+def test_binding_has_the_c_names():
+    for n in declared_functions():
+        assert callable(getattr(g, n))
+
+
+def plan(mc, ma, mb, ext, dtype=g.GETT_FLOAT32, strides=(None, None, None), flags=0):
+    sp = lambda m: [x for x in m.split(",") if x] if "," in m else list(m)
+    shp = lambda m: [ext[x] for x in sp(m)]
+    st, h = g.gett_plan(dtype, mc, shp(mc), strides[0], ma, shp(ma), strides[1], mb, shp(mb),
+                        strides[2], flags)
+    return st, h
+
+
+def describe(*a, **k):
+    st, h = plan(*a, **k)
+    assert st == 0, g.gett_status_string(st)
+    d = json.loads(g.gett_plan_describe(h))
+    g.gett_destroy(h)
+    return d
+
+
+def test_paper_index_sets():
+    """The analyser's I_m / I_n / I_k for every example the paper gives."""
+    cases = json.load(open(os.path.join(GOLDEN, "index_sets.json")))["cases"]
+    for cs in cases:
+        sp = lambda m: [x for x in m.split(",") if x] if "," in m else list(m)
+        names = set(sp(cs["C"])) | set(sp(cs["A"])) | set(sp(cs["B"]))
+        ext = {n: 3 + i for i, n in enumerate(sorted(names))}   # distinct extents: no merging
+        # strided layouts with gaps so that nothing merges either
+        strides = []
+        for m in (cs["C"], cs["A"], cs["B"]):
+            s, acc = [], 1
+            for n in sp(m):
+                s.append(acc)
+                acc *= ext[n] + 1
+            strides.append(s)
+        d = describe(cs["C"], cs["A"], cs["B"], ext, strides=tuple(strides))
+        got = lambda key: sorted(x["name"] for x in d[key])
+        assert got("I_m") == sorted(cs["I_m"]), cs["cite"]
+        assert got("I_n") == sorted(cs["I_n"]), cs["cite"]
+        assert got("I_k") == sorted(cs["I_k"]), cs["cite"]
+
+
+def test_listing8_super_indices():
+    """Sec. 5, Listing 8: for C_abcijk = A_ijmc B_mkab (all 24) the indices a,b
+    and i,j merge into super-indices of 576 with the listing's strides."""
+    gold = json.load(open(os.path.join(GOLDEN, "listing8_log.json")))
+    n = gold["contraction"]["extent"]
+    d = describe("abcijk", "ijmc", "mkab", {m: n for m in "abcijkm"})
+    assert sorted(d["merges"]) == ["(a,b)", "(i,j)"]
+    byname = {x["name"]: x for x in d["I_m"] + d["I_n"] + d["I_k"]}
+    assert byname["(a,b)"]["extent"] == gold["super_indices"]["ab"]
+    assert byname["(i,j)"]["extent"] == gold["super_indices"]["ij"]
+    # leading dimensions of the listing's GEMM: B's (a,b) stride, A's m stride, C's (i,j) stride
+    assert byname["(a,b)"]["strideB"] == gold["leading_dims"]["lda_on_B"]
+    assert byname["m"]["strideA"] == gold["leading_dims"]["ldb_on_A"]
+    assert byname["(i,j)"]["strideC"] == gold["leading_dims"]["ldc"]
+    # per-loop offsets of the looped indices c and k
+    assert byname["c"]["strideA"] == gold["offsets"]["A_per_c"]
+    assert byname["c"]["strideC"] == gold["offsets"]["C_per_c"]
+    assert byname["k"]["strideB"] == gold["offsets"]["B_per_k"]
+    assert byname["k"]["strideC"] == gold["offsets"]["C_per_k"]
+    assert d["size_k"] == gold["gemm"]["k"]
+
+
+def test_listing6_is_not_merged():
+    """Sec. 4, Listing 6: a and c are consecutive in A (a,c,k) but not in C
+    (a,b,c), so the super-index merge of footnote 18 must not join them."""
+    d = describe("abc", "ack", "bk", {m: 8 for m in "abck"})
+    assert d["merges"] == []
+
+
+def test_workload_plans():
+    """The decisions for the five workloads (C's stride-one index on the
+    column side; merges of the 6D case; vector gathers along stride-one runs)."""
+    exp = {
+        1: dict(swapped=True, merges=[], gx="k-vector", gy="row-vector"),
+        2: dict(swapped=True, merges=[], gx="k-vector", gy="row-vector"),
+        3: dict(swapped=False, merges=[], gx="row-vector", gy="k-vector"),
+        4: dict(swapped=True, merges=["(a,b)", "(j,k)"], gx="row-vector", gy="k-vector"),
+        5: dict(swapped=True, merges=[], gx="k-vector", gy="row-vector"),
+    }
+    for w in wl.WORKLOADS:
+        dt = g.GETT_FLOAT32 if w.dtype == "f32" else g.GETT_FLOAT64
+        d = describe(w.modes_C, w.modes_A, w.modes_B, w.extents, dtype=dt)
+        e = exp[w.number]
+        assert d["swapped"] == e["swapped"], w.name
+        assert sorted(d["merges"]) == e["merges"], w.name
+        assert d["gather_x"] == e["gx"] and d["gather_y"] == e["gy"], w.name
+        assert d["c_vector"] is True
+        assert d["flops"] == wl.flop_count(w)
+        # C's stride-one index leads the column order
+        first_y = d["y_order"][0]
+        strides = {x["name"]: x["strideC"] for x in d["I_m"] + d["I_n"]}
+        assert strides[first_y] == 1
+
+
+def test_flags_change_the_plan():
+    w = wl.WORKLOADS[4]
+    d0 = describe(w.modes_C, w.modes_A, w.modes_B, w.extents)
+    d1 = describe(w.modes_C, w.modes_A, w.modes_B, w.extents, flags=g.GETT_FLAG_NO_SWAP)
+    d2 = describe(w.modes_C, w.modes_A, w.modes_B, w.extents, flags=g.GETT_FLAG_SCALAR)
+    assert d0["swapped"] and not d1["swapped"]
+    assert d2["gather_x"] == d2["gather_y"] == "scalar" and d2["c_vector"] is False
+
+
+def test_kbox_covers_contracted_set():
+    """K boxes tile the contracted index space: steps * box >= S_Ik with the
+    block split of one index (index reinterpretation, Sec. 3.2.1)."""
+    for ext_k in [(7,), (24,), (48, 48), (3, 5, 2), (64, 64), (1,)]:
+        names = [f"k{i}" for i in range(len(ext_k))]
+        ext = {"m": 9, "n": 10, **dict(zip(names, ext_k))}
+        d = describe("m,n", ",".join(["m"] + names), ",".join(names + ["n"]), ext)
+        kb = d["kbox"]
+        tot = 1
+        for e in ext_k:
+            tot *= e
+        assert kb["steps"] * kb["elements"] >= tot
+        assert kb["elements"] <= d["tile"]["kt"]
+
+
+@pytest.mark.parametrize("mc,ma,mb,code", [
+    ("m,n,b", "m,k,b", "k,n,b", 2),     # batch index in all three (fn. 9)
+    ("m,n", "m,k", "n", 2),             # k only in A
+    ("m,n,z", "m,k", "k,n", 2),         # z only in C
+    ("m,n", "m,m,k", "k,n", 2),         # repeated index
+    ("m,n", "m,,k", "k,n", 2),          # empty name
+])
+def test_invalid_indices(mc, ma, mb, code):
+    sp = lambda m: [x for x in m.split(",") if x]
+    st, h = g.gett_plan(0, mc, [2] * len(sp(mc)), None, ma, [2] * len(sp(ma)), None, mb,
+                        [2] * len(sp(mb)), None, 0)
+    assert st == code and h is None
+
+
+def test_invalid_values_and_unsupported():
+    st, _ = g.gett_plan(7, "m,n", [2, 2], None, "m,k", [2, 2], None, "k,n", [2, 2], None)
+    assert st == 1                                                  # bad dtype
+    st, _ = g.gett_plan(0, "m,n", [2, 3], None, "m,k", [2, 2], None, "k,n", [2, 2], None)
+    assert st == 2                                                  # extent mismatch
+    st, _ = g.gett_plan(0, "m,n", [-1, 2], None, "m,k", [-1, 2], None, "k,n", [2, 2], None)
+    assert st == 1                                                  # negative extent
+    st, _ = g.gett_plan(0, "m,n", [4, 4], [1, 2], "m,k", [4, 2], None, "k,n", [2, 4], None)
+    assert st == 3                                                  # overlapping C
+    st, _ = g.gett_plan(0, "m,n", [4, 4], [0, 4], "m,k", [4, 2], None, "k,n", [2, 4], None)
+    assert st == 1                                                  # zero stride
+    big = 1 << 16
+    st, _ = g.gett_plan(0, "m,n", [big, big], None, "m,k", [big, 2], None, "k,n", [2, big], None)
+    assert st == 3                                                  # C offsets beyond 2^31
+    modes = ",".join(f"i{i}" for i in range(13))
+    st, _ = g.gett_plan(0, modes, [1] * 13, None, "k,", [1], None, "k,", [1], None)
+    assert st == 3                                                  # rank > GETT_MAX_RANK
+
+
+def test_contract_host_side_errors():
+    st, h = plan("m,n", "m,k", "k,n", {"m": 8, "n": 8, "k": 8})
+    assert st == 0
+    assert g.gett_contract(None, 1.0, 0x1000, 0x2000, 0.0, 0x3000) == 1   # null plan
+    assert g.gett_contract(h, 1.0, 0x1000, 0x2000, 0.0, 0) == 1           # null C
+    assert g.gett_contract(h, 1.0, 0, 0x2000, 0.0, 0x3000) == 1           # null A
+    assert g.gett_contract(h, 1.0, 0x1001, 0x2000, 0.0, 0x3000) == 1      # misaligned
+    assert g.gett_contract(h, 1.0, 0x1000, 0x2000, 0.0, 0x1010) == 1      # C overlaps A
+    g.gett_destroy(h)
+    assert g.gett_destroy(None) == 0
+    assert g.gett_plan_describe(None) == ""
+    assert g.gett_status_string(4) == "HIP runtime error"
+
+
+def test_contract_empty_c_is_a_no_op():
+    st, h = plan("m,n", "m,k", "k,n", {"m": 0, "n": 8, "k": 8})
+    assert st == 0
+    assert json.loads(g.gett_plan_describe(h))["empty_c"] is True
+    assert g.gett_contract(h, 1.0, 0x1000, 0x2000, 0.0, 0x3000) == 0
+    g.gett_destroy(h)
+
+
+def test_launch_failure_is_reported():
+    """The launch error path, forced from the host (no GPU call happens)."""
+    code = (
+        "import os, sys; sys.path.insert(0, %r);"
+        "import paper_1607_00145_amd as g;"
+        "st, h = g.gett_plan(0, 'm,n', [8, 8], None, 'm,k', [8, 8], None, 'k,n', [8, 8], None);"
+        "print(g.gett_contract(h, 1.0, 0x10000, 0x20000, 0.0, 0x30000))" % ROOT)
+    env = dict(os.environ, GETT_FAULT_INJECT="launch")
+    out = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True)
+    assert out.stdout.strip() == "4", out.stderr
+
+
+def test_expression_parser():
+    assert g.parse_expression("C[a,b,i,j] = A[i,m,a] * B[m,j,b]") == ("a,b,i,j", "i,m,a", "m,j,b")
+    assert g.parse_expression("C[m1] = A[m1,k] * B[k]") == ("m1,", "m1,k", "k,")

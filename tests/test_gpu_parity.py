@@ -1,0 +1,186 @@
+"""GPU parity: the HIP path (through the C interface) against the oracle.
+
+Bar: max |diff| / (|alpha| * sum_k |a||b| + |beta| * |c|) <= 1e-4 for fp32 and
+1e-12 for fp64, element by element; integer-valued inputs must match exactly;
+elements of the C buffer that are not part of C must be left untouched."""
+import json
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_1607_00145_amd as g
+import workloads as wl
+from gpu_util import TOL, Operand, make_operand, reference, result_view, run_gpu, split, \
+    touched_mask
+
+pytestmark = pytest.mark.gpu
+DTYPES = [np.float32, np.float64]
+
+
+def check_case(dev, rng, modes, shapes, dtype, alpha, beta, kinds=("dense",) * 3, flags=0,
+               dist="uniform", offsets=(0, 0, 0)):
+    mc, ma, mb = modes
+    C = make_operand(rng, shapes[0], dtype, kinds[0], dist, offsets[0])
+    A = make_operand(rng, shapes[1], dtype, kinds[1], dist, offsets[1])
+    B = make_operand(rng, shapes[2], dtype, kinds[2], dist, offsets[2])
+    inside = touched_mask(C)
+    if beta == 0:
+        C.flat[inside] = np.nan          # beta == 0 must not read C; every element gets written
+    C.flat[~inside] = 7777.0             # canaries in gaps and guard bands
+    before = C.flat.copy()
+    ref = reference(modes, (C, A, B), alpha, beta)
+    got_flat, _ = run_gpu(dev, modes, (C, A, B), alpha, beta, flags)
+    assert np.array_equal(got_flat[~inside], before[~inside]), "wrote outside C"
+    got = result_view(got_flat, C)
+    err = oracle.rel_error(got, ref)
+    assert err <= TOL[dtype], f"rel err {err:.3e} for {modes} {shapes}"
+    return got, ref
+
+
+@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_random_contractions(gpu, seed, dtype):
+    rng = np.random.default_rng(10_000 + seed)
+    mc, ma, mb, ext = wl.random_problem(rng, max_rank=6, max_ext=7,
+                                        allow_empty_sets=(seed % 6 == 5))
+    shp = lambda m: [ext[x] for x in split(m)]
+    kinds = tuple(rng.choice(["dense", "gapped", "permuted"]) for _ in range(3))
+    alpha = float(rng.choice([1.0, -0.75, 2.5]))
+    beta = float(rng.choice([0.0, 1.0, -1.25]))
+    check_case(gpu, rng, (mc, ma, mb), (shp(mc), shp(ma), shp(mb)), dtype, alpha, beta, kinds)
+
+
+@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_integer_inputs_bit_exact(gpu, seed, dtype):
+    """Integer inputs make every partial sum exact: results must be identical."""
+    rng = np.random.default_rng(20_000 + seed)
+    mc, ma, mb, ext = wl.random_problem(rng, max_rank=6, max_ext=9)
+    shp = lambda m: [ext[x] for x in split(m)]
+    beta = float(seed % 2)
+    got, ref = check_case(gpu, rng, (mc, ma, mb), (shp(mc), shp(ma), shp(mb)), dtype, 1.0, beta,
+                          dist="int")
+    np.testing.assert_array_equal(got.astype(np.float64), ref.out64)
+
+
+SCALED = {
+    1: {"a": 37, "b": 29, "c": 5, "k": 41},
+    2: {"a": 23, "b": 19, "c": 21, "d": 13, "e": 16},
+    3: {"a": 11, "b": 13, "i": 12, "j": 14, "e": 9, "f": 17},
+    4: {"a": 7, "b": 6, "c": 9, "d": 24, "i": 5, "j": 8, "k": 7},
+    5: {"m1": 40, "m2": 6, "n1": 36, "n2": 7, "k1": 10, "k2": 33},
+}
+
+
+@pytest.mark.parametrize("number", [1, 2, 3, 4, 5])
+def test_workload_structure_scaled(gpu, number):
+    """Each workload's index structure at sizes the oracle checks in full:
+    several tiles along each free set and ragged tails everywhere."""
+    w = wl.scaled(wl.WORKLOADS[number - 1], SCALED[number])
+    rng = np.random.default_rng(w.seed)
+    check_case(gpu, rng, (w.modes_C, w.modes_A, w.modes_B),
+               (w.shape("C"), w.shape("A"), w.shape("B")), w.np_dtype, w.alpha, w.beta)
+
+
+@pytest.mark.parametrize("number", [1, 2, 3, 4, 5])
+def test_workload_full_size_sampled(gpu, number):
+    """Full-size workloads in the benchmark's launch configuration; the
+    oracle checks 4096 sampled elements; for beta == 0 (C pre-filled with NaN)
+    every element must have been written."""
+    import torch
+    w = wl.WORKLOADS[number - 1]
+    A, B, Cin = wl.make_inputs(w)
+    dev = gpu
+    tA = torch.from_numpy(np.asfortranarray(A).reshape(-1, order="F")).to(dev)
+    tB = torch.from_numpy(np.asfortranarray(B).reshape(-1, order="F")).to(dev)
+    nC = w.numel("C")
+    if Cin is not None:
+        tC = torch.from_numpy(np.asfortranarray(Cin).reshape(-1, order="F")).to(dev)
+    else:
+        tC = torch.full((nC,), float("nan"), dtype=tA.dtype, device=dev)
+    dt = g.GETT_FLOAT32 if w.dtype == "f32" else g.GETT_FLOAT64
+    st, h = g.gett_plan(dt, w.modes_C, w.shape("C"), None, w.modes_A, w.shape("A"), None,
+                        w.modes_B, w.shape("B"), None, 0)
+    assert st == 0
+    st = g.gett_contract(h, w.alpha, tA.data_ptr(), tB.data_ptr(), w.beta, tC.data_ptr(),
+                         torch.cuda.current_stream().cuda_stream)
+    assert st == 0
+    torch.cuda.synchronize()
+    g.gett_destroy(h)
+    if Cin is None:
+        assert bool(torch.isfinite(tC).all()), "some element of C was not written"
+    rng = np.random.default_rng(w.seed + 99)
+    pts = np.concatenate([rng.integers(0, nC, 4090), [0, nC - 1, 1, nC - 2, nC // 2, 12345]])
+    got = tC[torch.from_numpy(pts).to(dev)].cpu().numpy()
+    ref = oracle.contract(w.modes_C, w.modes_A, w.modes_B, A, B, w.alpha, w.beta, Cin,
+                          shape_C=w.shape("C"), points=pts)
+    err = oracle.rel_error(got, ref)
+    assert err <= TOL[w.np_dtype], f"{w.name}: rel err {err:.3e}"
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_alpha_zero_reads_no_operand(gpu, dtype):
+    rng = np.random.default_rng(5)
+    modes = ("a,b", "a,k", "k,b")
+    C = make_operand(rng, [70, 45], dtype)
+    A = make_operand(rng, [70, 33], dtype)
+    B = make_operand(rng, [33, 45], dtype)
+    A.flat[:] = np.nan
+    B.flat[:] = np.nan
+    ref = result_view(C.flat, C).astype(np.float64) * -2.0
+    got_flat, _ = run_gpu(gpu, modes, (C, A, B), 0.0, -2.0)
+    np.testing.assert_array_equal(result_view(got_flat, C).astype(np.float64), ref)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("flags", [g.GETT_FLAG_SCALAR, g.GETT_FLAG_NO_SWAP,
+                                   g.GETT_FLAG_SCALAR | g.GETT_FLAG_NO_SWAP])
+def test_flags(gpu, dtype, flags):
+    rng = np.random.default_rng(6)
+    w = wl.scaled(wl.WORKLOADS[4], SCALED[5])
+    check_case(gpu, rng, (w.modes_C, w.modes_A, w.modes_B),
+               (w.shape("C"), w.shape("A"), w.shape("B")), dtype, 1.5, 0.5, flags=flags)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_unaligned_pointers_use_element_accesses(gpu, dtype):
+    """Base pointers off the 16-byte grid: vector accesses must be dropped."""
+    rng = np.random.default_rng(7)
+    w = wl.scaled(wl.WORKLOADS[1], SCALED[2])
+    check_case(gpu, rng, (w.modes_C, w.modes_A, w.modes_B),
+               (w.shape("C"), w.shape("A"), w.shape("B")), dtype, 1.0, 1.0, offsets=(1, 3, 1))
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_many_contracted_boxes(gpu, dtype):
+    """Long contraction over several indices with ragged blocks."""
+    rng = np.random.default_rng(8)
+    modes = ("m,n", "k1,m,k2,k3", "k3,n,k2,k1")
+    ext = {"m": 67, "n": 70, "k1": 13, "k2": 9, "k3": 21}
+    shp = lambda s: [ext[x] for x in split(s)]
+    check_case(gpu, rng, modes, (shp(modes[0]), shp(modes[1]), shp(modes[2])), dtype, 1.0, 0.0)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_zero_contracted_extent(gpu, dtype):
+    rng = np.random.default_rng(9)
+    C = make_operand(rng, [20, 30], dtype)
+    A = make_operand(rng, [20, 0], dtype)
+    B = make_operand(rng, [0, 30], dtype)
+    ref = result_view(C.flat, C).astype(np.float64) * 0.5
+    got_flat, _ = run_gpu(gpu, ("a,b", "a,k", "k,b"), (C, A, B), 1.0, 0.5)
+    np.testing.assert_array_equal(result_view(got_flat, C).astype(np.float64), ref)
+
+
+def test_plan_class_on_torch_views(gpu):
+    import torch
+    a = torch.randn(40, 30, 20, dtype=torch.float64, device=gpu).permute(2, 0, 1)  # (20,40,30)
+    b = torch.randn(30, 50, dtype=torch.float64, device=gpu)
+    c = torch.zeros(50, 20, 40, dtype=torch.float64, device=gpu)
+    p = g.Plan("C[n,i,j] = A[i,j,k] * B[k,n]", C=c, A=a, B=b)
+    p(a, b, c, 1.0, 0.0)
+    torch.cuda.synchronize()
+    ref = torch.einsum("ijk,kn->nij", a.cpu(), b.cpu())
+    assert torch.allclose(c.cpu(), ref, rtol=1e-12, atol=1e-12)
+    assert p.describe()["dtype"] == "f64"
