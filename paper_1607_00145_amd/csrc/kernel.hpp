@@ -16,8 +16,8 @@
 //
 // Register tile of a wavefront.  Lane l (l16 = l % 16, g = l / 16) of an
 // MFMA 16x16x4 supplies row l16 of the A-operand and column l16 of the
-// B-operand at contracted position g, and receives results for rows
-// 4g..4g+3 of column l16.  The kernel lets one 16-byte LDS read per lane
+// B-operand at contracted position g, and receives four results of column
+// l16 (rows Traits<T>::mrow(g, 0..3)).  The kernel lets one 16-byte LDS read per lane
 // feed VW blocks at once (VW = 4 for fp32, 2 for fp64): within a group of
 // 16*VW rows, MFMA row r of block i is tile row VW*r + i (same for columns).
 // A lane then owns VW consecutive columns of C for each of its rows, which
@@ -38,15 +38,20 @@ typedef double f64x2 __attribute__((ext_vector_type(2)));
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 
 template <typename T> struct Traits;
+// Result layout of the 16x16x4 MFMAs: lane l, accumulator element r holds
+// row mrow(l / 16, r) of column l % 16.  The fp32 instruction gives each lane
+// four consecutive rows; the fp64 instruction interleaves them with stride 4.
 template <> struct Traits<float> {
     typedef f32x4 vec;   // 16-byte vector
     typedef f32x4 acc;   // 16x16 MFMA accumulator slice of one lane
     static constexpr int VW = 4;
+    static __device__ __forceinline__ int mrow(int g, int r) { return 4 * g + r; }
 };
 template <> struct Traits<double> {
     typedef f64x2 vec;
     typedef f64x4 acc;
     static constexpr int VW = 2;
+    static __device__ __forceinline__ int mrow(int g, int r) { return g + 4 * r; }
 };
 
 __device__ __forceinline__ f32x4 mfma16x16x4(float a, float b, f32x4 c)
@@ -351,7 +356,7 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
         for (int i = 0; i < VW; ++i)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int xl = wm * WTM + rg * 16 * VW + VW * (4 * g + r) + i;
+                const int xl = wm * WTM + rg * 16 * VW + VW * Traits<T>::mrow(g, r) + i;
                 const int64_t ox = offCx[xl];
                 if (ox < 0) continue;
 #pragma unroll
