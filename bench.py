@@ -206,6 +206,9 @@ def main():
     ap.add_argument("--report-runs", type=int, default=20)
     ap.add_argument("--no-report", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB a few times (the reference "
+                         "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the contraction is built and timed on a single "
@@ -220,6 +223,15 @@ def main():
     g.load_library()   # fails loudly when the HIP library is not built
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
+    if args.calibrate_copy:
+        n = args.calibrate_copy * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n * 4, "launches": 5}), flush=True)
+        return
     w = wl.BY_NAME[args.workload]
 
     # ---- headline: K back-to-back steps, inputs resident ----
