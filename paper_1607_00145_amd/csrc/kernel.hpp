@@ -87,26 +87,29 @@ __device__ __forceinline__ void tile_of_block(const KDesc &d, int &tx, int &ty)
 // Origin of K box `s`: block `s % nblk` of index kj, then one point of each
 // later contracted index (first one fastest).  Returns the origin offsets in
 // X and Y and the number of valid positions left along index kj.
-__device__ __forceinline__ int box_origin(const KDesc &d, uint32_t s, int64_t &ox, int64_t &oy)
+__device__ __forceinline__ int box_origin(const KDesc &d, uint32_t s, int &ox, int &oy)
 {
     const uint32_t nb = (uint32_t)d.nblk;
     const uint32_t rest0 = s / nb;
     const int blk = (int)(s - rest0 * nb);
     uint32_t rest = rest0;
-    ox = (int64_t)blk * d.tj * d.strXk[d.kj];
-    oy = (int64_t)blk * d.tj * d.strYk[d.kj];
+    ox = blk * d.tj * (int)d.strXk[d.kj];
+    oy = blk * d.tj * (int)d.strYk[d.kj];
     for (int i = d.kj + 1; i < d.nk; ++i) {
         const uint32_t e = (uint32_t)d.extK[i];
         const uint32_t q = rest / e;
         const uint32_t c = rest - q * e;
         rest = q;
-        ox += (int64_t)c * d.strXk[i];
-        oy += (int64_t)c * d.strYk[i];
+        ox += (int)c * (int)d.strXk[i];
+        oy += (int)c * (int)d.strYk[i];
     }
     return d.extK[d.kj] - blk * d.tj;
 }
 
-// Per-thread description of the part of one operand tile it gathers.
+// Per-thread description of the part of one operand tile it gathers.  Item
+// `it` of thread `tid` is element (or vector) tid + it * NTH of the tile in
+// the mode's order; the tile shapes are chosen so that consecutive items of
+// one thread are a fixed LDS distance apart.
 template <typename T, int ROWS, int KT, int MODE, int NTH>
 struct Gather {
     static constexpr int VW = Traits<T>::VW;
@@ -115,16 +118,20 @@ struct Gather {
     static constexpr int ITEMS = ROWS * KT / W;
     static constexpr int NI = ITEMS / NTH;
     static_assert(ITEMS % NTH == 0, "tile must split evenly over the workgroup");
+    static_assert(NTH % (ROWS / VW) == 0 && NTH % (KT / VW) == 0 && NTH % KT == 0 &&
+                      NTH % ROWS == 0,
+                  "items of one thread must be a fixed LDS distance apart");
     typedef typename Traits<T>::vec vec;
 
-    int64_t goff[NI];   // element offset in the operand (without the box origin)
-    int kc[NI];         // position along index kj inside the box; kInvalidK: never valid
-    int lds[NI];        // destination element in the LDS tile
-    T val[NI][W];       // staged values
+    int goff[NI];   // element offset in the operand (without the box origin); < 2^31
+    int kc[NI];     // position along index kj inside the box; kInvalidK: never valid
+    int lds0;       // LDS slot of item 0
+    int lstep;      // LDS distance between consecutive items
+    T val[NI][W];   // staged values
 
     // rowoff: LDS table of operand offsets per tile row (-1 = outside the tensor)
     // koff/kco: LDS tables of offsets / kj-positions per box element
-    __device__ __forceinline__ void setup(int tid, const int64_t *rowoff, const int64_t *koff,
+    __device__ __forceinline__ void setup(int tid, const int *rowoff, const int *koff,
                                           const int *kco, int kfast)
     {
 #pragma unroll
@@ -144,22 +151,24 @@ struct Gather {
                 r = i % ROWS;
                 kk = i / ROWS;
             }
-            const int64_t ro = rowoff[r];
+            const int ro = rowoff[r];
             goff[it] = (ro < 0 ? 0 : ro) + koff[kk];
             kc[it] = ro < 0 ? kInvalidK : kco[kk];
-            lds[it] = kk * PITCH + r;
+            if (it == 0) lds0 = kk * PITCH + r;
+            if (it == 1) lstep = kk * PITCH + r - lds0;
         }
+        if (NI == 1) lstep = 0;
     }
 
-    __device__ __forceinline__ void load(const T *__restrict__ p, int64_t base, int limit)
+    __device__ __forceinline__ void load(const T *__restrict__ p, int limit)
     {
 #pragma unroll
         for (int it = 0; it < NI; ++it) {
             if (kc[it] < limit) {
                 if (W == 1) {
-                    val[it][0] = p[base + goff[it]];
+                    val[it][0] = p[goff[it]];
                 } else {
-                    const vec v = *reinterpret_cast<const vec *>(p + base + goff[it]);
+                    const vec v = *reinterpret_cast<const vec *>(p + goff[it]);
 #pragma unroll
                     for (int e = 0; e < W; ++e) val[it][e] = v[e];
                 }
@@ -174,16 +183,17 @@ struct Gather {
     {
 #pragma unroll
         for (int it = 0; it < NI; ++it) {
+            T *dst = tile + lds0 + it * lstep;
             if (MODE == kGatherRowVec) {
                 vec v;
 #pragma unroll
                 for (int e = 0; e < W; ++e) v[e] = val[it][e];
-                *reinterpret_cast<vec *>(tile + lds[it]) = v;
+                *reinterpret_cast<vec *>(dst) = v;
             } else if (MODE == kGatherKVec) {
 #pragma unroll
-                for (int e = 0; e < W; ++e) tile[lds[it] + e * PITCH] = val[it][e];
+                for (int e = 0; e < W; ++e) dst[e * PITCH] = val[it][e];
             } else {
-                tile[lds[it]] = val[it][0];
+                *dst = val[it][0];
             }
         }
     }
@@ -210,8 +220,10 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
 
     __shared__ __attribute__((aligned(16))) T xs[2][KT * GX::PITCH];
     __shared__ __attribute__((aligned(16))) T ys[2][KT * GY::PITCH];
-    __shared__ int64_t rowX[MT], rowY[NT], offCx[MT], offCy[NT];
-    __shared__ int64_t kX[KT], kY[KT];
+    // Element offsets fit in 31 bits (the plan refuses larger tensors); -1 marks
+    // a row or column outside the tensor.
+    __shared__ int rowX[MT], rowY[NT], offCx[MT], offCy[NT];
+    __shared__ int kX[KT], kY[KT];
     __shared__ int kco[KT];
 
     const int tid = (int)threadIdx.x;
@@ -221,7 +233,7 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     // ---- identify_subtensor: offsets of this tile's rows, columns, box ----
     for (int r = tid; r < MT; r += NTH) {
         uint32_t x = (uint32_t)tx * MT + r;
-        int64_t ox = -1, oc = -1;
+        int ox = -1, oc = -1;
         if ((int64_t)x < d.sizeX) {
             ox = 0;
             oc = 0;
@@ -230,8 +242,8 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
                 const uint32_t q = x / e;
                 const uint32_t id = x - q * e;
                 x = q;
-                ox += (int64_t)id * d.strXop[i];
-                oc += (int64_t)id * d.strCx[i];
+                ox += (int)id * (int)d.strXop[i];
+                oc += (int)id * (int)d.strCx[i];
             }
         }
         rowX[r] = ox;
@@ -239,7 +251,7 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     }
     for (int r = tid; r < NT; r += NTH) {
         uint32_t y = (uint32_t)ty * NT + r;
-        int64_t oy = -1, oc = -1;
+        int oy = -1, oc = -1;
         if ((int64_t)y < d.sizeY) {
             oy = 0;
             oc = 0;
@@ -248,15 +260,15 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
                 const uint32_t q = y / e;
                 const uint32_t id = y - q * e;
                 y = q;
-                oy += (int64_t)id * d.strYop[i];
-                oc += (int64_t)id * d.strCy[i];
+                oy += (int)id * (int)d.strYop[i];
+                oc += (int)id * (int)d.strCy[i];
             }
         }
         rowY[r] = oy;
         offCy[r] = oc;
     }
     for (int kk = tid; kk < KT; kk += NTH) {
-        int64_t ox = 0, oy = 0;
+        int ox = 0, oy = 0;
         int pos = kInvalidK;
         if (kk < d.kbox) {
             uint32_t k = (uint32_t)kk;
@@ -265,12 +277,12 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
                 const uint32_t q = k / e;
                 const uint32_t id = k - q * e;
                 k = q;
-                ox += (int64_t)id * d.strXk[i];
-                oy += (int64_t)id * d.strYk[i];
+                ox += (int)id * (int)d.strXk[i];
+                oy += (int)id * (int)d.strYk[i];
             }
             pos = (int)k;   // position along index kj, < tj
-            ox += (int64_t)k * d.strXk[d.kj];
-            oy += (int64_t)k * d.strYk[d.kj];
+            ox += (int)k * (int)d.strXk[d.kj];
+            oy += (int)k * (int)d.strYk[d.kj];
         }
         kX[kk] = ox;
         kY[kk] = oy;
@@ -300,10 +312,10 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
 
     const uint32_t nsteps = (uint32_t)d.nsteps;
     if (nsteps > 0) {
-        int64_t ox, oy;
+        int ox, oy;
         const int lim = box_origin(d, 0, ox, oy);
-        gx.load(X, ox, lim);
-        gy.load(Y, oy, lim);
+        gx.load(X + ox, lim);
+        gy.load(Y + oy, lim);
         gx.store(xs[0]);
         gy.store(ys[0]);
     }
@@ -313,10 +325,10 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
         const int buf = (int)(s & 1);
         const bool more = s + 1 < nsteps;
         if (more) {
-            int64_t ox, oy;
+            int ox, oy;
             const int lim = box_origin(d, s + 1, ox, oy);
-            gx.load(X, ox, lim);
-            gy.load(Y, oy, lim);
+            gx.load(X + ox, lim);
+            gy.load(Y + oy, lim);
         }
         const T *xt = xs[buf] + wm * WTM + VW * l16;
         const T *yt = ys[buf] + wn * WTN + VW * l16;
@@ -349,43 +361,76 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     }
 
     // ---- unpack: C <- alpha * acc + beta * C through C's strides (Eq. 11) ----
+    // One row group at a time: first every C load of the group (so they are in
+    // flight together), then the updates and non-temporal stores (C is written
+    // once and not reused).
     const bool readC = beta != T(0);
+    constexpr int NR = VW * 4;   // rows of one row group owned by a lane
 #pragma unroll
-    for (int rg = 0; rg < RG; ++rg)
+    for (int rg = 0; rg < RG; ++rg) {
+        int ox[NR];
 #pragma unroll
         for (int i = 0; i < VW; ++i)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int xl = wm * WTM + rg * 16 * VW + VW * Traits<T>::mrow(g, r) + i;
-                const int64_t ox = offCx[xl];
-                if (ox < 0) continue;
+            for (int r = 0; r < 4; ++r)
+                ox[i * 4 + r] = offCx[wm * WTM + rg * 16 * VW + VW * Traits<T>::mrow(g, r) + i];
+        if (d.cvec) {
+            int oy[CG];
+#pragma unroll
+            for (int cg = 0; cg < CG; ++cg) oy[cg] = offCy[wn * WTN + cg * 16 * VW + VW * l16];
+            vec cv[NR][CG];
+            if (readC) {
+#pragma unroll
+                for (int q = 0; q < NR; ++q)
+#pragma unroll
+                    for (int cg = 0; cg < CG; ++cg)
+                        if (ox[q] >= 0 && oy[cg] >= 0)
+                            cv[q][cg] = __builtin_nontemporal_load(
+                                reinterpret_cast<const vec *>(C + ox[q] + oy[cg]));
+            }
+#pragma unroll
+            for (int q = 0; q < NR; ++q)
 #pragma unroll
                 for (int cg = 0; cg < CG; ++cg) {
-                    const int yl = wn * WTN + cg * 16 * VW + VW * l16;
-                    if (d.cvec) {
-                        const int64_t oy = offCy[yl];
-                        if (oy < 0) continue;
-                        T *p = C + ox + oy;
-                        vec cv;
-                        if (readC) cv = *reinterpret_cast<const vec *>(p);
+                    if (ox[q] < 0 || oy[cg] < 0) continue;
+                    vec out;
 #pragma unroll
-                        for (int j = 0; j < VW; ++j) {
-                            const T a = alpha * acc[rg * VW + i][cg * VW + j][r];
-                            cv[j] = readC ? a + beta * cv[j] : a;
-                        }
-                        *reinterpret_cast<vec *>(p) = cv;
-                    } else {
-#pragma unroll
-                        for (int j = 0; j < VW; ++j) {
-                            const int64_t oy = offCy[yl + j];
-                            if (oy < 0) continue;
-                            T *p = C + ox + oy;
-                            const T a = alpha * acc[rg * VW + i][cg * VW + j][r];
-                            *p = readC ? a + beta * (*p) : a;
-                        }
+                    for (int j = 0; j < VW; ++j) {
+                        const T a = alpha * acc[rg * VW + q / 4][cg * VW + j][q % 4];
+                        out[j] = readC ? a + beta * cv[q][cg][j] : a;
                     }
+                    __builtin_nontemporal_store(out, reinterpret_cast<vec *>(C + ox[q] + oy[cg]));
                 }
+        } else {
+            int oy[CG][VW];
+#pragma unroll
+            for (int cg = 0; cg < CG; ++cg)
+#pragma unroll
+                for (int j = 0; j < VW; ++j) oy[cg][j] = offCy[wn * WTN + cg * 16 * VW + VW * l16 + j];
+            T cv[NR][CG][VW];
+            if (readC) {
+#pragma unroll
+                for (int q = 0; q < NR; ++q)
+#pragma unroll
+                    for (int cg = 0; cg < CG; ++cg)
+#pragma unroll
+                        for (int j = 0; j < VW; ++j)
+                            if (ox[q] >= 0 && oy[cg][j] >= 0)
+                                cv[q][cg][j] = __builtin_nontemporal_load(C + ox[q] + oy[cg][j]);
             }
+#pragma unroll
+            for (int q = 0; q < NR; ++q)
+#pragma unroll
+                for (int cg = 0; cg < CG; ++cg)
+#pragma unroll
+                    for (int j = 0; j < VW; ++j) {
+                        if (ox[q] < 0 || oy[cg][j] < 0) continue;
+                        const T a = alpha * acc[rg * VW + q / 4][cg * VW + j][q % 4];
+                        __builtin_nontemporal_store(readC ? a + beta * cv[q][cg][j] : a,
+                                                    C + ox[q] + oy[cg][j]);
+                    }
+        }
+    }
 }
 
 }  // namespace gett
