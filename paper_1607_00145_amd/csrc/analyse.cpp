@@ -20,7 +20,9 @@
 //      over the contracted indices, splitting one index into blocks
 //      (Sec. 3.2.1, Examples 1-2: index reinterpretation) -- and the gather
 //      mode of each operand.
+#include <math.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -303,36 +305,12 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     if ((int)Ix.size() > kMaxDims || (int)Iy.size() > kMaxDims || (int)Ik.size() > kMaxDims)
         return GETT_ERROR_NOT_SUPPORTED;
 
-    // ---- tile shape ----
+    // ---- K box for a given box depth: whole leading contracted indices,
+    //      then a block of one index (index reinterpretation) ----
     const int VW = dtype == GETT_FLOAT32 ? 4 : 2;
     const int64_t sizeX = swap ? an.sizeN : an.sizeM;
     const int64_t sizeY = swap ? an.sizeM : an.sizeN;
-    int tile = 0;
-    {
-        const TileShape &t0 = tile_shape(dtype, 0);
-        const int64_t wg0 = ((sizeX + t0.mt - 1) / t0.mt) * ((sizeY + t0.nt - 1) / t0.nt);
-        if (wg0 < 256 && num_tiles(dtype) > 1) tile = 1;
-    }
-    const TileShape &ts = tile_shape(dtype, tile);
-
-    // ---- K box: whole leading contracted indices, then a block of one ----
-    int kj = 0;
-    int64_t prefix = 1;
     const int nk = (int)Ik.size();
-    while (kj < nk - 1 && prefix * Ik[kj].extent <= ts.kt) {
-        prefix *= Ik[kj].extent;
-        ++kj;
-    }
-    int64_t tj = std::min<int64_t>(Ik[kj].extent, ts.kt / prefix);
-    if (tj < 1) tj = 1;
-    // Prefer a block length that divides the index (no ragged last block)
-    // unless that would lose more than half of the box.
-    {
-        int64_t best = tj;
-        for (int64_t t = tj; t >= 1; --t)
-            if (Ik[kj].extent % t == 0) { best = t; break; }
-        if (best * 2 > tj) tj = best;
-    }
     // A contracted stride-one run gathered as vectors needs whole vectors per block.
     auto kvec_ok = [&](auto strOf) {
         if (strOf(Ik[0]) != 1) return false;
@@ -342,18 +320,86 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         return true;
     };
     const bool wantKvec = !(flags & GETT_FLAG_SCALAR) && (kvec_ok(sX) || kvec_ok(sY));
-    if (wantKvec && kj == 0 && tj % VW) {
-        const int64_t t2 = (tj / VW) * VW;
-        if (t2 >= VW) {
-            tj = t2;
-            while (Ik[0].extent % tj && tj > VW) tj -= VW;   // keep it dividing when possible
+    struct Box {
+        int kj;
+        int64_t tj, kbox, nblk, nsteps;
+    };
+    auto box_for = [&](int kt) {
+        Box b;
+        b.kj = 0;
+        int64_t prefix = 1;
+        while (b.kj < nk - 1 && prefix * Ik[b.kj].extent <= kt) {
+            prefix *= Ik[b.kj].extent;
+            ++b.kj;
+        }
+        int64_t tj = std::max<int64_t>(1, std::min<int64_t>(Ik[b.kj].extent, kt / prefix));
+        // Prefer a block length that divides the index (no ragged last block)
+        // unless that would lose more than half of the box.
+        {
+            int64_t best = tj;
+            for (int64_t t = tj; t >= 1; --t)
+                if (Ik[b.kj].extent % t == 0) { best = t; break; }
+            if (best * 2 > tj) tj = best;
+        }
+        if (wantKvec && b.kj == 0 && tj % VW) {
+            const int64_t t2 = (tj / VW) * VW;
+            if (t2 >= VW) {
+                tj = t2;
+                while (Ik[0].extent % tj && tj > VW) tj -= VW;   // keep it dividing when possible
+            }
+        }
+        b.tj = tj;
+        b.kbox = prefix * tj;
+        b.nblk = (Ik[b.kj].extent + tj - 1) / tj;
+        b.nsteps = b.nblk;
+        for (int i = b.kj + 1; i < nk; ++i) b.nsteps *= Ik[i].extent;
+        if (an.emptySum) b.nsteps = 0;
+        return b;
+    };
+
+    // ---- tile shape: the paper ranks candidates with a performance model
+    //      (Sec. 3.4: macro-kernel time from flops / (peak * penalty), packing
+    //      and unpacking time from bytes / bandwidth).  Here: MFMA time of the
+    //      busiest compute unit (tiles are dealt to 256 CUs in rounds, each
+    //      tile including its padding) against the C stream through HBM; the
+    //      shorter one overlaps the longer one only in part. ----
+    const double itemB = dtype == GETT_FLOAT32 ? 4.0 : 8.0;
+    const double peakCU = (dtype == GETT_FLOAT32 ? 157.3e12 : 78.6e12) / 256.0;
+    const double bw = 6.0e12;   // sustained HBM bandwidth of a streaming kernel
+    const double bytesX = itemB * (double)sizeX * (double)an.sizeK;
+    const double bytesY = itemB * (double)sizeY * (double)an.sizeK;
+    const double bytesC = itemB * (double)sizeX * (double)sizeY;
+    int tile = 0;
+    double bestCost = 1e300;
+    std::ostringstream costs;
+    for (int t = 0; t < num_tiles(dtype); ++t) {
+        const TileShape &c = tile_shape(dtype, t);
+        const Box b = box_for(c.kt);
+        const double tx = (double)((sizeX + c.mt - 1) / c.mt);
+        const double ty = (double)((sizeY + c.nt - 1) / c.nt);
+        const double rounds = std::ceil(tx * ty / 256.0);
+        const double kpad = (double)std::max<int64_t>(b.nsteps, 1) * c.kt;
+        const double tMfma = rounds * (double)c.mt * c.nt * kpad * 2.0 / (peakCU * c.eff);
+        const double tMem = (bytesC + 0.05 * (bytesX * ty + bytesY * tx)) / bw;
+        const double cost = std::max(tMfma, tMem) + 0.3 * std::min(tMfma, tMem);
+        costs << (t ? "," : "") << cost * 1e6;
+        if (cost < bestCost) {
+            bestCost = cost;
+            tile = t;
         }
     }
-    const int64_t kbox = prefix * tj;
-    const int64_t nblk = (Ik[kj].extent + tj - 1) / tj;
-    int64_t nsteps = nblk;
-    for (int i = kj + 1; i < nk; ++i) nsteps *= Ik[i].extent;
-    if (an.emptySum) nsteps = 0;
+    bool forced = false;
+    if (const char *ft = getenv("GETT_FORCE_TILE")) {   // tuning and test hook
+        const int v = atoi(ft);
+        if (v >= 0 && v < num_tiles(dtype)) {
+            tile = v;
+            forced = true;
+        }
+    }
+    const TileShape &ts = tile_shape(dtype, tile);
+    const Box box = box_for(ts.kt);
+    const int kj = box.kj;
+    const int64_t tj = box.tj, kbox = box.kbox, nblk = box.nblk, nsteps = box.nsteps;
 
     // ---- gather modes ----
     auto row_vec_ok = [&](const std::vector<Index> &I, auto strOf) {
@@ -381,6 +427,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     bool cvec = !(flags & GETT_FLAG_SCALAR) && Iy[0].strC == 1 && Iy[0].extent % VW == 0;
     for (auto &x : Ix) if (x.strC % VW) cvec = false;
     for (size_t i = 1; i < Iy.size(); ++i) if (Iy[i].strC % VW) cvec = false;
+    if (ts.ry != VW) cvec = false;   // the tile's lanes do not own VW consecutive columns
 
     // ---- descriptor ----
     KDesc d;
@@ -460,7 +507,8 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     names("k_order", Ik);
     o << ",\"size_x\":" << sizeX << ",\"size_y\":" << sizeY << ",\"size_k\":" << an.sizeK;
     o << ",\"tile\":{\"id\":" << tile << ",\"mt\":" << ts.mt << ",\"nt\":" << ts.nt << ",\"kt\":" << ts.kt
-      << ",\"waves\":[" << ts.wm << "," << ts.wn << "]}";
+      << ",\"waves\":[" << ts.wm << "," << ts.wn << "],\"reads\":[" << ts.rx << "," << ts.ry
+      << "],\"forced\":" << (forced ? "true" : "false") << ",\"model_us\":[" << costs.str() << "]}";
     o << ",\"kbox\":{\"kj\":" << kj << ",\"tj\":" << tj << ",\"elements\":" << kbox << ",\"blocks\":" << nblk
       << ",\"steps\":" << nsteps << "}";
     o << ",\"gather_x\":\"" << mode_name(xmode) << "\",\"gather_y\":\"" << mode_name(ymode)

@@ -17,14 +17,15 @@
 // Register tile of a wavefront.  Lane l (l16 = l % 16, g = l / 16) of an
 // MFMA 16x16x4 supplies row l16 of the A-operand and column l16 of the
 // B-operand at contracted position g, and receives four results of column
-// l16 (rows Traits<T>::mrow(g, 0..3)).  The kernel lets one 16-byte LDS read per lane
-// feed VW blocks at once (VW = 4 for fp32, 2 for fp64): within a group of
-// 16*VW rows, MFMA row r of block i is tile row VW*r + i (same for columns).
-// A lane then owns VW consecutive columns of C for each of its rows, which
-// the epilogue writes as one 16-byte vector; with the operands arranged so
-// that C's stride-one index runs along y, 16 lanes store 256 contiguous bytes.
-// The contracted positions used by lane group g at MFMA step s are
-// 4s + g for both operands, so each product pairs matching indices.
+// l16 (rows Traits<T>::mrow(g, 0..3)).  One LDS read of R consecutive rows
+// per lane feeds R blocks at once (R = RX on the row side, RY on the column
+// side; 1, or VW = 16 bytes / element): within a group of 16*R rows, MFMA row
+// r of block i is tile row R*r + i.  With RY = VW a lane owns VW consecutive
+// columns of C for each of its rows, which the epilogue writes as one 16-byte
+// vector; with the operands arranged so that C's stride-one index runs along
+// y, 16 lanes store 256 contiguous bytes.  The contracted positions used by
+// lane group g at MFMA step s are 4s + g for both operands, so each product
+// pairs matching indices.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -199,7 +200,23 @@ struct Gather {
     }
 };
 
-template <typename T, int MT, int NT, int KT, int WM, int WN, int XMODE, int YMODE>
+// R consecutive elements read from LDS by one lane (R = 1: a scalar).
+template <typename T, int R> struct RVec {
+    typedef T __attribute__((ext_vector_type(R))) type;
+    static __device__ __forceinline__ T at(const type &v, int i) { return v[i]; }
+};
+template <typename T> struct RVec<T, 1> {
+    typedef T type;
+    static __device__ __forceinline__ T at(const type &v, int) { return v; }
+};
+
+// Tile row of MFMA row `rho` in block `b` when R rows are read per lane.
+template <int R> __device__ __forceinline__ int block_row(int b, int rho)
+{
+    return (b / R) * 16 * R + R * rho + (b % R);
+}
+
+template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int XMODE, int YMODE>
 __global__ void __launch_bounds__(WM *WN * 64)
 gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
                   T *__restrict__ C, const T alpha, const T beta)
@@ -208,15 +225,20 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     constexpr int VW = Traits<T>::VW;
     constexpr int WTM = MT / WM;            // wave tile rows
     constexpr int WTN = NT / WN;            // wave tile columns
-    constexpr int RG = WTM / (16 * VW);     // row groups per wave
-    constexpr int CG = WTN / (16 * VW);     // column groups per wave
-    static_assert(RG >= 1 && CG >= 1 && WTM % (16 * VW) == 0 && WTN % (16 * VW) == 0,
-                  "wave tile must be a multiple of 16*VW in both directions");
+    constexpr int RB = WTM / 16;            // MFMA blocks per wave along x
+    constexpr int CB = WTN / 16;            // MFMA blocks per wave along y
+    static_assert(WTM % (16 * RX) == 0 && WTN % (16 * RY) == 0,
+                  "wave tile must be a multiple of 16*R in both directions");
+    static_assert(RX == 1 || RX == 2 || RX == 4, "read width");
+    static_assert(RY == 1 || RY == 2 || RY == 4, "read width");
+    static_assert(RX <= VW && RY <= VW, "at most 16 bytes per LDS read");
     static_assert(KT % 4 == 0, "K tile must be a multiple of the MFMA depth");
     typedef Gather<T, MT, KT, XMODE, NTH> GX;
     typedef Gather<T, NT, KT, YMODE, NTH> GY;
     typedef typename Traits<T>::vec vec;
     typedef typename Traits<T>::acc accv;
+    typedef RVec<T, RX> XV;
+    typedef RVec<T, RY> YV;
 
     __shared__ __attribute__((aligned(16))) T xs[2][KT * GX::PITCH];
     __shared__ __attribute__((aligned(16))) T ys[2][KT * GY::PITCH];
@@ -302,14 +324,34 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     const int l16 = lane & 15;
     const int g = lane >> 4;
 
-    accv acc[RG * VW][CG * VW];
+    accv acc[RB][CB];
 #pragma unroll
-    for (int a = 0; a < RG * VW; ++a)
+    for (int a = 0; a < RB; ++a)
 #pragma unroll
-        for (int b = 0; b < CG * VW; ++b)
+        for (int b = 0; b < CB; ++b)
 #pragma unroll
             for (int r = 0; r < 4; ++r) acc[a][b][r] = T(0);
 
+    // The lane's C rows, RX blocks (4*RX rows) at a time, and its columns.
+    constexpr int NR = 4 * RX;
+    auto rows_of = [&](int grp, int *ox) {
+#pragma unroll
+        for (int i = 0; i < RX; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                ox[i * 4 + r] =
+                    offCx[wm * WTM + block_row<RX>(grp * RX + i, Traits<T>::mrow(g, r))];
+    };
+    // With RY == VW and C vectors enabled, column group cg's VW columns are
+    // consecutive: one offset per group.
+    constexpr bool kVecC = RY == VW;
+    constexpr int CGV = CB / RY;   // column groups per wave
+    auto cols_of = [&](int *oy) {
+#pragma unroll
+        for (int cg = 0; cg < CGV; ++cg) oy[cg] = offCy[wn * WTN + cg * 16 * RY + RY * l16];
+    };
+    const bool readC = beta != T(0);
+    const bool useCvec = kVecC && d.cvec;
     const uint32_t nsteps = (uint32_t)d.nsteps;
     if (nsteps > 0) {
         int ox, oy;
@@ -330,28 +372,25 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
             gx.load(X + ox, lim);
             gy.load(Y + oy, lim);
         }
-        const T *xt = xs[buf] + wm * WTM + VW * l16;
-        const T *yt = ys[buf] + wn * WTN + VW * l16;
+        const T *xt = xs[buf] + wm * WTM + RX * l16;
+        const T *yt = ys[buf] + wn * WTN + RY * l16;
 #pragma unroll
         for (int ks = 0; ks < KT / 4; ++ks) {
             const int k = 4 * ks + g;
-            vec av[RG], bv[CG];
+            typename XV::type av[RB / RX];
+            typename YV::type bv[CB / RY];
 #pragma unroll
-            for (int rg = 0; rg < RG; ++rg)
-                av[rg] = *reinterpret_cast<const vec *>(xt + k * GX::PITCH + rg * 16 * VW);
+            for (int gi = 0; gi < RB / RX; ++gi)
+                av[gi] = *reinterpret_cast<const typename XV::type *>(xt + k * GX::PITCH + gi * 16 * RX);
 #pragma unroll
-            for (int cg = 0; cg < CG; ++cg)
-                bv[cg] = *reinterpret_cast<const vec *>(yt + k * GY::PITCH + cg * 16 * VW);
+            for (int gj = 0; gj < CB / RY; ++gj)
+                bv[gj] = *reinterpret_cast<const typename YV::type *>(yt + k * GY::PITCH + gj * 16 * RY);
 #pragma unroll
-            for (int rg = 0; rg < RG; ++rg)
+            for (int a = 0; a < RB; ++a)
 #pragma unroll
-                for (int i = 0; i < VW; ++i)
-#pragma unroll
-                    for (int cg = 0; cg < CG; ++cg)
-#pragma unroll
-                        for (int j = 0; j < VW; ++j)
-                            acc[rg * VW + i][cg * VW + j] =
-                                mfma16x16x4(av[rg][i], bv[cg][j], acc[rg * VW + i][cg * VW + j]);
+                for (int b = 0; b < CB; ++b)
+                    acc[a][b] = mfma16x16x4(XV::at(av[a / RX], a % RX), YV::at(bv[b / RY], b % RY),
+                                            acc[a][b]);
         }
         if (more) {
             gx.store(xs[buf ^ 1]);
@@ -361,29 +400,22 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     }
 
     // ---- unpack: C <- alpha * acc + beta * C through C's strides (Eq. 11) ----
-    // One row group at a time: first every C load of the group (so they are in
-    // flight together), then the updates and non-temporal stores (C is written
-    // once and not reused).
-    const bool readC = beta != T(0);
-    constexpr int NR = VW * 4;   // rows of one row group owned by a lane
+    // RX blocks of rows at a time: first every C load of the group (so they are
+    // in flight together), then the updates and non-temporal stores (C is
+    // written once and not reused).
 #pragma unroll
-    for (int rg = 0; rg < RG; ++rg) {
+    for (int grp = 0; grp < RB / RX; ++grp) {
         int ox[NR];
-#pragma unroll
-        for (int i = 0; i < VW; ++i)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-                ox[i * 4 + r] = offCx[wm * WTM + rg * 16 * VW + VW * Traits<T>::mrow(g, r) + i];
-        if (d.cvec) {
-            int oy[CG];
-#pragma unroll
-            for (int cg = 0; cg < CG; ++cg) oy[cg] = offCy[wn * WTN + cg * 16 * VW + VW * l16];
-            vec cv[NR][CG];
+        rows_of(grp, ox);
+        if (useCvec) {
+            int oy[CGV];
+            cols_of(oy);
+            vec cv[NR][CGV];
             if (readC) {
 #pragma unroll
                 for (int q = 0; q < NR; ++q)
 #pragma unroll
-                    for (int cg = 0; cg < CG; ++cg)
+                    for (int cg = 0; cg < CGV; ++cg)
                         if (ox[q] >= 0 && oy[cg] >= 0)
                             cv[q][cg] = __builtin_nontemporal_load(
                                 reinterpret_cast<const vec *>(C + ox[q] + oy[cg]));
@@ -391,44 +423,37 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
 #pragma unroll
             for (int q = 0; q < NR; ++q)
 #pragma unroll
-                for (int cg = 0; cg < CG; ++cg) {
+                for (int cg = 0; cg < CGV; ++cg) {
                     if (ox[q] < 0 || oy[cg] < 0) continue;
                     vec out;
 #pragma unroll
                     for (int j = 0; j < VW; ++j) {
-                        const T a = alpha * acc[rg * VW + q / 4][cg * VW + j][q % 4];
+                        const T a = alpha * acc[grp * RX + q / 4][kVecC ? cg * RY + j : 0][q % 4];
                         out[j] = readC ? a + beta * cv[q][cg][j] : a;
                     }
                     __builtin_nontemporal_store(out, reinterpret_cast<vec *>(C + ox[q] + oy[cg]));
                 }
         } else {
-            int oy[CG][VW];
+            int oy[CB];
 #pragma unroll
-            for (int cg = 0; cg < CG; ++cg)
-#pragma unroll
-                for (int j = 0; j < VW; ++j) oy[cg][j] = offCy[wn * WTN + cg * 16 * VW + VW * l16 + j];
-            T cv[NR][CG][VW];
+            for (int b = 0; b < CB; ++b) oy[b] = offCy[wn * WTN + block_row<RY>(b, l16)];
+            T cv[NR][CB];
             if (readC) {
 #pragma unroll
                 for (int q = 0; q < NR; ++q)
 #pragma unroll
-                    for (int cg = 0; cg < CG; ++cg)
-#pragma unroll
-                        for (int j = 0; j < VW; ++j)
-                            if (ox[q] >= 0 && oy[cg][j] >= 0)
-                                cv[q][cg][j] = __builtin_nontemporal_load(C + ox[q] + oy[cg][j]);
+                    for (int b = 0; b < CB; ++b)
+                        if (ox[q] >= 0 && oy[b] >= 0)
+                            cv[q][b] = __builtin_nontemporal_load(C + ox[q] + oy[b]);
             }
 #pragma unroll
             for (int q = 0; q < NR; ++q)
 #pragma unroll
-                for (int cg = 0; cg < CG; ++cg)
-#pragma unroll
-                    for (int j = 0; j < VW; ++j) {
-                        if (ox[q] < 0 || oy[cg][j] < 0) continue;
-                        const T a = alpha * acc[rg * VW + q / 4][cg * VW + j][q % 4];
-                        __builtin_nontemporal_store(readC ? a + beta * cv[q][cg][j] : a,
-                                                    C + ox[q] + oy[cg][j]);
-                    }
+                for (int b = 0; b < CB; ++b) {
+                    if (ox[q] < 0 || oy[b] < 0) continue;
+                    const T a = alpha * acc[grp * RX + q / 4][b][q % 4];
+                    __builtin_nontemporal_store(readC ? a + beta * cv[q][b] : a, C + ox[q] + oy[b]);
+                }
         }
     }
 }

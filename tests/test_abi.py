@@ -125,7 +125,8 @@ def test_workload_plans():
         assert d["swapped"] == e["swapped"], w.name
         assert sorted(d["merges"]) == e["merges"], w.name
         assert d["gather_x"] == e["gx"] and d["gather_y"] == e["gy"], w.name
-        assert d["c_vector"] is True
+        vw = 4 if w.dtype == "f32" else 2
+        assert d["c_vector"] is (d["tile"]["reads"][1] == vw)
         assert d["flops"] == wl.flop_count(w)
         # C's stride-one index leads the column order
         first_y = d["y_order"][0]

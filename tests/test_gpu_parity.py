@@ -184,3 +184,24 @@ def test_plan_class_on_torch_views(gpu):
     ref = torch.einsum("ijk,kn->nij", a.cpu(), b.cpu())
     assert torch.allclose(c.cpu(), ref, rtol=1e-12, atol=1e-12)
     assert p.describe()["dtype"] == "f64"
+
+
+TILES = {np.float32: 2, np.float64: 4}
+
+
+@pytest.mark.parametrize("dtype,tile", [(dt, t) for dt in DTYPES for t in range(TILES[dt])])
+@pytest.mark.parametrize("case", ["random", "scaled3", "scaled4"])
+def test_every_tile_shape(gpu, monkeypatch, dtype, tile, case):
+    """Each compiled tile shape, forced through the analyser's test hook."""
+    monkeypatch.setenv("GETT_FORCE_TILE", str(tile))
+    rng = np.random.default_rng(30_000 + tile)
+    if case == "random":
+        mc, ma, mb, ext = wl.random_problem(rng, max_rank=6, max_ext=9)
+        shp = lambda m: [ext[x] for x in split(m)]
+        modes, shapes, alpha, beta = (mc, ma, mb), (shp(mc), shp(ma), shp(mb)), 1.5, -0.5
+    else:
+        w = wl.scaled(wl.WORKLOADS[int(case[-1]) - 1], SCALED[int(case[-1])])
+        modes = (w.modes_C, w.modes_A, w.modes_B)
+        shapes = (w.shape("C"), w.shape("A"), w.shape("B"))
+        alpha, beta = w.alpha, w.beta
+    check_case(gpu, rng, modes, shapes, dtype, alpha, beta)
