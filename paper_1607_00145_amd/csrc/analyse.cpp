@@ -370,7 +370,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     const double bytesY = itemB * (double)sizeY * (double)an.sizeK;
     const double bytesC = itemB * (double)sizeX * (double)sizeY;
     int tile = 0;
-    double bestCost = 1e300;
+    double bestCost = 1e300, bestMfma = 0, bestMem = 0;
     std::ostringstream costs;
     for (int t = 0; t < num_tiles(dtype); ++t) {
         const TileShape &c = tile_shape(dtype, t);
@@ -385,6 +385,8 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         costs << (t ? "," : "") << cost * 1e6;
         if (cost < bestCost) {
             bestCost = cost;
+            bestMfma = tMfma;
+            bestMem = tMem;
             tile = t;
         }
     }
@@ -398,6 +400,20 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     }
     const TileShape &ts = tile_shape(dtype, tile);
     const Box box = box_for(ts.kt);
+    // A contraction bound by the C stream walks C in memory order: x indices
+    // by C stride (the row operand's stride-one index stays first when it is
+    // a free index, for its vector gathers) and tiles y-fastest.
+    const bool streaming = bestMem > bestMfma;
+    if (streaming) {
+        std::stable_sort(Ix.begin(), Ix.end(), [](const Index &a, const Index &b) {
+            return a.strC < b.strC;
+        });
+        for (size_t i = 0; i < Ix.size(); ++i)
+            if (sX(Ix[i]) == 1) {
+                std::rotate(Ix.begin(), Ix.begin() + i, Ix.begin() + i + 1);
+                break;
+            }
+    }
     const int kj = box.kj;
     const int64_t tj = box.tj, kbox = box.kbox, nblk = box.nblk, nsteps = box.nsteps;
 
@@ -465,6 +481,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     d.tilesX = (int32_t)tilesX;
     d.tilesY = (int32_t)tilesY;
     d.group = (int32_t)std::max<int64_t>(1, std::min<int64_t>(8, tilesX));
+    d.order = streaming ? 1 : 0;
     d.cvec = cvec ? 1 : 0;
     d.xscalar_kfast = sX(Ik[0]) < sX(Ix[0]) ? 1 : 0;
     d.yscalar_kfast = sY(Ik[0]) < sY(Iy[0]) ? 1 : 0;
@@ -509,6 +526,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     o << ",\"tile\":{\"id\":" << tile << ",\"mt\":" << ts.mt << ",\"nt\":" << ts.nt << ",\"kt\":" << ts.kt
       << ",\"waves\":[" << ts.wm << "," << ts.wn << "],\"reads\":[" << ts.rx << "," << ts.ry
       << "],\"forced\":" << (forced ? "true" : "false") << ",\"model_us\":[" << costs.str() << "]}";
+    o << ",\"streaming\":" << (streaming ? "true" : "false");
     o << ",\"kbox\":{\"kj\":" << kj << ",\"tj\":" << tj << ",\"elements\":" << kbox << ",\"blocks\":" << nblk
       << ",\"steps\":" << nsteps << "}";
     o << ",\"gather_x\":\"" << mode_name(xmode) << "\",\"gather_y\":\"" << mode_name(ymode)

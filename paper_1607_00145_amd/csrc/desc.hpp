@@ -49,6 +49,7 @@ struct KDesc {
     // ---- grid ----
     int32_t tilesX, tilesY;        // tiles along x and y
     int32_t group;                 // tiles along x that share a column band (L2 reuse)
+    int32_t order;                 // 0: banded tile walk, 1: y-fastest walk (C stream order)
     int32_t cvec;                  // 1: C accesses may use 16-byte vectors along y
     int32_t xscalar_kfast;         // scalar gather of X: 1 = contracted index fastest
     int32_t yscalar_kfast;         // scalar gather of Y: 1 = contracted index fastest

@@ -68,8 +68,11 @@ constexpr int kInvalidK = 0x7fffffff;
 
 // Map the hardware workgroup id to a tile.  Workgroups are dealt round-robin
 // to the 8 XCDs (each with its own L2); renumber so that consecutive logical
-// tiles run on one XCD, then walk tiles in bands of `group` x-tiles so that
-// neighbours share operand rows/columns in L2.
+// tiles run on one XCD.  Then either walk tiles in bands of `group` x-tiles,
+// so that neighbours share operand rows/columns in L2 (compute-bound
+// contractions), or walk y fastest, so that the workgroups running at one time
+// write neighbouring stretches of C (streaming contractions, where DRAM page
+// locality of the C stream decides the bandwidth).
 __device__ __forceinline__ void tile_of_block(const KDesc &d, int &tx, int &ty)
 {
     const int nwg = (int)gridDim.x;
@@ -77,6 +80,11 @@ __device__ __forceinline__ void tile_of_block(const KDesc &d, int &tx, int &ty)
     const int full = nwg & ~7;
     int logical = bid;
     if (bid < full) logical = (bid & 7) * (full >> 3) + (bid >> 3);
+    if (d.order == 1) {
+        tx = logical / d.tilesY;
+        ty = logical - tx * d.tilesY;
+        return;
+    }
     const int band = d.group * d.tilesY;
     const int first = (logical / band) * d.group;
     const int gsz = min(d.tilesX - first, d.group);
