@@ -361,11 +361,10 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     //      (Sec. 3.4: macro-kernel time from flops / (peak * penalty), packing
     //      and unpacking time from bytes / bandwidth).  Here: MFMA time of the
     //      busiest compute unit (tiles are dealt to 256 CUs in rounds, each
-    //      tile including its padding) against the C stream through HBM; the
-    //      shorter one overlaps the longer one only in part. ----
+    //      tile including its padding) against the C stream through HBM at
+    //      the bandwidth the tile sustains; the longer one bounds the time. ----
     const double itemB = dtype == GETT_FLOAT32 ? 4.0 : 8.0;
     const double peakCU = (dtype == GETT_FLOAT32 ? 157.3e12 : 78.6e12) / 256.0;
-    const double bw = 6.0e12;   // sustained HBM bandwidth of a streaming kernel
     const double bytesX = itemB * (double)sizeX * (double)an.sizeK;
     const double bytesY = itemB * (double)sizeY * (double)an.sizeK;
     const double bytesC = itemB * (double)sizeX * (double)sizeY;
@@ -380,8 +379,8 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         const double rounds = std::ceil(tx * ty / 256.0);
         const double kpad = (double)std::max<int64_t>(b.nsteps, 1) * c.kt;
         const double tMfma = rounds * (double)c.mt * c.nt * kpad * 2.0 / (peakCU * c.eff);
-        const double tMem = (bytesC + 0.05 * (bytesX * ty + bytesY * tx)) / bw;
-        const double cost = std::max(tMfma, tMem) + 0.3 * std::min(tMfma, tMem);
+        const double tMem = (bytesC + 0.05 * (bytesX * ty + bytesY * tx)) / (8.0e12 * c.bw);
+        const double cost = std::max(tMfma, tMem);
         costs << (t ? "," : "") << cost * 1e6;
         if (cost < bestCost) {
             bestCost = cost;

@@ -224,8 +224,9 @@ template <int R> __device__ __forceinline__ int block_row(int b, int rho)
     return (b / R) * 16 * R + R * rho + (b % R);
 }
 
-template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int XMODE, int YMODE>
-__global__ void __launch_bounds__(WM *WN * 64)
+template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int WPE, int XMODE,
+          int YMODE>
+__global__ void __launch_bounds__(WM *WN * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
                   T *__restrict__ C, const T alpha, const T beta)
 {

@@ -26,7 +26,7 @@ hipError_t launch_one(const KDesc &d, const void *X, const void *Y, void *C, dou
     constexpr TileShape t = TileTable<T>::tiles[TI];
     const unsigned grid = (unsigned)d.tilesX * (unsigned)d.tilesY;
     if (grid == 0) return hipSuccess;
-    hipLaunchKernelGGL((gett_macro_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, XM, YM>),
+    hipLaunchKernelGGL((gett_macro_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.wpe, XM, YM>),
                        dim3(grid),
                        dim3(t.wm * t.wn * 64), 0, stream, d, static_cast<const T *>(X),
                        static_cast<const T *>(Y), static_cast<T *>(C), static_cast<T>(alpha),

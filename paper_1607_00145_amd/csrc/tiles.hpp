@@ -6,27 +6,33 @@
 // m_C, n_C, k_C (Sec. 3.3); the register tile of one wavefront,
 // (MT/WM) x (NT/WN) built from 16x16 MFMA blocks, plays the role of
 // m_R x n_R (Sec. 3.1).  RX / RY are the rows each lane reads from LDS at
-// once on the x / y side (1, or 16 bytes' worth).  `eff` is the fraction of
-// the MFMA peak the tile sustains when compute-bound, used by the analyser's
-// cost model (measured on MI355X).
+// once on the x / y side (1, or 16 bytes' worth).  `eff` and `bw` feed the
+// analyser's cost model; they were measured on MI355X with the workloads of
+// the benchmark.
 #pragma once
 
 namespace gett {
 
 struct TileShape {
     int mt, nt, kt, wm, wn, rx, ry;
-    float eff;
+    int wpe;     // minimum wavefronts per SIMD the register allocation must allow
+    float eff;   // fraction of the MFMA peak sustained when compute-bound
+    float bw;    // fraction of the HBM peak sustained when streaming C
 };
 
 constexpr TileShape kTilesF32[] = {
-    {128, 128, 16, 2, 2, 4, 4, 0.80f},
-    {64, 64, 16, 1, 1, 4, 4, 0.40f},
+    {128, 128, 16, 2, 2, 4, 4, 1, 0.75f, 0.61f},
+    {64, 64, 16, 1, 1, 4, 4, 1, 0.67f, 0.62f},
+    {128, 128, 16, 2, 2, 4, 4, 3, 0.71f, 0.65f},
+    {64, 256, 16, 1, 4, 4, 4, 3, 0.70f, 0.66f},
 };
 constexpr TileShape kTilesF64[] = {
-    {128, 128, 16, 2, 2, 2, 2, 0.60f},
-    {64, 64, 16, 1, 1, 2, 2, 0.30f},
-    {144, 144, 16, 3, 3, 1, 1, 0.70f},
-    {128, 64, 8, 2, 2, 2, 2, 0.50f},
+    {128, 128, 16, 2, 2, 2, 2, 1, 0.57f, 0.34f},
+    {64, 64, 16, 1, 1, 2, 2, 1, 0.40f, 0.32f},
+    {144, 144, 16, 3, 3, 1, 1, 1, 0.54f, 0.36f},
+    {128, 64, 8, 2, 2, 2, 2, 3, 0.41f, 0.54f},
+    {64, 128, 8, 1, 4, 2, 2, 3, 0.41f, 0.51f},
+    {32, 256, 16, 1, 4, 2, 2, 3, 0.41f, 0.41f},
 };
 constexpr int kNumTilesF32 = sizeof(kTilesF32) / sizeof(kTilesF32[0]);
 constexpr int kNumTilesF64 = sizeof(kTilesF64) / sizeof(kTilesF64[0]);
