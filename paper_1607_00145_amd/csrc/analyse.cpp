@@ -379,7 +379,10 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         const double rounds = std::ceil(tx * ty / 256.0);
         const double kpad = (double)std::max<int64_t>(b.nsteps, 1) * c.kt;
         const double tMfma = rounds * (double)c.mt * c.nt * kpad * 2.0 / (peakCU * c.eff);
-        const double tMem = (bytesC + 0.05 * (bytesX * ty + bytesY * tx)) / (8.0e12 * c.bw);
+        // The persistent streaming kernel needs the contracted set in one box.
+        const bool canStream = c.stream && b.nsteps <= 1;
+        const double bwFrac = canStream ? std::max(c.bw, c.sbw) : c.bw;
+        const double tMem = (bytesC + 0.05 * (bytesX * ty + bytesY * tx)) / (8.0e12 * bwFrac);
         const double cost = std::max(tMfma, tMem);
         costs << (t ? "," : "") << cost * 1e6;
         if (cost < bestCost) {
@@ -399,6 +402,12 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     }
     const TileShape &ts = tile_shape(dtype, tile);
     const Box box = box_for(ts.kt);
+    const bool tileCanStream = ts.stream && box.nsteps <= 1;
+    int kind = (bestMem > bestMfma && tileCanStream && ts.sbw > ts.bw) ? 1 : 0;
+    if (const char *fk = getenv("GETT_FORCE_KIND")) {   // tuning and test hook
+        const int v = atoi(fk);
+        if (v == 0 || (v == 1 && tileCanStream)) kind = v;
+    }
     // A contraction bound by the C stream walks C in memory order: x indices
     // by C stride (the row operand's stride-one index stays first when it is
     // a free index, for its vector gathers) and tiles y-fastest.
@@ -493,6 +502,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     plan.descScalar.cvec = 0;
     plan.tile = tile;
     plan.xmode = xmode;
+    plan.kind = kind;
     plan.ymode = ymode;
     const double item = dtype == GETT_FLOAT32 ? 4.0 : 8.0;
     plan.flops = 2.0 * (double)an.sizeM * (double)an.sizeN * (double)an.sizeK;
@@ -526,6 +536,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
       << ",\"waves\":[" << ts.wm << "," << ts.wn << "],\"reads\":[" << ts.rx << "," << ts.ry
       << "],\"forced\":" << (forced ? "true" : "false") << ",\"model_us\":[" << costs.str() << "]}";
     o << ",\"streaming\":" << (streaming ? "true" : "false");
+    o << ",\"kernel\":\"" << (kind ? "stream" : "macro") << "\"";
     o << ",\"kbox\":{\"kj\":" << kj << ",\"tj\":" << tj << ",\"elements\":" << kbox << ",\"blocks\":" << nblk
       << ",\"steps\":" << nsteps << "}";
     o << ",\"gather_x\":\"" << mode_name(xmode) << "\",\"gather_y\":\"" << mode_name(ymode)

@@ -88,7 +88,7 @@ gett_status_t gett_contract(const gett_plan_t plan, double alpha, const void *A,
         X = nullptr;
         Y = nullptr;
     }
-    gett::LaunchFn fn = gett::launch_fn(P.dtype, P.tile, xmode, ymode);
+    gett::LaunchFn fn = gett::launch_fn(P.dtype, P.tile, xmode, ymode, P.kind);
     if (!fn) return GETT_ERROR_NOT_SUPPORTED;
     if (inject_launch_fault()) return GETT_ERROR_HIP;
     const hipError_t e = fn(d, X, Y, C, alpha, beta, (hipStream_t)stream);
@@ -123,13 +123,13 @@ const char *gett_plan_describe(const gett_plan_t plan)
 
 namespace gett {
 
-LaunchFn launch_fn_f32(int tile, int xm, int ym);
-LaunchFn launch_fn_f64(int tile, int xm, int ym);
+LaunchFn launch_fn_f32(int tile, int xm, int ym, int kind);
+LaunchFn launch_fn_f64(int tile, int xm, int ym, int kind);
 
-LaunchFn launch_fn(gett_dtype_t dtype, int tile, int xmode, int ymode)
+LaunchFn launch_fn(gett_dtype_t dtype, int tile, int xmode, int ymode, int kind)
 {
-    return dtype == GETT_FLOAT32 ? launch_fn_f32(tile, xmode, ymode)
-                                 : launch_fn_f64(tile, xmode, ymode);
+    return dtype == GETT_FLOAT32 ? launch_fn_f32(tile, xmode, ymode, kind)
+                                 : launch_fn_f64(tile, xmode, ymode, kind);
 }
 
 }  // namespace gett

@@ -116,33 +116,37 @@ __device__ __forceinline__ int box_origin(const KDesc &d, uint32_t s, int &ox, i
 }
 
 // Per-thread description of the part of one operand tile it gathers.  Item
-// `it` of thread `tid` is element (or vector) tid + it * NTH of the tile in
-// the mode's order; the tile shapes are chosen so that consecutive items of
-// one thread are a fixed LDS distance apart.
+// `it` of thread `tid` is element (or 16-byte vector) tid + it * NTH of the
+// tile in the mode's order; items past the tile's end are idle.
 template <typename T, int ROWS, int KT, int MODE, int NTH>
 struct Gather {
     static constexpr int VW = Traits<T>::VW;
     static constexpr int PITCH = ROWS + VW;   // LDS row pitch (elements) of the [k][row] layout
     static constexpr int W = (MODE == kGatherScalar) ? 1 : VW;
+    static_assert(MODE == kGatherScalar || (ROWS % VW == 0 && KT % VW == 0), "vector gathers");
     static constexpr int ITEMS = ROWS * KT / W;
-    static constexpr int NI = ITEMS / NTH;
-    static_assert(ITEMS % NTH == 0, "tile must split evenly over the workgroup");
-    static_assert(NTH % (ROWS / VW) == 0 && NTH % (KT / VW) == 0 && NTH % KT == 0 &&
-                      NTH % ROWS == 0,
-                  "items of one thread must be a fixed LDS distance apart");
+    static constexpr int NI = (ITEMS + NTH - 1) / NTH;
+    static constexpr bool kFull = ITEMS % NTH == 0;
+    // Consecutive items of one thread sit a fixed LDS distance apart when the
+    // workgroup covers whole rows (or whole K lines) per item round.
+    static constexpr bool kConst =
+        NI <= 1 || (kFull && (MODE == kGatherRowVec ? NTH % (ROWS / VW) == 0
+                              : MODE == kGatherKVec ? NTH % (KT / VW) == 0
+                                                    : NTH % KT == 0 && NTH % ROWS == 0));
     typedef typename Traits<T>::vec vec;
 
-    int goff[NI];   // element offset in the operand (without the box origin); < 2^31
-    int kc[NI];     // position along index kj inside the box; kInvalidK: never valid
-    int lds0;       // LDS slot of item 0
-    int lstep;      // LDS distance between consecutive items
-    T val[NI][W];   // staged values
+    int goff[NI];                 // element offset in the operand (without the box origin)
+    int kc[NI];                   // position along index kj inside the box; kInvalidK: never valid
+    int lds[kConst ? 1 : NI];     // LDS slot of each item (of item 0 when kConst); -1: idle
+    int lstep;                    // LDS distance between consecutive items (kConst)
+    T val[NI][W];                 // staged values
 
     // rowoff: LDS table of operand offsets per tile row (-1 = outside the tensor)
     // koff/kco: LDS tables of offsets / kj-positions per box element
     __device__ __forceinline__ void setup(int tid, const int *rowoff, const int *koff,
                                           const int *kco, int kfast)
     {
+        lstep = 0;
 #pragma unroll
         for (int it = 0; it < NI; ++it) {
             const int i = tid + it * NTH;
@@ -160,13 +164,18 @@ struct Gather {
                 r = i % ROWS;
                 kk = i / ROWS;
             }
-            const int ro = rowoff[r];
-            goff[it] = (ro < 0 ? 0 : ro) + koff[kk];
+            const bool act = kFull || i < ITEMS;
+            const int ro = act ? rowoff[r] : -1;
+            goff[it] = (ro < 0 ? 0 : ro) + (act ? koff[kk] : 0);
             kc[it] = ro < 0 ? kInvalidK : kco[kk];
-            if (it == 0) lds0 = kk * PITCH + r;
-            if (it == 1) lstep = kk * PITCH + r - lds0;
+            const int slot = act ? kk * PITCH + r : -1;
+            if (kConst) {
+                if (it == 0) lds[0] = slot;
+                if (it == 1) lstep = slot - lds[0];
+            } else {
+                lds[kConst ? 0 : it] = slot;
+            }
         }
-        if (NI == 1) lstep = 0;
     }
 
     __device__ __forceinline__ void load(const T *__restrict__ p, int limit)
@@ -192,7 +201,9 @@ struct Gather {
     {
 #pragma unroll
         for (int it = 0; it < NI; ++it) {
-            T *dst = tile + lds0 + it * lstep;
+            const int slot = kConst ? lds[0] + it * lstep : lds[kConst ? 0 : it];
+            if (!kFull && slot < 0) continue;
+            T *dst = tile + slot;
             if (MODE == kGatherRowVec) {
                 vec v;
 #pragma unroll
@@ -224,80 +235,44 @@ template <int R> __device__ __forceinline__ int block_row(int b, int rho)
     return (b / R) * 16 * R + R * rho + (b % R);
 }
 
-template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int WPE, int XMODE,
-          int YMODE>
-__global__ void __launch_bounds__(WM *WN * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
-gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
-                  T *__restrict__ C, const T alpha, const T beta)
+// identify_subtensor for one tile: operand and C offsets of every tile row
+// (x side) and column (y side), one mixed-radix decomposition each.
+template <int MT, int NT, int NTH>
+__device__ __forceinline__ void tile_tables(const KDesc &d, int tx, int ty, int tid, int *rowX,
+                                            int *offCx, int *rowY, int *offCy)
 {
-    constexpr int NTH = WM * WN * 64;
-    constexpr int VW = Traits<T>::VW;
-    constexpr int WTM = MT / WM;            // wave tile rows
-    constexpr int WTN = NT / WN;            // wave tile columns
-    constexpr int RB = WTM / 16;            // MFMA blocks per wave along x
-    constexpr int CB = WTN / 16;            // MFMA blocks per wave along y
-    static_assert(WTM % (16 * RX) == 0 && WTN % (16 * RY) == 0,
-                  "wave tile must be a multiple of 16*R in both directions");
-    static_assert(RX == 1 || RX == 2 || RX == 4, "read width");
-    static_assert(RY == 1 || RY == 2 || RY == 4, "read width");
-    static_assert(RX <= VW && RY <= VW, "at most 16 bytes per LDS read");
-    static_assert(KT % 4 == 0, "K tile must be a multiple of the MFMA depth");
-    typedef Gather<T, MT, KT, XMODE, NTH> GX;
-    typedef Gather<T, NT, KT, YMODE, NTH> GY;
-    typedef typename Traits<T>::vec vec;
-    typedef typename Traits<T>::acc accv;
-    typedef RVec<T, RX> XV;
-    typedef RVec<T, RY> YV;
-
-    __shared__ __attribute__((aligned(16))) T xs[2][KT * GX::PITCH];
-    __shared__ __attribute__((aligned(16))) T ys[2][KT * GY::PITCH];
-    // Element offsets fit in 31 bits (the plan refuses larger tensors); -1 marks
-    // a row or column outside the tensor.
-    __shared__ int rowX[MT], rowY[NT], offCx[MT], offCy[NT];
-    __shared__ int kX[KT], kY[KT];
-    __shared__ int kco[KT];
-
-    const int tid = (int)threadIdx.x;
-    int tx, ty;
-    tile_of_block(d, tx, ty);
-
-    // ---- identify_subtensor: offsets of this tile's rows, columns, box ----
-    for (int r = tid; r < MT; r += NTH) {
-        uint32_t x = (uint32_t)tx * MT + r;
-        int ox = -1, oc = -1;
-        if ((int64_t)x < d.sizeX) {
-            ox = 0;
+    for (int r = tid; r < MT + NT; r += NTH) {
+        const bool isx = r < MT;
+        const int rr = isx ? r : r - MT;
+        uint32_t v = (uint32_t)(isx ? tx * MT : ty * NT) + rr;
+        int oo = -1, oc = -1;
+        if ((int64_t)v < (isx ? d.sizeX : d.sizeY)) {
+            oo = 0;
             oc = 0;
-            for (int i = 0; i < d.nx; ++i) {
-                const uint32_t e = (uint32_t)d.extX[i];
-                const uint32_t q = x / e;
-                const uint32_t id = x - q * e;
-                x = q;
-                ox += (int)id * (int)d.strXop[i];
-                oc += (int)id * (int)d.strCx[i];
+            const int n = isx ? d.nx : d.ny;
+            for (int i = 0; i < n; ++i) {
+                const uint32_t e = (uint32_t)(isx ? d.extX[i] : d.extY[i]);
+                const uint32_t q = v / e;
+                const uint32_t id = v - q * e;
+                v = q;
+                oo += (int)id * (int)(isx ? d.strXop[i] : d.strYop[i]);
+                oc += (int)id * (int)(isx ? d.strCx[i] : d.strCy[i]);
             }
         }
-        rowX[r] = ox;
-        offCx[r] = oc;
-    }
-    for (int r = tid; r < NT; r += NTH) {
-        uint32_t y = (uint32_t)ty * NT + r;
-        int oy = -1, oc = -1;
-        if ((int64_t)y < d.sizeY) {
-            oy = 0;
-            oc = 0;
-            for (int i = 0; i < d.ny; ++i) {
-                const uint32_t e = (uint32_t)d.extY[i];
-                const uint32_t q = y / e;
-                const uint32_t id = y - q * e;
-                y = q;
-                oy += (int)id * (int)d.strYop[i];
-                oc += (int)id * (int)d.strCy[i];
-            }
+        if (isx) {
+            rowX[rr] = oo;
+            offCx[rr] = oc;
+        } else {
+            rowY[rr] = oo;
+            offCy[rr] = oc;
         }
-        rowY[r] = oy;
-        offCy[r] = oc;
     }
+}
+
+// Offsets and kj-positions of the positions of one K box.
+template <int KT, int NTH>
+__device__ __forceinline__ void box_tables(const KDesc &d, int tid, int *kX, int *kY, int *kco)
+{
     for (int kk = tid; kk < KT; kk += NTH) {
         int ox = 0, oy = 0;
         int pos = kInvalidK;
@@ -319,48 +294,196 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
         kY[kk] = oy;
         kco[kk] = pos;
     }
-    __syncthreads();
+}
 
-    GX gx;
-    GY gy;
-    gx.setup(tid, rowX, kX, kco, d.xscalar_kfast);
-    gy.setup(tid, rowY, kY, kco, d.yscalar_kfast);
-
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wm = wave % WM;
-    const int wn = wave / WM;
-    const int l16 = lane & 15;
-    const int g = lane >> 4;
+// The register tile of one wavefront and the operations on it.
+template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY>
+struct WaveTile {
+    static constexpr int VW = Traits<T>::VW;
+    static constexpr int WTM = MT / WM;   // wave tile rows
+    static constexpr int WTN = NT / WN;   // wave tile columns
+    static constexpr int RB = WTM / 16;   // MFMA blocks per wave along x
+    static constexpr int CB = WTN / 16;   // MFMA blocks per wave along y
+    static_assert(WTM % (16 * RX) == 0 && WTN % (16 * RY) == 0,
+                  "wave tile must be a multiple of 16*R in both directions");
+    static_assert(RX == 1 || RX == 2 || RX == 4, "read width");
+    static_assert(RY == 1 || RY == 2 || RY == 4, "read width");
+    static_assert(RX <= VW && RY <= VW, "at most 16 bytes per LDS read");
+    static_assert(KT % 4 == 0, "K tile must be a multiple of the MFMA depth");
+    static constexpr int NR = 4 * RX;       // rows of one epilogue group owned by a lane
+    static constexpr bool kVecC = RY == VW; // a lane owns VW consecutive columns
+    static constexpr int CGV = CB / RY;     // column groups per wave
+    typedef typename Traits<T>::vec vec;
+    typedef typename Traits<T>::acc accv;
+    typedef RVec<T, RX> XV;
+    typedef RVec<T, RY> YV;
 
     accv acc[RB][CB];
-#pragma unroll
-    for (int a = 0; a < RB; ++a)
-#pragma unroll
-        for (int b = 0; b < CB; ++b)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) acc[a][b][r] = T(0);
+    int wm, wn, l16, g;
 
-    // The lane's C rows, RX blocks (4*RX rows) at a time, and its columns.
-    constexpr int NR = 4 * RX;
-    auto rows_of = [&](int grp, int *ox) {
+    __device__ __forceinline__ void init(int tid)
+    {
+        const int lane = tid & 63;
+        const int wave = tid >> 6;
+        wm = wave % WM;
+        wn = wave / WM;
+        l16 = lane & 15;
+        g = lane >> 4;
+    }
+
+    __device__ __forceinline__ void zero()
+    {
+#pragma unroll
+        for (int a = 0; a < RB; ++a)
+#pragma unroll
+            for (int b = 0; b < CB; ++b)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) acc[a][b][r] = T(0);
+    }
+
+    // acc += X~ * Y~ over the KT positions of one packed box (LDS [k][row]).
+    template <int PX, int PY>
+    __device__ __forceinline__ void macro(const T *xs, const T *ys)
+    {
+        const T *xt = xs + wm * WTM + RX * l16;
+        const T *yt = ys + wn * WTN + RY * l16;
+#pragma unroll
+        for (int ks = 0; ks < KT / 4; ++ks) {
+            const int k = 4 * ks + g;
+            typename XV::type av[RB / RX];
+            typename YV::type bv[CB / RY];
+#pragma unroll
+            for (int gi = 0; gi < RB / RX; ++gi)
+                av[gi] = *reinterpret_cast<const typename XV::type *>(xt + k * PX + gi * 16 * RX);
+#pragma unroll
+            for (int gj = 0; gj < CB / RY; ++gj)
+                bv[gj] = *reinterpret_cast<const typename YV::type *>(yt + k * PY + gj * 16 * RY);
+#pragma unroll
+            for (int a = 0; a < RB; ++a)
+#pragma unroll
+                for (int b = 0; b < CB; ++b)
+                    acc[a][b] = mfma16x16x4(XV::at(av[a / RX], a % RX), YV::at(bv[b / RY], b % RY),
+                                            acc[a][b]);
+        }
+    }
+
+    __device__ __forceinline__ void rows_of(const int *offCx, int grp, int *ox) const
+    {
 #pragma unroll
         for (int i = 0; i < RX; ++i)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
                 ox[i * 4 + r] =
                     offCx[wm * WTM + block_row<RX>(grp * RX + i, Traits<T>::mrow(g, r))];
-    };
-    // With RY == VW and C vectors enabled, column group cg's VW columns are
-    // consecutive: one offset per group.
-    constexpr bool kVecC = RY == VW;
-    constexpr int CGV = CB / RY;   // column groups per wave
-    auto cols_of = [&](int *oy) {
+    }
+    __device__ __forceinline__ void cols_vec(const int *offCy, int *oy) const
+    {
 #pragma unroll
         for (int cg = 0; cg < CGV; ++cg) oy[cg] = offCy[wn * WTN + cg * 16 * RY + RY * l16];
-    };
-    const bool readC = beta != T(0);
-    const bool useCvec = kVecC && d.cvec;
+    }
+
+    // Unpack (Eq. 11): C <- alpha * acc + beta * C through C's offsets, RX
+    // blocks of rows at a time -- every C load of the group first, so they are
+    // in flight together, then the updates and non-temporal stores (C is
+    // written once and not reused).  C is not read when beta == 0.
+    __device__ __forceinline__ void unpack(T *__restrict__ C, const int *offCx, const int *offCy,
+                                           T alpha, T beta, bool cvec) const
+    {
+        const bool readC = beta != T(0);
+#pragma unroll
+        for (int grp = 0; grp < RB / RX; ++grp) {
+            int ox[NR];
+            rows_of(offCx, grp, ox);
+            if (kVecC && cvec) {
+                int oy[CGV];
+                cols_vec(offCy, oy);
+                vec cv[NR][CGV];
+                if (readC) {
+#pragma unroll
+                    for (int q = 0; q < NR; ++q)
+#pragma unroll
+                        for (int cg = 0; cg < CGV; ++cg)
+                            if (ox[q] >= 0 && oy[cg] >= 0)
+                                cv[q][cg] = __builtin_nontemporal_load(
+                                    reinterpret_cast<const vec *>(C + ox[q] + oy[cg]));
+                }
+#pragma unroll
+                for (int q = 0; q < NR; ++q)
+#pragma unroll
+                    for (int cg = 0; cg < CGV; ++cg) {
+                        if (ox[q] < 0 || oy[cg] < 0) continue;
+                        vec out;
+#pragma unroll
+                        for (int j = 0; j < VW; ++j) {
+                            const T a = alpha * acc[grp * RX + q / 4][kVecC ? cg * RY + j : 0][q % 4];
+                            out[j] = readC ? a + beta * cv[q][cg][j] : a;
+                        }
+                        __builtin_nontemporal_store(out, reinterpret_cast<vec *>(C + ox[q] + oy[cg]));
+                    }
+            } else {
+                int oy[CB];
+#pragma unroll
+                for (int b = 0; b < CB; ++b) oy[b] = offCy[wn * WTN + block_row<RY>(b, l16)];
+                T cv[NR][CB];
+                if (readC) {
+#pragma unroll
+                    for (int q = 0; q < NR; ++q)
+#pragma unroll
+                        for (int b = 0; b < CB; ++b)
+                            if (ox[q] >= 0 && oy[b] >= 0)
+                                cv[q][b] = __builtin_nontemporal_load(C + ox[q] + oy[b]);
+                }
+#pragma unroll
+                for (int q = 0; q < NR; ++q)
+#pragma unroll
+                    for (int b = 0; b < CB; ++b) {
+                        if (ox[q] < 0 || oy[b] < 0) continue;
+                        const T a = alpha * acc[grp * RX + q / 4][b][q % 4];
+                        __builtin_nontemporal_store(readC ? a + beta * cv[q][b] : a,
+                                                    C + ox[q] + oy[b]);
+                    }
+            }
+        }
+    }
+};
+
+// ---------------------------------------------------------------------------
+// The macro-kernel: one tile per workgroup, any number of K boxes, LDS
+// double-buffered along the contracted indices.
+template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int WPE, int XMODE,
+          int YMODE>
+__global__ void __launch_bounds__(WM *WN * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
+gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
+                  T *__restrict__ C, const T alpha, const T beta)
+{
+    constexpr int NTH = WM * WN * 64;
+    typedef Gather<T, MT, KT, XMODE, NTH> GX;
+    typedef Gather<T, NT, KT, YMODE, NTH> GY;
+    typedef WaveTile<T, MT, NT, KT, WM, WN, RX, RY> WT;
+
+    __shared__ __attribute__((aligned(16))) T xs[2][KT * GX::PITCH];
+    __shared__ __attribute__((aligned(16))) T ys[2][KT * GY::PITCH];
+    // Element offsets fit in 31 bits (the plan refuses larger tensors); -1 marks
+    // a row or column outside the tensor.
+    __shared__ int rowX[MT], rowY[NT], offCx[MT], offCy[NT];
+    __shared__ int kX[KT], kY[KT];
+    __shared__ int kco[KT];
+
+    const int tid = (int)threadIdx.x;
+    int tx, ty;
+    tile_of_block(d, tx, ty);
+    tile_tables<MT, NT, NTH>(d, tx, ty, tid, rowX, offCx, rowY, offCy);
+    box_tables<KT, NTH>(d, tid, kX, kY, kco);
+    __syncthreads();
+
+    GX gx;
+    GY gy;
+    gx.setup(tid, rowX, kX, kco, d.xscalar_kfast);
+    gy.setup(tid, rowY, kY, kco, d.yscalar_kfast);
+    WT w;
+    w.init(tid);
+    w.zero();
+
     const uint32_t nsteps = (uint32_t)d.nsteps;
     if (nsteps > 0) {
         int ox, oy;
@@ -381,89 +504,98 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
             gx.load(X + ox, lim);
             gy.load(Y + oy, lim);
         }
-        const T *xt = xs[buf] + wm * WTM + RX * l16;
-        const T *yt = ys[buf] + wn * WTN + RY * l16;
-#pragma unroll
-        for (int ks = 0; ks < KT / 4; ++ks) {
-            const int k = 4 * ks + g;
-            typename XV::type av[RB / RX];
-            typename YV::type bv[CB / RY];
-#pragma unroll
-            for (int gi = 0; gi < RB / RX; ++gi)
-                av[gi] = *reinterpret_cast<const typename XV::type *>(xt + k * GX::PITCH + gi * 16 * RX);
-#pragma unroll
-            for (int gj = 0; gj < CB / RY; ++gj)
-                bv[gj] = *reinterpret_cast<const typename YV::type *>(yt + k * GY::PITCH + gj * 16 * RY);
-#pragma unroll
-            for (int a = 0; a < RB; ++a)
-#pragma unroll
-                for (int b = 0; b < CB; ++b)
-                    acc[a][b] = mfma16x16x4(XV::at(av[a / RX], a % RX), YV::at(bv[b / RY], b % RY),
-                                            acc[a][b]);
-        }
+        w.template macro<GX::PITCH, GY::PITCH>(xs[buf], ys[buf]);
         if (more) {
             gx.store(xs[buf ^ 1]);
             gy.store(ys[buf ^ 1]);
         }
         __syncthreads();
     }
+    w.unpack(C, offCx, offCy, alpha, beta, d.cvec != 0);
+}
 
-    // ---- unpack: C <- alpha * acc + beta * C through C's strides (Eq. 11) ----
-    // RX blocks of rows at a time: first every C load of the group (so they are
-    // in flight together), then the updates and non-temporal stores (C is
-    // written once and not reused).
-#pragma unroll
-    for (int grp = 0; grp < RB / RX; ++grp) {
-        int ox[NR];
-        rows_of(grp, ox);
-        if (useCvec) {
-            int oy[CGV];
-            cols_of(oy);
-            vec cv[NR][CGV];
-            if (readC) {
-#pragma unroll
-                for (int q = 0; q < NR; ++q)
-#pragma unroll
-                    for (int cg = 0; cg < CGV; ++cg)
-                        if (ox[q] >= 0 && oy[cg] >= 0)
-                            cv[q][cg] = __builtin_nontemporal_load(
-                                reinterpret_cast<const vec *>(C + ox[q] + oy[cg]));
-            }
-#pragma unroll
-            for (int q = 0; q < NR; ++q)
-#pragma unroll
-                for (int cg = 0; cg < CGV; ++cg) {
-                    if (ox[q] < 0 || oy[cg] < 0) continue;
-                    vec out;
-#pragma unroll
-                    for (int j = 0; j < VW; ++j) {
-                        const T a = alpha * acc[grp * RX + q / 4][kVecC ? cg * RY + j : 0][q % 4];
-                        out[j] = readC ? a + beta * cv[q][cg][j] : a;
-                    }
-                    __builtin_nontemporal_store(out, reinterpret_cast<vec *>(C + ox[q] + oy[cg]));
-                }
-        } else {
-            int oy[CB];
-#pragma unroll
-            for (int b = 0; b < CB; ++b) oy[b] = offCy[wn * WTN + block_row<RY>(b, l16)];
-            T cv[NR][CB];
-            if (readC) {
-#pragma unroll
-                for (int q = 0; q < NR; ++q)
-#pragma unroll
-                    for (int b = 0; b < CB; ++b)
-                        if (ox[q] >= 0 && oy[b] >= 0)
-                            cv[q][b] = __builtin_nontemporal_load(C + ox[q] + oy[b]);
-            }
-#pragma unroll
-            for (int q = 0; q < NR; ++q)
-#pragma unroll
-                for (int b = 0; b < CB; ++b) {
-                    if (ox[q] < 0 || oy[b] < 0) continue;
-                    const T a = alpha * acc[grp * RX + q / 4][b][q % 4];
-                    __builtin_nontemporal_store(readC ? a + beta * cv[q][b] : a, C + ox[q] + oy[b]);
-                }
+// ---------------------------------------------------------------------------
+// The streaming kernel, for contractions whose contracted set fits in one K
+// box (the panel-panel case of Table I: k small) and whose time goes to the C
+// stream.  A persistent workgroup walks tiles t = blockIdx.x, + gridDim.x, ...
+// in C's memory order (y fastest), so the workgroups running together write
+// neighbouring stretches of C, and overlaps each tile's stores with the next
+// tile's packing:
+//   tables(t+1); barrier; issue the gathers of t+1;
+//   macro(t) from the packed panels; barrier;
+//   store the gathered panels of t+1 to LDS; unpack(t); barrier.
+template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int WPE, int XMODE,
+          int YMODE>
+__global__ void __launch_bounds__(WM *WN * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
+gett_stream_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
+                   T *__restrict__ C, const T alpha, const T beta)
+{
+    constexpr int NTH = WM * WN * 64;
+    typedef Gather<T, MT, KT, XMODE, NTH> GX;
+    typedef Gather<T, NT, KT, YMODE, NTH> GY;
+    typedef WaveTile<T, MT, NT, KT, WM, WN, RX, RY> WT;
+
+    __shared__ __attribute__((aligned(16))) T xs[KT * GX::PITCH];
+    __shared__ __attribute__((aligned(16))) T ys[KT * GY::PITCH];
+    __shared__ int rowX[2][MT], rowY[2][NT], offCx[2][MT], offCy[2][NT];
+    __shared__ int kX[KT], kY[KT];
+    __shared__ int kco[KT];
+
+    const int tid = (int)threadIdx.x;
+    const int ntiles = d.tilesX * d.tilesY;
+    const int G = (int)gridDim.x;
+    int t = (int)blockIdx.x;
+    if (t >= ntiles) return;   // uniform per workgroup; the host never launches more
+
+    const bool withK = d.nsteps > 0;   // 0: alpha == 0 or an empty sum, A and B unread
+    int ox0 = 0, oy0 = 0, lim = 0;
+    if (withK) lim = box_origin(d, 0, ox0, oy0);
+    const T *Xb = X + ox0;
+    const T *Yb = Y + oy0;
+
+    box_tables<KT, NTH>(d, tid, kX, kY, kco);
+    tile_tables<MT, NT, NTH>(d, t / d.tilesY, t % d.tilesY, tid, rowX[0], offCx[0], rowY[0],
+                             offCy[0]);
+    __syncthreads();
+
+    GX gx;
+    GY gy;
+    WT w;
+    w.init(tid);
+    if (withK) {
+        gx.setup(tid, rowX[0], kX, kco, d.xscalar_kfast);
+        gy.setup(tid, rowY[0], kY, kco, d.yscalar_kfast);
+        gx.load(Xb, lim);
+        gy.load(Yb, lim);
+        gx.store(xs);
+        gy.store(ys);
+    }
+    __syncthreads();
+
+    for (int j = 0; t < ntiles; ++j, t += G) {
+        const int cur = j & 1;
+        const int tn = t + G;
+        const bool more = tn < ntiles;
+        if (more) {
+            tile_tables<MT, NT, NTH>(d, tn / d.tilesY, tn % d.tilesY, tid, rowX[cur ^ 1],
+                                     offCx[cur ^ 1], rowY[cur ^ 1], offCy[cur ^ 1]);
         }
+        __syncthreads();
+        if (more && withK) {
+            gx.setup(tid, rowX[cur ^ 1], kX, kco, d.xscalar_kfast);
+            gy.setup(tid, rowY[cur ^ 1], kY, kco, d.yscalar_kfast);
+            gx.load(Xb, lim);
+            gy.load(Yb, lim);
+        }
+        w.zero();
+        if (withK) w.template macro<GX::PITCH, GY::PITCH>(xs, ys);
+        __syncthreads();
+        if (more && withK) {
+            gx.store(xs);
+            gy.store(ys);
+        }
+        w.unpack(C, offCx[cur], offCy[cur], alpha, beta, d.cvec != 0);
+        __syncthreads();
     }
 }
 

@@ -19,26 +19,54 @@ template <> struct TileTable<double> {
     static constexpr int n = kNumTilesF64;
 };
 
-template <typename T, int TI, int XM, int YM>
+// Workgroups of a persistent kernel: as many as fit on the device at once,
+// and no more than there are tiles.
+template <typename K>
+unsigned persistent_grid(K kernel, int threads, unsigned tiles)
+{
+    int dev = 0, cus = 0, per = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, 0) != hipSuccess) return 0;
+    const unsigned n = (unsigned)(cus * (per > 0 ? per : 1));
+    return n < tiles ? n : tiles;
+}
+
+template <typename T, int TI, int XM, int YM, int KIND>
 hipError_t launch_one(const KDesc &d, const void *X, const void *Y, void *C, double alpha,
                       double beta, hipStream_t stream)
 {
     constexpr TileShape t = TileTable<T>::tiles[TI];
-    const unsigned grid = (unsigned)d.tilesX * (unsigned)d.tilesY;
-    if (grid == 0) return hipSuccess;
-    hipLaunchKernelGGL((gett_macro_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.wpe, XM, YM>),
-                       dim3(grid),
-                       dim3(t.wm * t.wn * 64), 0, stream, d, static_cast<const T *>(X),
-                       static_cast<const T *>(Y), static_cast<T *>(C), static_cast<T>(alpha),
-                       static_cast<T>(beta));
+    const unsigned tiles = (unsigned)d.tilesX * (unsigned)d.tilesY;
+    if (tiles == 0) return hipSuccess;
+    const int threads = t.wm * t.wn * 64;
+    if constexpr (KIND == 0) {
+        hipLaunchKernelGGL(
+            (gett_macro_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.wpe, XM, YM>),
+            dim3(tiles), dim3(threads), 0, stream, d, static_cast<const T *>(X),
+            static_cast<const T *>(Y), static_cast<T *>(C), static_cast<T>(alpha),
+            static_cast<T>(beta));
+    } else {
+        auto k = gett_stream_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.stream, XM, YM>;
+        const unsigned grid = persistent_grid(k, threads, tiles);
+        if (grid == 0) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(k, dim3(grid), dim3(threads), 0, stream, d,
+                           static_cast<const T *>(X), static_cast<const T *>(Y),
+                           static_cast<T *>(C), static_cast<T>(alpha), static_cast<T>(beta));
+    }
     return hipGetLastError();
 }
 
 template <typename T, int TI>
-LaunchFn pick_modes(int xm, int ym)
+LaunchFn pick_modes(int xm, int ym, int kind)
 {
-#define GETT_CASE(a, b) \
-    if (xm == a && ym == b) return &launch_one<T, TI, a, b>;
+    constexpr bool kStream = TileTable<T>::tiles[TI].stream != 0;
+#define GETT_CASE(a, b)                                                                       \
+    if (xm == a && ym == b) {                                                                 \
+        if (kind == 0) return &launch_one<T, TI, a, b, 0>;                                   \
+        if (kStream) return &launch_one<T, TI, a, b, kStream ? 1 : 0>;                       \
+        return nullptr;                                                                       \
+    }
     GETT_CASE(0, 0) GETT_CASE(0, 1) GETT_CASE(0, 2)
     GETT_CASE(1, 0) GETT_CASE(1, 1) GETT_CASE(1, 2)
     GETT_CASE(2, 0) GETT_CASE(2, 1) GETT_CASE(2, 2)

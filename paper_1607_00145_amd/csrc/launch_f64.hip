@@ -3,16 +3,21 @@
 
 namespace gett {
 
-LaunchFn launch_fn_f64(int tile, int xm, int ym)
+LaunchFn launch_fn_f64(int tile, int xm, int ym, int kind)
 {
-    static_assert(kNumTilesF64 == 6, "update the tile switch");
+    static_assert(kNumTilesF64 == 11, "update the tile switch");
     switch (tile) {
-    case 0: return pick_modes<double, 0>(xm, ym);
-    case 1: return pick_modes<double, 1>(xm, ym);
-    case 2: return pick_modes<double, 2>(xm, ym);
-    case 3: return pick_modes<double, 3>(xm, ym);
-    case 4: return pick_modes<double, 4>(xm, ym);
-    case 5: return pick_modes<double, 5>(xm, ym);
+    case 0: return pick_modes<double, 0>(xm, ym, kind);
+    case 1: return pick_modes<double, 1>(xm, ym, kind);
+    case 2: return pick_modes<double, 2>(xm, ym, kind);
+    case 3: return pick_modes<double, 3>(xm, ym, kind);
+    case 4: return pick_modes<double, 4>(xm, ym, kind);
+    case 5: return pick_modes<double, 5>(xm, ym, kind);
+    case 6: return pick_modes<double, 6>(xm, ym, kind);
+    case 7: return pick_modes<double, 7>(xm, ym, kind);
+    case 8: return pick_modes<double, 8>(xm, ym, kind);
+    case 9: return pick_modes<double, 9>(xm, ym, kind);
+    case 10: return pick_modes<double, 10>(xm, ym, kind);
     }
     return nullptr;
 }

@@ -41,6 +41,7 @@ struct gett_plan_s {
     gett::KDesc descScalar;  // the same work with scalar gathers and C accesses
     int tile;                // index into the tile table of the dtype
     int xmode, ymode;        // gather modes of the preferred kernel
+    int kind;                // 0: macro-kernel, 1: persistent streaming kernel
     double flops;            // 2 * S_Im * S_In * S_Ik (Eq. 14)
     double bytesAlgo;        // |A| + |B| + |C| (+|C| when beta may be read)
     std::string text;        // JSON description
@@ -53,7 +54,8 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
                       const int64_t *sC, const char *mA, const int64_t *eA, const int64_t *sA,
                       const char *mB, const int64_t *eB, const int64_t *sB, uint32_t flags);
 
-// Launch table lookup (defined with the kernel instantiations).
-LaunchFn launch_fn(gett_dtype_t dtype, int tile, int xmode, int ymode);
+// Launch table lookup (defined with the kernel instantiations).  kind 0: the
+// macro-kernel, 1: the persistent streaming kernel.
+LaunchFn launch_fn(gett_dtype_t dtype, int tile, int xmode, int ymode, int kind);
 
 }  // namespace gett

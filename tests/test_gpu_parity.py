@@ -186,17 +186,24 @@ def test_plan_class_on_torch_views(gpu):
     assert p.describe()["dtype"] == "f64"
 
 
-TILES = {np.float32: 4, np.float64: 6}
+TILES = {np.float32: 4, np.float64: 11}
 
 
 @pytest.mark.parametrize("dtype,tile", [(dt, t) for dt in DTYPES for t in range(TILES[dt])])
-@pytest.mark.parametrize("case", ["random", "scaled3", "scaled4"])
-def test_every_tile_shape(gpu, monkeypatch, dtype, tile, case):
-    """Each compiled tile shape, forced through the analyser's test hook."""
+@pytest.mark.parametrize("kind", [0, 1])
+@pytest.mark.parametrize("case", ["random", "smallk", "scaled2", "scaled3", "scaled4"])
+def test_every_tile_shape(gpu, monkeypatch, dtype, tile, kind, case):
+    """Each compiled tile shape and kernel kind (macro-kernel / persistent
+    streaming kernel), forced through the analyser's test hooks."""
     monkeypatch.setenv("GETT_FORCE_TILE", str(tile))
-    rng = np.random.default_rng(30_000 + tile)
-    if case == "random":
-        mc, ma, mb, ext = wl.random_problem(rng, max_rank=6, max_ext=9)
+    monkeypatch.setenv("GETT_FORCE_KIND", str(kind))
+    rng = np.random.default_rng(30_000 + 10 * tile + kind)
+    if case in ("random", "smallk"):
+        while True:
+            mc, ma, mb, ext = wl.random_problem(rng, max_rank=6, max_ext=9)
+            kext = int(np.prod([ext[x] for x in split(ma) if x not in split(mc)]))
+            if case == "random" or kext <= 16:
+                break
         shp = lambda m: [ext[x] for x in split(m)]
         modes, shapes, alpha, beta = (mc, ma, mb), (shp(mc), shp(ma), shp(mb)), 1.5, -0.5
     else:
@@ -205,3 +212,16 @@ def test_every_tile_shape(gpu, monkeypatch, dtype, tile, case):
         shapes = (w.shape("C"), w.shape("A"), w.shape("B"))
         alpha, beta = w.alpha, w.beta
     check_case(gpu, rng, modes, shapes, dtype, alpha, beta)
+
+
+@pytest.mark.parametrize("number", [2, 4])
+def test_streaming_kernel_many_tiles_per_workgroup(gpu, monkeypatch, number):
+    """The persistent streaming kernel with far more tiles than workgroups
+    (each workgroup walks many tiles), at a size the oracle checks in full."""
+    monkeypatch.setenv("GETT_FORCE_KIND", "1")
+    big = {2: {"a": 128, "b": 100, "c": 64, "d": 20, "e": 16},
+           4: {"a": 16, "b": 16, "c": 16, "d": 24, "i": 20, "j": 8, "k": 8}}[number]
+    w = wl.scaled(wl.WORKLOADS[number - 1], big)
+    rng = np.random.default_rng(w.seed + 7)
+    check_case(gpu, rng, (w.modes_C, w.modes_A, w.modes_B),
+               (w.shape("C"), w.shape("A"), w.shape("B")), w.np_dtype, w.alpha, w.beta)
