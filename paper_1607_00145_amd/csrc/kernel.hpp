@@ -30,6 +30,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "desc.hpp"
 
 namespace gett {
@@ -118,7 +120,7 @@ __device__ __forceinline__ int box_origin(const KDesc &d, uint32_t s, int &ox, i
 // Per-thread description of the part of one operand tile it gathers.  Item
 // `it` of thread `tid` is element (or 16-byte vector) tid + it * NTH of the
 // tile in the mode's order; items past the tile's end are idle.
-template <typename T, int ROWS, int KT, int MODE, int NTH>
+template <typename T, int ROWS, int KT, int MODE, int NTH, int STAGES = 1>
 struct Gather {
     static constexpr int VW = Traits<T>::VW;
     static constexpr int PITCH = ROWS + VW;   // LDS row pitch (elements) of the [k][row] layout
@@ -139,7 +141,7 @@ struct Gather {
     int kc[NI];                   // position along index kj inside the box; kInvalidK: never valid
     int lds[kConst ? 1 : NI];     // LDS slot of each item (of item 0 when kConst); -1: idle
     int lstep;                    // LDS distance between consecutive items (kConst)
-    T val[NI][W];                 // staged values
+    T val[STAGES][NI][W];         // staged values, one set per stage in flight
 
     // rowoff: LDS table of operand offsets per tile row (-1 = outside the tensor)
     // koff/kco: LDS tables of offsets / kj-positions per box element
@@ -178,25 +180,27 @@ struct Gather {
         }
     }
 
+    template <int B = 0>
     __device__ __forceinline__ void load(const T *__restrict__ p, int limit)
     {
 #pragma unroll
         for (int it = 0; it < NI; ++it) {
             if (kc[it] < limit) {
                 if (W == 1) {
-                    val[it][0] = p[goff[it]];
+                    val[B][it][0] = p[goff[it]];
                 } else {
                     const vec v = *reinterpret_cast<const vec *>(p + goff[it]);
 #pragma unroll
-                    for (int e = 0; e < W; ++e) val[it][e] = v[e];
+                    for (int e = 0; e < W; ++e) val[B][it][e] = v[e];
                 }
             } else {
 #pragma unroll
-                for (int e = 0; e < W; ++e) val[it][e] = T(0);
+                for (int e = 0; e < W; ++e) val[B][it][e] = T(0);
             }
         }
     }
 
+    template <int B = 0>
     __device__ __forceinline__ void store(T *tile) const
     {
 #pragma unroll
@@ -207,13 +211,13 @@ struct Gather {
             if (MODE == kGatherRowVec) {
                 vec v;
 #pragma unroll
-                for (int e = 0; e < W; ++e) v[e] = val[it][e];
+                for (int e = 0; e < W; ++e) v[e] = val[B][it][e];
                 *reinterpret_cast<vec *>(dst) = v;
             } else if (MODE == kGatherKVec) {
 #pragma unroll
-                for (int e = 0; e < W; ++e) dst[e * PITCH] = val[it][e];
+                for (int e = 0; e < W; ++e) dst[e * PITCH] = val[B][it][e];
             } else {
-                *dst = val[it][0];
+                *dst = val[B][it][0];
             }
         }
     }
@@ -448,17 +452,21 @@ struct WaveTile {
 };
 
 // ---------------------------------------------------------------------------
-// The macro-kernel: one tile per workgroup, any number of K boxes, LDS
-// double-buffered along the contracted indices.
-template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int WPE, int XMODE,
-          int YMODE>
+// The macro-kernel: one tile per workgroup, any number of K boxes, two LDS
+// buffers.  With PF = 1 the gathers of box s+1 are issued before the MFMAs
+// of box s; with PF = 2 there are two register stages and the gathers of box
+// s+2 are issued before the MFMAs of box s, so a gather has two boxes' worth
+// of MFMA time to arrive before its values are written to LDS.
+template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int WPE, int PF,
+          int XMODE, int YMODE>
 __global__ void __launch_bounds__(WM *WN * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
                   T *__restrict__ C, const T alpha, const T beta)
 {
+    static_assert(PF == 1 || PF == 2, "prefetch depth");
     constexpr int NTH = WM * WN * 64;
-    typedef Gather<T, MT, KT, XMODE, NTH> GX;
-    typedef Gather<T, NT, KT, YMODE, NTH> GY;
+    typedef Gather<T, MT, KT, XMODE, NTH, PF> GX;
+    typedef Gather<T, NT, KT, YMODE, NTH, PF> GY;
     typedef WaveTile<T, MT, NT, KT, WM, WN, RX, RY> WT;
 
     __shared__ __attribute__((aligned(16))) T xs[2][KT * GX::PITCH];
@@ -485,31 +493,58 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     w.zero();
 
     const uint32_t nsteps = (uint32_t)d.nsteps;
-    if (nsteps > 0) {
+    auto fetch = [&](auto stage, uint32_t s) {
+        constexpr int B = decltype(stage)::value;
         int ox, oy;
-        const int lim = box_origin(d, 0, ox, oy);
-        gx.load(X + ox, lim);
-        gy.load(Y + oy, lim);
-        gx.store(xs[0]);
-        gy.store(ys[0]);
-    }
-    __syncthreads();
-
-    for (uint32_t s = 0; s < nsteps; ++s) {
-        const int buf = (int)(s & 1);
-        const bool more = s + 1 < nsteps;
-        if (more) {
-            int ox, oy;
-            const int lim = box_origin(d, s + 1, ox, oy);
-            gx.load(X + ox, lim);
-            gy.load(Y + oy, lim);
-        }
-        w.template macro<GX::PITCH, GY::PITCH>(xs[buf], ys[buf]);
-        if (more) {
-            gx.store(xs[buf ^ 1]);
-            gy.store(ys[buf ^ 1]);
+        const int lim = box_origin(d, s, ox, oy);
+        gx.template load<B>(X + ox, lim);
+        gy.template load<B>(Y + oy, lim);
+    };
+    typedef std::integral_constant<int, 0> S0;
+    typedef std::integral_constant<int, 1> S1;
+    if constexpr (PF == 1) {
+        if (nsteps > 0) {
+            fetch(S0(), 0);
+            gx.template store<0>(xs[0]);
+            gy.template store<0>(ys[0]);
         }
         __syncthreads();
+        for (uint32_t s = 0; s < nsteps; ++s) {
+            const int buf = (int)(s & 1);
+            const bool more = s + 1 < nsteps;
+            if (more) fetch(S0(), s + 1);
+            w.template macro<GX::PITCH, GY::PITCH>(xs[buf], ys[buf]);
+            if (more) {
+                gx.template store<0>(xs[buf ^ 1]);
+                gy.template store<0>(ys[buf ^ 1]);
+            }
+            __syncthreads();
+        }
+    } else {
+        // One box: start the gathers of box s+2 into this stage's registers,
+        // run the MFMAs of box s from LDS buffer B, move box s+1's registers
+        // into the other buffer.
+        auto step = [&](auto stage, uint32_t s) {
+            constexpr int B = decltype(stage)::value;
+            if (s + 2 < nsteps) fetch(stage, s + 2);
+            w.template macro<GX::PITCH, GY::PITCH>(xs[B], ys[B]);
+            if (s + 1 < nsteps) {
+                gx.template store<B ^ 1>(xs[B ^ 1]);
+                gy.template store<B ^ 1>(ys[B ^ 1]);
+            }
+            __syncthreads();
+        };
+        if (nsteps > 0) {
+            fetch(S0(), 0);
+            if (nsteps > 1) fetch(S1(), 1);
+            gx.template store<0>(xs[0]);
+            gy.template store<0>(ys[0]);
+        }
+        __syncthreads();
+        for (uint32_t s = 0; s < nsteps; s += 2) {
+            step(S0(), s);
+            if (s + 1 < nsteps) step(S1(), s + 1);
+        }
     }
     w.unpack(C, offCx, offCy, alpha, beta, d.cvec != 0);
 }
