@@ -452,25 +452,26 @@ struct WaveTile {
 };
 
 // ---------------------------------------------------------------------------
-// The macro-kernel: one tile per workgroup, any number of K boxes, two LDS
-// buffers.  With PF = 1 the gathers of box s+1 are issued before the MFMAs
+// The macro-kernel: one tile per workgroup, any number of K boxes, NBUF LDS
+// buffers (one suits a contracted set that fits one box).  With PF = 1 the gathers of box s+1 are issued before the MFMAs
 // of box s; with PF = 2 there are two register stages and the gathers of box
 // s+2 are issued before the MFMAs of box s, so a gather has two boxes' worth
 // of MFMA time to arrive before its values are written to LDS.
 template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int WPE, int PF,
-          int XMODE, int YMODE>
+          int NBUF, int XMODE, int YMODE>
 __global__ void __launch_bounds__(WM *WN * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
                   T *__restrict__ C, const T alpha, const T beta)
 {
     static_assert(PF == 1 || PF == 2, "prefetch depth");
+    static_assert(NBUF == 2 || (NBUF == 1 && PF == 1), "one LDS buffer goes with one stage");
     constexpr int NTH = WM * WN * 64;
     typedef Gather<T, MT, KT, XMODE, NTH, PF> GX;
     typedef Gather<T, NT, KT, YMODE, NTH, PF> GY;
     typedef WaveTile<T, MT, NT, KT, WM, WN, RX, RY> WT;
 
-    __shared__ __attribute__((aligned(16))) T xs[2][KT * GX::PITCH];
-    __shared__ __attribute__((aligned(16))) T ys[2][KT * GY::PITCH];
+    __shared__ __attribute__((aligned(16))) T xs[NBUF][KT * GX::PITCH];
+    __shared__ __attribute__((aligned(16))) T ys[NBUF][KT * GY::PITCH];
     // Element offsets fit in 31 bits (the plan refuses larger tensors); -1 marks
     // a row or column outside the tensor.
     __shared__ int rowX[MT], rowY[NT], offCx[MT], offCy[NT];
@@ -510,13 +511,14 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
         }
         __syncthreads();
         for (uint32_t s = 0; s < nsteps; ++s) {
-            const int buf = (int)(s & 1);
+            const int buf = NBUF == 2 ? (int)(s & 1) : 0;
             const bool more = s + 1 < nsteps;
             if (more) fetch(S0(), s + 1);
             w.template macro<GX::PITCH, GY::PITCH>(xs[buf], ys[buf]);
+            if (NBUF == 1 && more) __syncthreads();   // the single buffer is free again
             if (more) {
-                gx.template store<0>(xs[buf ^ 1]);
-                gy.template store<0>(ys[buf ^ 1]);
+                gx.template store<0>(xs[NBUF == 2 ? buf ^ 1 : 0]);
+                gy.template store<0>(ys[NBUF == 2 ? buf ^ 1 : 0]);
             }
             __syncthreads();
         }
@@ -527,10 +529,10 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
         auto step = [&](auto stage, uint32_t s) {
             constexpr int B = decltype(stage)::value;
             if (s + 2 < nsteps) fetch(stage, s + 2);
-            w.template macro<GX::PITCH, GY::PITCH>(xs[B], ys[B]);
+            w.template macro<GX::PITCH, GY::PITCH>(xs[B % NBUF], ys[B % NBUF]);
             if (s + 1 < nsteps) {
-                gx.template store<B ^ 1>(xs[B ^ 1]);
-                gy.template store<B ^ 1>(ys[B ^ 1]);
+                gx.template store<B ^ 1>(xs[(B ^ 1) % NBUF]);
+                gy.template store<B ^ 1>(ys[(B ^ 1) % NBUF]);
             }
             __syncthreads();
         };

@@ -42,7 +42,8 @@ hipError_t launch_one(const KDesc &d, const void *X, const void *Y, void *C, dou
     const int threads = t.wm * t.wn * 64;
     if constexpr (KIND == 0) {
         hipLaunchKernelGGL(
-            (gett_macro_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.wpe, t.pf, XM, YM>),
+            (gett_macro_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.wpe, t.pf, t.nbuf, XM,
+                               YM>),
             dim3(tiles), dim3(threads), 0, stream, d, static_cast<const T *>(X),
             static_cast<const T *>(Y), static_cast<T *>(C), static_cast<T>(alpha),
             static_cast<T>(beta));
