@@ -490,6 +490,8 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     d.tilesY = (int32_t)tilesY;
     d.group = (int32_t)std::max<int64_t>(1, std::min<int64_t>(8, tilesX));
     d.order = streaming ? 1 : 0;
+    d.xcdremap = -1;   // decided per call (see gett_contract)
+    if (const char *xr = getenv("GETT_XCD_REMAP")) d.xcdremap = atoi(xr) != 0;   // tuning hook
     d.cvec = cvec ? 1 : 0;
     d.xscalar_kfast = sX(Ik[0]) < sX(Ix[0]) ? 1 : 0;
     d.yscalar_kfast = sY(Ik[0]) < sY(Iy[0]) ? 1 : 0;

@@ -83,6 +83,10 @@ gett_status_t gett_contract(const gett_plan_t plan, double alpha, const void *A,
     if (xmode != gett::kGatherScalar && ((uintptr_t)X % 16)) xmode = gett::kGatherScalar;
     if (ymode != gett::kGatherScalar && ((uintptr_t)Y % 16)) ymode = gett::kGatherScalar;
     if (d.cvec && ((uintptr_t)C % 16)) d.cvec = 0;
+    // Tile walk across the XCDs: consecutive tiles on one XCD suits the
+    // compute-bound and write-only walks; a read-modify-write C stream
+    // (streaming walk, beta != 0) runs faster in hardware order (measured).
+    if (d.xcdremap < 0) d.xcdremap = (d.order == 1 && beta != 0.0) ? 0 : 1;
     if (!readAB) {   // alpha == 0 or empty sum: C <- beta * C, A and B untouched
         d.nsteps = 0;
         X = nullptr;

@@ -50,6 +50,8 @@ struct KDesc {
     int32_t tilesX, tilesY;        // tiles along x and y
     int32_t group;                 // tiles along x that share a column band (L2 reuse)
     int32_t order;                 // 0: banded tile walk, 1: y-fastest walk (C stream order)
+    int32_t xcdremap;              // 1: consecutive tiles on one XCD, 0: hardware order
+                                   // (-1 in a plan: chosen per call)
     int32_t cvec;                  // 1: C accesses may use 16-byte vectors along y
     int32_t xscalar_kfast;         // scalar gather of X: 1 = contracted index fastest
     int32_t yscalar_kfast;         // scalar gather of Y: 1 = contracted index fastest

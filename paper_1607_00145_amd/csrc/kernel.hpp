@@ -81,7 +81,7 @@ __device__ __forceinline__ void tile_of_block(const KDesc &d, int &tx, int &ty)
     const int bid = (int)blockIdx.x;
     const int full = nwg & ~7;
     int logical = bid;
-    if (bid < full) logical = (bid & 7) * (full >> 3) + (bid >> 3);
+    if (d.xcdremap && bid < full) logical = (bid & 7) * (full >> 3) + (bid >> 3);
     if (d.order == 1) {
         tx = logical / d.tilesY;
         ty = logical - tx * d.tilesY;
