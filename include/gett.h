@@ -122,6 +122,33 @@ gett_status_t gett_plan(gett_plan_t *plan, gett_dtype_t dtype,
 gett_status_t gett_contract(const gett_plan_t plan, double alpha, const void *A, const void *B,
                             double beta, void *C, void *stream);
 
+/*
+ * gett_plan_tune -- time the plan's best candidates and keep the fastest.
+ *
+ * gett_plan ranks every compiled kernel candidate (tile shape x kernel kind)
+ * with a performance model (Sec. 3.4) and uses the best estimate.  As the
+ * paper's code generator does (Sec. 6, Sec. 7.3: compile and time the most
+ * promising candidates; Table II --maxImplementations), this call runs the
+ * first `max_candidates` of that ranking on the caller's data, measures each
+ * with HIP events on `stream`, and switches the plan to the fastest one.  The
+ * choice is remembered for the rest of the process: a later gett_plan with the
+ * same descriptor (dtype, mode strings, extents, strides, flags) starts from
+ * it (the paper's database of known implementations, kept in memory).
+ *
+ *   plan            a plan from gett_plan(); updated in place.
+ *   max_candidates  >= 1; the paper's default is 16.
+ *   A, B            device operands laid out as the plan describes.
+ *   C               device buffer laid out as the plan's C.  It is
+ *                   OVERWRITTEN (every candidate runs with alpha 1, beta 0).
+ *   stream          a hipStream_t (NULL: the default stream); synchronised.
+ *
+ * Errors: GETT_ERROR_INVALID_VALUE (NULL plan, max_candidates < 1, or a
+ * pointer gett_contract rejects), GETT_ERROR_HIP (event or launch failure; the
+ * plan is then unchanged).  Not safe to call concurrently on one plan.
+ */
+gett_status_t gett_plan_tune(gett_plan_t plan, int max_candidates, const void *A, const void *B,
+                             void *C, void *stream);
+
 /* gett_destroy -- free a plan.  NULL is accepted and ignored. */
 gett_status_t gett_destroy(gett_plan_t plan);
 

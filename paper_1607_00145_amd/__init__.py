@@ -26,6 +26,12 @@ GETT_FLAG_NONE = 0
 GETT_FLAG_NO_SWAP = 1
 GETT_FLAG_SCALAR = 2
 GETT_MAX_RANK = 12
+GETT_SUCCESS = 0
+GETT_ERROR_INVALID_VALUE = 1
+GETT_ERROR_INVALID_INDICES = 2
+GETT_ERROR_NOT_SUPPORTED = 3
+GETT_ERROR_HIP = 4
+GETT_ERROR_ALLOC = 5
 
 STATUS = {0: "GETT_SUCCESS", 1: "GETT_ERROR_INVALID_VALUE", 2: "GETT_ERROR_INVALID_INDICES",
           3: "GETT_ERROR_NOT_SUPPORTED", 4: "GETT_ERROR_HIP", 5: "GETT_ERROR_ALLOC"}
@@ -59,6 +65,9 @@ def load_library() -> ctypes.CDLL:
     lib.gett_contract.argtypes = [ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p,
                                   ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p,
                                   ctypes.c_void_p]
+    lib.gett_plan_tune.restype = ctypes.c_int
+    lib.gett_plan_tune.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
+                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.gett_destroy.restype = ctypes.c_int
     lib.gett_destroy.argtypes = [ctypes.c_void_p]
     lib.gett_status_string.restype = ctypes.c_char_p
@@ -94,6 +103,13 @@ def gett_contract(plan, alpha: float, A: int, B: int, beta: float, C: int, strea
     """Device pointers as integers; stream as a hipStream_t integer (0 = default)."""
     return load_library().gett_contract(plan, float(alpha), A or None, B or None, float(beta),
                                         C or None, stream or None)
+
+
+def gett_plan_tune(plan, max_candidates: int, A: int, B: int, C: int, stream: int = 0) -> int:
+    """Times the plan's best `max_candidates` candidates on (A, B, C) and keeps the
+    fastest; C is overwritten.  Device pointers and stream as integers."""
+    return load_library().gett_plan_tune(plan, int(max_candidates), A or None, B or None,
+                                         C or None, stream or None)
 
 
 def gett_destroy(plan) -> int:
@@ -169,6 +185,22 @@ class Plan:
         if st != 0:
             raise GettError(st, "gett_contract")
         return C
+
+    def tune(self, A, B, C, max_candidates: int = 16, stream=None):
+        """Runs the best `max_candidates` kernels of the performance model's ranking
+        on these tensors and keeps the fastest (C is overwritten)."""
+        import torch
+        for name, t in (("A", A), ("B", B), ("C", C)):
+            if not t.is_cuda:
+                raise ValueError(f"{name} must be a device tensor")
+        if tuple((tuple(t.shape), tuple(t.stride())) for t in (C, A, B)) != self.sig:
+            raise ValueError("tensor shapes/strides differ from the plan's")
+        s = stream if stream is not None else torch.cuda.current_stream()
+        st = gett_plan_tune(self._h, max_candidates, A.data_ptr(), B.data_ptr(), C.data_ptr(),
+                            s.cuda_stream)
+        if st != 0:
+            raise GettError(st, "gett_plan_tune")
+        return self.describe()
 
     def close(self):
         if getattr(self, "_h", None):

@@ -188,7 +188,8 @@ const char *mode_name(int m)
 
 gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, const int64_t *eC,
                       const int64_t *sC, const char *mA, const int64_t *eA, const int64_t *sA,
-                      const char *mB, const int64_t *eB, const int64_t *sB, uint32_t flags)
+                      const char *mB, const int64_t *eB, const int64_t *sB, uint32_t flags,
+                      const Choice *force)
 {
     if (dtype != GETT_FLOAT32 && dtype != GETT_FLOAT64) return GETT_ERROR_INVALID_VALUE;
     Tensor A, B, C;
@@ -368,9 +369,8 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     const double bytesX = itemB * (double)sizeX * (double)an.sizeK;
     const double bytesY = itemB * (double)sizeY * (double)an.sizeK;
     const double bytesC = itemB * (double)sizeX * (double)sizeY;
-    int tile = 0;
-    double bestCost = 1e300, bestMfma = 0, bestMem = 0;
-    std::ostringstream costs;
+    // Every (tile, kernel kind) pair is a candidate; the model ranks them.
+    std::vector<Candidate> ranked;
     for (int t = 0; t < num_tiles(dtype); ++t) {
         const TileShape &c = tile_shape(dtype, t);
         const Box b = box_for(c.kt);
@@ -381,33 +381,52 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         const double tMfma = rounds * (double)c.mt * c.nt * kpad * 2.0 / (peakCU * c.eff);
         // The persistent streaming kernel needs the contracted set in one box.
         const bool canStream = c.stream && b.nsteps <= 1;
-        const double bwFrac = canStream ? std::max(c.bw, c.sbw) : c.bw;
-        const double tMem = (bytesC + 0.05 * (bytesX * ty + bytesY * tx)) / (8.0e12 * bwFrac);
-        const double cost = std::max(tMfma, tMem);
-        costs << (t ? "," : "") << cost * 1e6;
-        if (cost < bestCost) {
-            bestCost = cost;
-            bestMfma = tMfma;
-            bestMem = tMem;
-            tile = t;
+        for (int k = 0; k < (canStream ? 2 : 1); ++k) {
+            const double bwFrac = k ? c.sbw : c.bw;
+            const double tMem =
+                (bytesC + 0.05 * (bytesX * ty + bytesY * tx)) / (8.0e12 * bwFrac);
+            Candidate cd;
+            cd.tile = t;
+            cd.kind = k;
+            cd.tMfma = tMfma;
+            cd.tMem = tMem;
+            cd.cost = std::max(tMfma, tMem);
+            ranked.push_back(cd);
         }
     }
-    bool forced = false;
-    if (const char *ft = getenv("GETT_FORCE_TILE")) {   // tuning and test hook
-        const int v = atoi(ft);
-        if (v >= 0 && v < num_tiles(dtype)) {
-            tile = v;
-            forced = true;
+    std::stable_sort(ranked.begin(), ranked.end(),
+                     [](const Candidate &a, const Candidate &b) { return a.cost < b.cost; });
+    Candidate pick = ranked[0];
+    const char *how = "model";
+    auto find = [&](int t, int k) -> const Candidate * {
+        for (auto &c : ranked)
+            if (c.tile == t && c.kind == k) return &c;
+        return nullptr;
+    };
+    // tuning and test hooks; a choice being timed by gett_plan_tune overrides
+    // them, a remembered one does not
+    const char *ft = getenv("GETT_FORCE_TILE");
+    const char *fk = getenv("GETT_FORCE_KIND");
+    if (force && (force->timing || !(ft || fk))) {
+        if (const Candidate *c = find(force->tile, force->kind)) {
+            pick = *c;
+            how = force->source;
+        }
+    } else if (ft || fk) {
+        const int t = ft ? atoi(ft) : pick.tile;
+        const int k = fk ? atoi(fk) : 0;
+        const Candidate *c = find(t, k);
+        if (!c) c = find(t, 0);
+        if (c) {
+            pick = *c;
+            how = "forced";
         }
     }
+    const int tile = pick.tile;
+    const int kind = pick.kind;
+    const double bestMfma = pick.tMfma, bestMem = pick.tMem;
     const TileShape &ts = tile_shape(dtype, tile);
     const Box box = box_for(ts.kt);
-    const bool tileCanStream = ts.stream && box.nsteps <= 1;
-    int kind = (bestMem > bestMfma && tileCanStream && ts.sbw > ts.bw) ? 1 : 0;
-    if (const char *fk = getenv("GETT_FORCE_KIND")) {   // tuning and test hook
-        const int v = atoi(fk);
-        if (v == 0 || (v == 1 && tileCanStream)) kind = v;
-    }
     // A contraction bound by the C stream walks C in memory order: x indices
     // by C stride (the row operand's stride-one index stays first when it is
     // a free index, for its vector gathers) and tiles y-fastest.
@@ -498,6 +517,9 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
 
     plan.dtype = dtype;
     plan.flags = flags;
+    plan.rank[0] = (int)C.modes.size();
+    plan.rank[1] = (int)A.modes.size();
+    plan.rank[2] = (int)B.modes.size();
     plan.an = an;
     plan.desc = d;
     plan.descScalar = d;
@@ -505,6 +527,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     plan.tile = tile;
     plan.xmode = xmode;
     plan.kind = kind;
+    plan.ranked = ranked;
     plan.ymode = ymode;
     const double item = dtype == GETT_FLOAT32 ? 4.0 : 8.0;
     plan.flops = 2.0 * (double)an.sizeM * (double)an.sizeN * (double)an.sizeK;
@@ -536,7 +559,12 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     o << ",\"size_x\":" << sizeX << ",\"size_y\":" << sizeY << ",\"size_k\":" << an.sizeK;
     o << ",\"tile\":{\"id\":" << tile << ",\"mt\":" << ts.mt << ",\"nt\":" << ts.nt << ",\"kt\":" << ts.kt
       << ",\"waves\":[" << ts.wm << "," << ts.wn << "],\"reads\":[" << ts.rx << "," << ts.ry
-      << "],\"forced\":" << (forced ? "true" : "false") << ",\"model_us\":[" << costs.str() << "]}";
+      << "],\"chosen_by\":\"" << how << "\",\"model_us\":" << pick.cost * 1e6 << "}";
+    o << ",\"candidates\":[";
+    for (size_t i = 0; i < ranked.size(); ++i)
+        o << (i ? "," : "") << "{\"tile\":" << ranked[i].tile << ",\"kind\":\""
+          << (ranked[i].kind ? "stream" : "macro") << "\",\"model_us\":" << ranked[i].cost * 1e6 << "}";
+    o << "]";
     o << ",\"streaming\":" << (streaming ? "true" : "false");
     o << ",\"kernel\":\"" << (kind ? "stream" : "macro") << "\"";
     o << ",\"kbox\":{\"kj\":" << kj << ",\"tj\":" << tj << ",\"elements\":" << kbox << ",\"blocks\":" << nblk

@@ -1,10 +1,16 @@
 // api.cpp -- the C entry points declared in include/gett.h.
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
+
+#include <algorithm>
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
+#include <sstream>
+#include <string>
+#include <unordered_map>
 
 #include "plan.hpp"
 
@@ -28,6 +34,54 @@ bool inject_launch_fault()
     return v && strcmp(v, "launch") == 0;
 }
 
+// Null, misaligned or overlapping operand pointers (A and B only matter when
+// they are read).
+bool pointers_ok(const gett_plan_s &P, bool readAB, const void *A, const void *B, const void *C)
+{
+    const int64_t item = P.dtype == GETT_FLOAT32 ? 4 : 8;
+    if (!C || (uintptr_t)C % item) return false;
+    if (!readAB) return true;
+    if (!A || !B || (uintptr_t)A % item || (uintptr_t)B % item) return false;
+    const int64_t bytesC = (P.an.maxOffC + 1) * item;
+    return !overlaps(C, bytesC, A, (P.an.maxOffA + 1) * item) &&
+           !overlaps(C, bytesC, B, (P.an.maxOffB + 1) * item);
+}
+
+// The tuned choice of every descriptor tuned in this process (the paper's
+// database of known implementations, Sec. 6, kept in memory).
+std::mutex g_tunedMutex;
+std::unordered_map<std::string, std::pair<int, int>> g_tuned;
+
+std::string key_of(const gett_plan_s &p)
+{
+    std::ostringstream k;
+    k << (int)p.dtype << "|" << p.flags;
+    for (int i = 0; i < 3; ++i) {
+        k << "|" << p.modes[i] << "|";
+        for (auto v : p.ext[i]) k << v << ",";
+        k << "|";
+        if (p.hasStride[i])
+            for (auto v : p.str[i]) k << v << ",";
+        else
+            k << "F";
+    }
+    return k.str();
+}
+
+gett_status_t plan_with(gett_plan_s &p, gett_dtype_t dtype, const char *const m[3],
+                        const int64_t *const e[3], const int64_t *const st[3], uint32_t flags,
+                        const gett::Choice *force)
+{
+    try {
+        return gett::analyse(p, dtype, m[0], e[0], st[0], m[1], e[1], st[1], m[2], e[2], st[2],
+                             flags, force);
+    } catch (const std::bad_alloc &) {
+        return GETT_ERROR_ALLOC;
+    } catch (...) {
+        return GETT_ERROR_INVALID_VALUE;
+    }
+}
+
 }  // namespace
 
 extern "C" {
@@ -41,18 +95,42 @@ gett_status_t gett_plan(gett_plan_t *plan, gett_dtype_t dtype, const char *modes
     *plan = nullptr;
     gett_plan_s *p = new (std::nothrow) gett_plan_s();
     if (!p) return GETT_ERROR_ALLOC;
-    gett_status_t st;
-    try {
-        st = gett::analyse(*p, dtype, modes_C, extent_C, stride_C, modes_A, extent_A, stride_A,
-                           modes_B, extent_B, stride_B, flags);
-    } catch (const std::bad_alloc &) {
-        st = GETT_ERROR_ALLOC;
-    } catch (...) {
-        st = GETT_ERROR_INVALID_VALUE;
+    const char *m[3] = {modes_C, modes_A, modes_B};
+    const int64_t *e[3] = {extent_C, extent_A, extent_B};
+    const int64_t *st[3] = {stride_C, stride_A, stride_B};
+    gett_status_t status = plan_with(*p, dtype, m, e, st, flags, nullptr);
+    if (status == GETT_SUCCESS) {
+        try {
+            // keep the arguments (the analysis validated them) for re-planning
+            for (int i = 0; i < 3; ++i) {
+                p->modes[i] = m[i] ? m[i] : "";
+                p->hasStride[i] = st[i] != nullptr;
+            }
+            for (int i = 0; i < 3; ++i) {
+                const size_t n = (size_t)p->rank[i];
+                p->ext[i].assign(e[i], e[i] + n);
+                if (st[i]) p->str[i].assign(st[i], st[i] + n);
+            }
+            int tile = -1, kind = 0;
+            {
+                std::lock_guard<std::mutex> lock(g_tunedMutex);
+                auto it = g_tuned.find(key_of(*p));
+                if (it != g_tuned.end()) {
+                    tile = it->second.first;
+                    kind = it->second.second;
+                }
+            }
+            if (tile >= 0) {   // this descriptor was tuned before in this process
+                const gett::Choice c = {tile, kind, "remembered", false};
+                status = plan_with(*p, dtype, m, e, st, flags, &c);
+            }
+        } catch (...) {
+            status = GETT_ERROR_ALLOC;
+        }
     }
-    if (st != GETT_SUCCESS) {
+    if (status != GETT_SUCCESS) {
         delete p;
-        return st;
+        return status;
     }
     *plan = p;
     return GETT_SUCCESS;
@@ -64,16 +142,8 @@ gett_status_t gett_contract(const gett_plan_t plan, double alpha, const void *A,
     if (!plan) return GETT_ERROR_INVALID_VALUE;
     const gett_plan_s &P = *plan;
     if (P.an.emptyC) return GETT_SUCCESS;   // C has no elements
-    const int64_t item = P.dtype == GETT_FLOAT32 ? 4 : 8;
     const bool readAB = alpha != 0.0 && !P.an.emptySum;
-    if (!C) return GETT_ERROR_INVALID_VALUE;
-    if (readAB && (!A || !B)) return GETT_ERROR_INVALID_VALUE;
-    if ((uintptr_t)C % item) return GETT_ERROR_INVALID_VALUE;
-    if (readAB && (((uintptr_t)A % item) || ((uintptr_t)B % item))) return GETT_ERROR_INVALID_VALUE;
-    const int64_t bytesC = (P.an.maxOffC + 1) * item;
-    if (readAB && (overlaps(C, bytesC, A, (P.an.maxOffA + 1) * item) ||
-                   overlaps(C, bytesC, B, (P.an.maxOffB + 1) * item)))
-        return GETT_ERROR_INVALID_VALUE;
+    if (!pointers_ok(P, readAB, A, B, C)) return GETT_ERROR_INVALID_VALUE;
 
     const void *X = P.an.swapped ? B : A;
     const void *Y = P.an.swapped ? A : B;
@@ -97,6 +167,88 @@ gett_status_t gett_contract(const gett_plan_t plan, double alpha, const void *A,
     if (inject_launch_fault()) return GETT_ERROR_HIP;
     const hipError_t e = fn(d, X, Y, C, alpha, beta, (hipStream_t)stream);
     return e == hipSuccess ? GETT_SUCCESS : GETT_ERROR_HIP;
+}
+
+gett_status_t gett_plan_tune(gett_plan_t plan, int max_candidates, const void *A, const void *B,
+                             void *C, void *stream)
+{
+    if (!plan || max_candidates < 1) return GETT_ERROR_INVALID_VALUE;
+    gett_plan_s &P = *plan;
+    if (P.an.emptyC) return GETT_SUCCESS;
+    if (!pointers_ok(P, !P.an.emptySum, A, B, C)) return GETT_ERROR_INVALID_VALUE;
+    // with an empty sum every candidate only scales C: nothing to choose
+    if (P.an.emptySum || P.ranked.size() < 2) return GETT_SUCCESS;
+    const char *m[3] = {P.modes[0].c_str(), P.modes[1].c_str(), P.modes[2].c_str()};
+    const int64_t *e[3], *st[3];
+    for (int i = 0; i < 3; ++i) {
+        e[i] = P.ext[i].empty() ? nullptr : P.ext[i].data();
+        st[i] = P.hasStride[i] ? P.str[i].data() : nullptr;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (hipEventCreate(&e0) != hipSuccess) return GETT_ERROR_HIP;
+    if (hipEventCreate(&e1) != hipSuccess) {
+        (void)hipEventDestroy(e0);
+        return GETT_ERROR_HIP;
+    }
+    gett_status_t status = GETT_SUCCESS;
+    const std::vector<gett::Candidate> ranked = P.ranked;
+    const size_t n = std::min(ranked.size(), (size_t)max_candidates);
+    std::ostringstream log;
+    int best = -1;
+    float bestMs = 0;
+    for (size_t i = 0; i < n && status == GETT_SUCCESS; ++i) {
+        gett_plan_s trial;
+        const gett::Choice c = {ranked[i].tile, ranked[i].kind, "tuned", true};
+        status = plan_with(trial, P.dtype, m, e, st, P.flags, &c);
+        if (status != GETT_SUCCESS) break;
+        // one untimed launch, then three timed (alpha 1, beta 0: C is overwritten)
+        status = gett_contract(&trial, 1.0, A, B, 0.0, C, stream);
+        if (status != GETT_SUCCESS) break;
+        if (hipEventRecord(e0, s) != hipSuccess) { status = GETT_ERROR_HIP; break; }
+        for (int r = 0; r < 3 && status == GETT_SUCCESS; ++r)
+            status = gett_contract(&trial, 1.0, A, B, 0.0, C, stream);
+        if (status != GETT_SUCCESS) break;
+        float ms = 0;
+        if (hipEventRecord(e1, s) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+            hipEventElapsedTime(&ms, e0, e1) != hipSuccess) {
+            status = GETT_ERROR_HIP;
+            break;
+        }
+        ms /= 3.0f;
+        log << (i ? "," : "") << "{\"tile\":" << ranked[i].tile << ",\"kind\":\""
+            << (ranked[i].kind ? "stream" : "macro") << "\",\"model_us\":" << ranked[i].cost * 1e6
+            << ",\"measured_us\":" << ms * 1e3 << "}";
+        if (best < 0 || ms < bestMs) {
+            best = (int)i;
+            bestMs = ms;
+        }
+    }
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    if (status != GETT_SUCCESS || best < 0) return status;
+    const gett::Choice c = {ranked[best].tile, ranked[best].kind, "tuned", true};
+    gett_plan_s tuned;
+    status = plan_with(tuned, P.dtype, m, e, st, P.flags, &c);
+    if (status != GETT_SUCCESS) return status;
+    try {
+        for (int i = 0; i < 3; ++i) {
+            tuned.modes[i] = P.modes[i];
+            tuned.ext[i] = P.ext[i];
+            tuned.str[i] = P.str[i];
+            tuned.hasStride[i] = P.hasStride[i];
+        }
+        tuned.text.pop_back();   // the closing brace of the description
+        tuned.text += ",\"tuning\":[" + log.str() + "]}";
+        {
+            std::lock_guard<std::mutex> lock(g_tunedMutex);
+            g_tuned[key_of(tuned)] = {c.tile, c.kind};
+        }
+        P = tuned;
+    } catch (...) {
+        return GETT_ERROR_ALLOC;
+    }
+    return GETT_SUCCESS;
 }
 
 gett_status_t gett_destroy(gett_plan_t plan)

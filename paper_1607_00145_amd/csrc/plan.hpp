@@ -28,6 +28,19 @@ struct Analysis {
     int64_t maxOffA = 0, maxOffB = 0, maxOffC = 0;   // largest element offsets
 };
 
+// A kernel candidate: tile shape and kind, with the model's estimate.
+struct Candidate {
+    int tile = 0, kind = 0;
+    double tMfma = 0, tMem = 0, cost = 0;   // seconds
+};
+
+// A candidate imposed on the analyser, and where the choice came from.
+struct Choice {
+    int tile, kind;
+    const char *source;   // "tuned" or "remembered"
+    bool timing;          // a candidate being timed: overrides the test hooks
+};
+
 typedef hipError_t (*LaunchFn)(const KDesc &, const void *, const void *, void *, double, double,
                                hipStream_t);
 
@@ -42,6 +55,12 @@ struct gett_plan_s {
     int tile;                // index into the tile table of the dtype
     int xmode, ymode;        // gather modes of the preferred kernel
     int kind;                // 0: macro-kernel, 1: persistent streaming kernel
+    std::vector<gett::Candidate> ranked;   // every candidate, best model estimate first
+    // the arguments of gett_plan, kept to re-plan with another candidate
+    std::string modes[3];
+    std::vector<int64_t> ext[3], str[3];
+    bool hasStride[3];
+    int rank[3];             // modes of C, A, B as parsed
     double flops;            // 2 * S_Im * S_In * S_Ik (Eq. 14)
     double bytesAlgo;        // |A| + |B| + |C| (+|C| when beta may be read)
     std::string text;        // JSON description
@@ -52,7 +71,8 @@ namespace gett {
 // Analyse and fill a plan; returns a status (the plan is unusable on error).
 gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, const int64_t *eC,
                       const int64_t *sC, const char *mA, const int64_t *eA, const int64_t *sA,
-                      const char *mB, const int64_t *eB, const int64_t *sB, uint32_t flags);
+                      const char *mB, const int64_t *eB, const int64_t *sB, uint32_t flags,
+                      const Choice *force);
 
 // Launch table lookup (defined with the kernel instantiations).  kind 0: the
 // macro-kernel, 1: the persistent streaming kernel.

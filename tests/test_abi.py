@@ -26,8 +26,8 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = g.load_library()
     names = declared_functions()
-    assert names == sorted(["gett_plan", "gett_contract", "gett_destroy", "gett_status_string",
-                            "gett_plan_describe"])
+    assert names == sorted(["gett_plan", "gett_contract", "gett_plan_tune", "gett_destroy",
+                            "gett_status_string", "gett_plan_describe"])
     for n in names:
         assert hasattr(lib, n), n
     out = subprocess.run(["nm", "-D", "--defined-only", g.LIB_PATH], capture_output=True,
@@ -228,3 +228,59 @@ def test_launch_failure_is_reported():
 def test_expression_parser():
     assert g.parse_expression("C[a,b,i,j] = A[i,m,a] * B[m,j,b]") == ("a,b,i,j", "i,m,a", "m,j,b")
     assert g.parse_expression("C[m1] = A[m1,k] * B[k]") == ("m1,", "m1,k", "k,")
+
+
+def test_candidates_are_ranked_by_the_model():
+    """Sec. 3.4: every compiled candidate gets a model estimate; the plan uses
+    the cheapest one unless told otherwise."""
+    for w in wl.WORKLOADS:
+        dt = g.GETT_FLOAT32 if w.dtype == "f32" else g.GETT_FLOAT64
+        st, h = plan(w.modes_C, w.modes_A, w.modes_B, w.extents, dtype=dt)
+        assert st == 0
+        d = json.loads(g.gett_plan_describe(h))
+        g.gett_destroy(h)
+        cands = d["candidates"]
+        assert len(cands) >= 2
+        costs = [c["model_us"] for c in cands]
+        assert costs == sorted(costs)
+        assert all(c > 0 for c in costs)
+        assert len({(c["tile"], c["kind"]) for c in cands}) == len(cands)
+        assert d["tile"]["chosen_by"] == "model"
+        assert (cands[0]["tile"], cands[0]["kind"]) == (d["tile"]["id"], d["kernel"])
+        assert d["tile"]["model_us"] == costs[0]
+
+
+def test_forced_candidate_is_reported():
+    code = ("import json, paper_1607_00145_amd as g\n"
+            "st, h = g.gett_plan(0, 'mn', [300, 200], None, 'mk', [300, 64], None, 'kn', [64, 200], None, 0)\n"
+            "d = json.loads(g.gett_plan_describe(h))\n"
+            "print(d['tile']['id'], d['tile']['chosen_by'])\n")
+    env = dict(os.environ, GETT_FORCE_TILE="0", GETT_FORCE_KIND="0", PYTHONPATH=ROOT)
+    out = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True,
+                         cwd=ROOT)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.split() == ["0", "forced"]
+
+
+def test_tune_host_side_errors():
+    """gett_plan_tune rejects bad arguments before any HIP call."""
+    st, h = plan("mn", "mk", "kn", {"m": 100, "n": 200, "k": 300})
+    assert st == 0
+    try:
+        assert g.gett_plan_tune(None, 4, 256, 1 << 20, 2 << 20) == g.GETT_ERROR_INVALID_VALUE
+        assert g.gett_plan_tune(h, 0, 256, 1 << 20, 2 << 20) == g.GETT_ERROR_INVALID_VALUE
+        assert g.gett_plan_tune(h, -3, 256, 1 << 20, 2 << 20) == g.GETT_ERROR_INVALID_VALUE
+        assert g.gett_plan_tune(h, 4, 0, 1 << 20, 2 << 20) == g.GETT_ERROR_INVALID_VALUE
+        assert g.gett_plan_tune(h, 4, 256, 1 << 20, 0) == g.GETT_ERROR_INVALID_VALUE
+        assert g.gett_plan_tune(h, 4, 258, 1 << 20, 2 << 20) == g.GETT_ERROR_INVALID_VALUE
+        # C overlapping A
+        assert g.gett_plan_tune(h, 4, 1 << 20, 4 << 20, (1 << 20) + 64) == \
+            g.GETT_ERROR_INVALID_VALUE
+        assert json.loads(g.gett_plan_describe(h))["tile"]["chosen_by"] == "model"
+    finally:
+        g.gett_destroy(h)
+    # an empty C: nothing to tune, nothing to check
+    st, h = plan("mn", "mk", "kn", {"m": 0, "n": 200, "k": 300})
+    assert st == 0
+    assert g.gett_plan_tune(h, 4, 0, 0, 0) == g.GETT_SUCCESS
+    g.gett_destroy(h)
