@@ -3,6 +3,7 @@
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-report]
                     [--no-cpu-baseline]
+    python bench.py --sweep fig11 [--max-candidates N] [--report-runs R]
 
 A step is one contraction C <- alpha*A*B + beta*C of the headline workload
 (bw4x3_fp32: C[a,b,c,d] = A[a,e,b] * B[e,d,c], a..d = 112, e = 16,
@@ -88,6 +89,17 @@ class Problem:
         if st != 0:
             raise RuntimeError(f"gett_contract: {self.g.gett_status_string(st)}")
 
+    def tune(self, max_candidates: int):
+        """gett_plan_tune on this problem's buffers (C is overwritten; it is
+        restored from the initial C when beta != 0)."""
+        st = self.g.gett_plan_tune(self.h, max_candidates, self.A.data_ptr(), self.B.data_ptr(),
+                                   self.C.data_ptr(), 0)
+        if st != 0:
+            raise RuntimeError(f"gett_plan_tune: {self.g.gett_status_string(st)}")
+        if self.C0 is not None:
+            self.C.copy_(self.C0)
+        self.plan = json.loads(self.g.gett_plan_describe(self.h))
+
     def close(self):
         self.g.gett_destroy(self.h)
 
@@ -172,9 +184,19 @@ def report_workload(w, dev, stream, runs, flush):
     rec["plan"]["tile"] = [p.plan["tile"]["mt"], p.plan["tile"]["nt"], p.plan["tile"]["kt"]]
     rec["plan"]["workgroups"] = p.plan["grid"]["workgroups"]
     p.close()
-    # equal-size GEMM (Sec. 7): S_Im x S_Ik times S_Ik x S_In with the same alpha, beta
     M, N, K = p.plan["size_x"], p.plan["size_y"], p.plan["size_k"]
     del p
+    gmin = time_gemm(M, N, K, w, dev, stream, runs, flush)
+    rec["gemm_ms_min"] = round(gmin, 5)
+    rec["gemm_gflops"] = round(flops / (gmin * 1e-3) / 1e9, 1)
+    rec["vs_equal_size_gemm"] = round(gmin / tmin, 4)
+    return rec
+
+
+def time_gemm(M, N, K, w, dev, stream, runs, flush):
+    """Cold minimum (ms) of the equal-size GEMM of Sec. 7 (S_Im x S_Ik times
+    S_Ik x S_In with the workload's alpha and beta) through torch."""
+    import torch
     torch.cuda.empty_cache()
     dt = torch.float32 if w.dtype == "f32" else torch.float64
     torch.backends.cuda.matmul.allow_tf32 = False
@@ -187,14 +209,53 @@ def report_workload(w, dev, stream, runs, flush):
         fn = lambda: torch.mm(a, b, out=c)
     for _ in range(3):
         fn()
-    gts = time_launches(fn, runs, stream, flush)
-    gmin = min(gts)
-    rec["gemm_ms_min"] = round(gmin, 5)
-    rec["gemm_gflops"] = round(flops / (gmin * 1e-3) / 1e9, 1)
-    rec["vs_equal_size_gemm"] = round(gmin / tmin, 4)
+    gmin = min(time_launches(fn, runs, stream, flush))
     del a, b, c
     torch.cuda.empty_cache()
-    return rec
+    return gmin
+
+
+def sweep_fig11(dev, stream, runs, flush, max_candidates):
+    """Sec. 7.3, Fig. 11 (and the candidate-search study of Fig. 13): both
+    contractions, both precisions, S_Ik from 8 to 1024.  One JSON line per
+    point: GETT with the model's choice, GETT after gett_plan_tune over the
+    best `max_candidates` candidates, and the equal-size GEMM, all cold."""
+    for dtype in ("f32", "f64"):
+        peak = (PEAK["f32_TFLOPs"] if dtype == "f32" else PEAK["f64_TFLOPs"]) * 1e12
+        for variant in ("a", "b"):
+            for k in wl.FIG11_K:
+                w = wl.fig11(variant, k, dtype)
+                flops = wl.flop_count(w)
+                p = Problem(w, dev)
+                tile = lambda: [p.plan["tile"][x] for x in ("mt", "nt", "kt")] + [p.plan["kernel"]]
+                model_tile = tile()
+                for _ in range(3):
+                    p.launch(stream)
+                tm = min(time_launches(lambda: p.launch(stream), runs, stream, flush))
+                p.tune(max_candidates)
+                for _ in range(3):
+                    p.launch(stream)
+                tt = min(time_launches(lambda: p.launch(stream), runs, stream, flush))
+                tuned_tile = tile()
+                M, N, K = p.plan["size_x"], p.plan["size_y"], p.plan["size_k"]
+                p.close()
+                del p
+                tg = time_gemm(M, N, K, w, dev, stream, runs, flush)
+                best = min(tm, tt)
+                rec = {"sweep": "fig11", "contraction": w.name, "expression": w.expression(),
+                       "dtype": dtype, "S_Ik": k, "bound": bound_of(w),
+                       "model_ms": round(tm, 5), "model_tile": model_tile,
+                       "model_gflops": round(flops / (tm * 1e-3) / 1e9, 1),
+                       "tuned_ms": round(tt, 5), "tuned_tile": tuned_tile,
+                       "tuned_gflops": round(flops / (tt * 1e-3) / 1e9, 1),
+                       "model_of_best": round(best / tm, 4),
+                       "frac_mfma_peak": round(flops / (best * 1e-3) / peak, 4),
+                       "gemm_ms": round(tg, 5),
+                       "gemm_gflops": round(flops / (tg * 1e-3) / 1e9, 1),
+                       "vs_equal_size_gemm": round(tg / best, 4)}
+                log(f"[sweep] {w.name}: model {tm*1e3:.1f} us, tuned {tt*1e3:.1f} us, "
+                    f"gemm {tg*1e3:.1f} us")
+                print(json.dumps(rec), flush=True)
 
 
 def main():
@@ -206,6 +267,10 @@ def main():
     ap.add_argument("--report-runs", type=int, default=20)
     ap.add_argument("--no-report", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", choices=["fig11"], default=None,
+                    help="run the S_Ik sweep of Fig. 11 instead (one JSON line per point)")
+    ap.add_argument("--max-candidates", type=int, default=16,
+                    help="candidates gett_plan_tune times in the sweep")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB a few times (the reference "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -231,6 +296,10 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": n * 4, "launches": 5}), flush=True)
+        return
+    if args.sweep:
+        flush_buf = torch.empty(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
+        sweep_fig11(dev, stream, args.report_runs, lambda: flush_buf.zero_(), args.max_candidates)
         return
     w = wl.BY_NAME[args.workload]
 

@@ -284,3 +284,20 @@ def test_tune_host_side_errors():
     assert st == 0
     assert g.gett_plan_tune(h, 4, 0, 0, 0) == g.GETT_SUCCESS
     g.gett_destroy(h)
+
+
+@pytest.mark.parametrize("variant", ["a", "b"])
+def test_fig11_sweep_plans(variant):
+    """Sec. 7.3, Fig. 11: S_Im = S_In = 1152 at every S_Ik of the sweep; C's
+    stride-one index i1 belongs to A, so the operands are exchanged."""
+    for k in wl.FIG11_K:
+        w = wl.fig11(variant, k)
+        assert wl.flop_count(w) == 2 * 1152 * 1152 * k
+        d = describe(w.modes_C, w.modes_A, w.modes_B, w.extents)
+        names = lambda key: sorted(x["name"] for x in d[key])
+        assert names("I_m") == ["i1", "i2"]
+        assert names("I_n") == (["j"] if variant == "a" else ["j1", "j2"])
+        assert names("I_k") == ["k"]
+        assert d["merges"] == []
+        assert d["swapped"] is True
+        assert d["size_x"] * d["size_y"] == 1152 * 1152 and d["size_k"] == k

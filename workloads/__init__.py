@@ -84,6 +84,29 @@ WORKLOADS: List[Workload] = [
 ]
 BY_NAME = {w.name: w for w in WORKLOADS}
 
+# Sec. 7.3, Fig. 11: two contractions with S_Im = S_In = 1152 and S_Ik swept
+# from 8 to 1024.  The split of 1152 into two indices is not given; 32 x 36 is
+# used for both i1 x i2 and j1 x j2.
+FIG11_K = (8, 16, 32, 64, 128, 256, 512, 1024)
+FIG11_VARIANTS = {
+    # i1 j i2 - i1 k i2 - j k
+    "a": ("i1,j,i2", "i1,k,i2", "j,k", {"i1": 32, "i2": 36, "j": 1152}),
+    # i1 j1 i2 j2 - i1 k i2 - j1 k j2
+    "b": ("i1,j1,i2,j2", "i1,k,i2", "j1,k,j2", {"i1": 32, "i2": 36, "j1": 32, "j2": 36}),
+}
+
+
+def fig11(variant: str, s_ik: int, dtype: str = "f32") -> Workload:
+    """One point of the Fig. 11 sweep (alpha 1, beta 0, U[-1,1] inputs)."""
+    mc, ma, mb, ext = FIG11_VARIANTS[variant]
+    ext = dict(ext, k=int(s_ik))
+    number = 100 + 20 * (ord(variant) - ord("a")) + FIG11_K.index(s_ik) if s_ik in FIG11_K \
+        else 1000 + int(s_ik)
+    if dtype == "f64":
+        number += 10
+    return Workload(number, f"fig11{variant}_k{s_ik}_{'fp32' if dtype == 'f32' else 'fp64'}",
+                    dtype, mc, ma, mb, ext)
+
 
 def _draw(rng: np.random.Generator, n: int, dist: str) -> np.ndarray:
     if dist == "uniform":
