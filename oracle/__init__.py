@@ -5,8 +5,9 @@ baseline leg of the benchmark import this package.  It shares no code with the
 GPU library (``paper_1607_00145_amd``) and imports nothing from it.
 
 The arithmetic lives in ``gett_oracle.c`` (plain C, fp64, the definition of
-Eq. 3 evaluated as the naive loop nest of Listing 3); this module only builds
-that file with gcc and marshals numpy arrays into it.
+Eq. 3 evaluated as the naive loop nest of Listing 3, and the transposition of
+Eq. 4); this module only builds that file with gcc and marshals numpy arrays
+into it.
 """
 from __future__ import annotations
 
@@ -57,6 +58,11 @@ def _load():
             ctypes.c_void_p, ctypes.c_int64, i64p,
             ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), ctypes.c_int]
         lib.oracle_max_threads.restype = ctypes.c_int
+        lib.oracle_transpose.restype = ctypes.c_int
+        lib.oracle_transpose.argtypes = [
+            ctypes.c_int, ctypes.c_int, i64p, i64p, i64p, ctypes.c_double, ctypes.c_void_p,
+            ctypes.c_double, ctypes.c_void_p, i64p,
+            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
         _lib = lib
     return _lib
 
@@ -139,6 +145,39 @@ def contract(modes_C: str, modes_A: str, modes_B: str, A: np.ndarray, B: np.ndar
         out = out.reshape(ec, order="F") if ec else out.reshape(())
         den = den.reshape(ec, order="F") if ec else den.reshape(())
     return Result(out, den)
+
+
+def transpose(A: np.ndarray, perm, alpha: float = 1.0, beta: float = 0.0,
+              B: np.ndarray | None = None) -> Result:
+    """Eq. 4: B[Pi(i)] <- alpha * A[i] + beta * B[Pi(i)], where output mode j is
+    input mode perm[j].  ``A`` and ``B`` may have any positive strides; ``B``
+    (shape A.shape[perm]) is read only when beta != 0.  Returns fp64 arrays
+    of the output's shape."""
+    if A.dtype not in (np.float32, np.float64):
+        raise TypeError("float32 or float64 only")
+    dt = A.dtype
+    perm = [int(p) for p in perm]
+    if len(perm) != A.ndim:
+        raise ValueError("perm must name every mode of A once")
+    pa, ea, sa = _view(A, dt)
+    out_shape = [ea[p] for p in perm]
+    pb, sb = None, None
+    if beta != 0:
+        if B is None or list(B.shape) != out_shape:
+            raise ValueError("B of shape A.shape[perm] is needed when beta != 0")
+        pb, _, sb = _view(B, dt)
+    n = int(np.prod(out_shape)) if out_shape else 1
+    out = np.zeros(max(n, 1), dtype=np.float64)
+    den = np.zeros(max(n, 1), dtype=np.float64)
+    rc = _load().oracle_transpose(
+        0 if dt == np.float32 else 1, len(ea), _i64(ea), _i64(sa), _i64(perm), float(alpha), pa,
+        float(beta), pb, _i64(sb) if sb is not None else None,
+        out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+        den.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    if rc != 0:
+        raise OracleError(rc)
+    shape = out_shape if out_shape else ()
+    return Result(out[:n].reshape(shape, order="F"), den[:n].reshape(shape, order="F"))
 
 
 def rel_error(got, ref: Result) -> float:

@@ -293,3 +293,82 @@ int oracle_max_threads(void)
     return 1;
 #endif
 }
+
+/*
+ * oracle_transpose: the general tensor transposition with input and output
+ * scaling of Sec. 2.3, Eq. 4:
+ *
+ *     out[Pi(i_1, ..., i_d)] = alpha * in[i_1, ..., i_d] + beta * out_in[Pi(i_1, ..., i_d)]
+ *
+ *   dtype    0 = float32, 1 = float64 (type of in and out_in)
+ *   rank     d (0 <= d <= 32); ext[d] extents of `in`; str_in[d] its strides
+ *   perm     output mode j is input mode perm[j] (a permutation of 0..d-1)
+ *   in       not read when alpha == 0
+ *   out_in   the old output (not read when beta == 0), addressed by
+ *            str_out_in[j] for output mode j
+ *   out64, den64  dense column-major over the output's extents
+ *            (ext[perm[0]] fastest): the unrounded fp64 result and
+ *            |alpha * in| + |beta * out_in| as the scale of its rounding error.
+ * Every input element is visited once, by an odometer over the input modes
+ * (mode 0 fastest); its output position is recomputed from the multi-index.
+ */
+int oracle_transpose(int dtype, int rank, const int64_t *ext, const int64_t *str_in,
+                     const int64_t *perm, double alpha, const void *in, double beta,
+                     const void *out_in, const int64_t *str_out_in, double *out64, double *den64)
+{
+    if (dtype != 0 && dtype != 1) return OR_ERR_VALUE;
+    if (rank < 0 || rank > OR_MAX_MODES) return OR_ERR_VALUE;
+    int seen[OR_MAX_MODES];
+    for (int j = 0; j < rank; ++j) seen[j] = 0;
+    for (int j = 0; j < rank; ++j) {
+        if (perm[j] < 0 || perm[j] >= rank || seen[perm[j]]) return OR_ERR_VALUE;
+        seen[perm[j]] = 1;
+    }
+    int64_t size = 1;
+    for (int i = 0; i < rank; ++i) {
+        if (ext[i] < 0) return OR_ERR_VALUE;
+        size *= ext[i];
+    }
+    if (size == 0) return OR_OK;
+    if ((alpha != 0.0 && !in) || (beta != 0.0 && !out_in) || !out64 || !den64)
+        return OR_ERR_VALUE;
+    /* dense column-major stride of each output mode, then of each input mode */
+    int64_t dense_out[OR_MAX_MODES], pos_stride[OR_MAX_MODES], old_stride[OR_MAX_MODES];
+    int64_t acc = 1;
+    for (int j = 0; j < rank; ++j) {
+        dense_out[j] = acc;
+        acc *= ext[perm[j]];
+    }
+    for (int j = 0; j < rank; ++j) {
+        pos_stride[perm[j]] = dense_out[j];
+        old_stride[perm[j]] = str_out_in ? str_out_in[j] : 0;
+    }
+    int64_t idx[OR_MAX_MODES];
+    for (int i = 0; i < rank; ++i) idx[i] = 0;
+    for (int64_t n = 0; n < size; ++n) {
+        int64_t offIn = 0, pos = 0, offOld = 0;
+        for (int i = 0; i < rank; ++i) {
+            offIn += idx[i] * str_in[i];
+            pos += idx[i] * pos_stride[i];
+            offOld += idx[i] * old_stride[i];
+        }
+        double r = 0.0, d = 0.0;
+        if (alpha != 0.0) {
+            double a = or_load(dtype, in, offIn);
+            r = alpha * a;
+            d = fabs(alpha * a);
+        }
+        if (beta != 0.0) {
+            double b = or_load(dtype, out_in, offOld);
+            r += beta * b;
+            d += fabs(beta * b);
+        }
+        out64[pos] = r;
+        den64[pos] = d;
+        for (int i = 0; i < rank; ++i) {
+            if (++idx[i] < ext[i]) break;
+            idx[i] = 0;
+        }
+    }
+    return OR_OK;
+}

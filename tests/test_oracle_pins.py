@@ -392,3 +392,93 @@ def test_error_metric_catches_a_dropped_term():
     bad = A[:, :15] @ B[:15, :]
     assert oracle.rel_error(bad, ref) > 1e-3
     assert oracle.rel_error(A @ B, ref) < 1e-14
+
+
+# ------------------------------------------- Eq. 4: tensor transposition ---
+
+def test_transpose_worked_example():
+    """A 2x3 matrix 1..6 in Fortran order, transposed (Sec. 2.3 with d = 2):
+    rows become columns."""
+    A = np.arange(1, 7, dtype=np.float64).reshape(2, 3, order="F")   # [[1,3,5],[2,4,6]]
+    r = oracle.transpose(A, [1, 0])
+    assert r.out64.shape == (3, 2)
+    assert r.out64.tolist() == [[1.0, 2.0], [3.0, 4.0], [5.0, 6.0]]
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float64])
+def test_transpose_matches_numpy_axis_permutation(dtype):
+    """Output mode j is input mode perm[j]: numpy's transpose with the same
+    axes gives the same array (alpha 1, beta 0, exact)."""
+    rng = np.random.default_rng(7)
+    for perm in ([0, 1, 2], [2, 0, 1], [1, 2, 0], [2, 1, 0], [3, 1, 0, 2]):
+        shape = [2, 3, 4, 5][:len(perm)]
+        A = rng.standard_normal(shape).astype(dtype)
+        got = oracle.transpose(A, perm).out64
+        assert np.array_equal(got, np.transpose(A, perm).astype(np.float64))
+
+
+def test_transpose_cycle_is_not_its_inverse():
+    """A 3-cycle distinguishes perm from its inverse (a swapped convention
+    would fail here)."""
+    A = np.arange(24, dtype=np.float64).reshape(2, 3, 4)
+    got = oracle.transpose(A, [1, 2, 0]).out64
+    assert got.shape == (3, 4, 2)
+    for i, j, k in itertools.product(range(2), range(3), range(4)):
+        assert got[j, k, i] == A[i, j, k]
+    inverse = oracle.transpose(A, [2, 0, 1]).out64
+    assert inverse.shape == (4, 2, 3)
+
+
+def test_transpose_round_trip_restores_input():
+    rng = np.random.default_rng(8)
+    A = rng.standard_normal((3, 4, 2, 5))
+    perm = [2, 0, 3, 1]
+    inv = list(np.argsort(perm))
+    once = oracle.transpose(A, perm).out64
+    back = oracle.transpose(np.asfortranarray(once), inv).out64
+    assert np.array_equal(back, A)
+
+
+def test_transpose_scaling_closed_form():
+    """Identity permutation: Eq. 4 reduces to alpha * a + beta * b elementwise
+    (BLAS axpby); den = |alpha a| + |beta b|."""
+    rng = np.random.default_rng(9)
+    A = rng.standard_normal((4, 5))
+    B = rng.standard_normal((4, 5))
+    r = oracle.transpose(A, [0, 1], alpha=0.5, beta=-2.0, B=B)
+    assert np.array_equal(r.out64, 0.5 * A + -2.0 * B)
+    assert np.array_equal(r.den64, np.abs(0.5 * A) + np.abs(-2.0 * B))
+
+
+def test_transpose_strided_views_and_beta():
+    """Strided input and a strided old output, beta != 0, against numpy."""
+    rng = np.random.default_rng(10)
+    base = rng.standard_normal((7, 9, 6))
+    A = base[::2, 1::2, :5]                      # (4, 4, 5), gaps in every mode
+    perm = [2, 0, 1]
+    obase = rng.standard_normal((11, 10, 9))
+    B = obase[1:6, :8:2, 2:6]                    # (5, 4, 4) = A.shape[perm], gapped
+    assert list(B.shape) == [A.shape[p] for p in perm]
+    r = oracle.transpose(A, perm, alpha=1.5, beta=0.25, B=B)
+    ref = 1.5 * np.transpose(A, perm) + 0.25 * B
+    assert np.allclose(r.out64, ref, rtol=0, atol=1e-15)
+
+
+def test_transpose_beta_zero_ignores_old_output():
+    A = np.ones((2, 2))
+    r = oracle.transpose(A, [1, 0], alpha=3.0, beta=0.0, B=None)
+    assert np.array_equal(r.out64, 3.0 * np.ones((2, 2)))
+
+
+def test_transpose_rejects_bad_permutation():
+    A = np.ones((2, 3))
+    for perm in ([0, 0], [0, 2], [1]):
+        with pytest.raises((oracle.OracleError, IndexError, ValueError)):
+            oracle.transpose(A, perm)
+
+
+def test_transpose_empty_and_scalar():
+    A = np.ones((0, 3))
+    assert oracle.transpose(A, [1, 0]).out64.shape == (3, 0)
+    s = np.array(2.5)
+    assert float(oracle.transpose(s, [], alpha=2.0).out64) == 5.0
