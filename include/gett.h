@@ -52,7 +52,7 @@ typedef enum {
     /* rank above GETT_MAX_RANK; C strides that may map two elements of C to
      * one address; a tensor whose largest element offset reaches 2^31 */
     GETT_ERROR_NOT_SUPPORTED = 3,
-    /* a HIP runtime call (kernel launch) failed */
+    /* a HIP runtime call (kernel launch) or a rocBLAS call failed */
     GETT_ERROR_HIP = 4,
     /* host memory allocation failed */
     GETT_ERROR_ALLOC = 5
@@ -163,6 +163,97 @@ const char *gett_status_string(gett_status_t status);
  * Returns "" for NULL.
  */
 const char *gett_plan_describe(const gett_plan_t plan);
+
+/* ------------------------------------------------------------------------
+ * Tensor transposition (Sec. 2.3, Eq. 4)
+ * ------------------------------------------------------------------------ */
+
+/*
+ * gett_transpose -- out[Pi(i)] <- alpha * in[i] + beta * out[Pi(i)].
+ *
+ *   dtype       element type of in and out.
+ *   rank        number of indices (0 <= rank <= GETT_MAX_RANK; 0: one element).
+ *   extent      extent of each index (>= 0).
+ *   stride_in   stride of each index in `in` (elements, >= 1), or NULL for
+ *               the Fortran layout in the given index order.
+ *   stride_out  stride of each index in `out`; the permutation Pi is carried
+ *               by these strides (index d of the input lands at stride
+ *               stride_out[d] of the output).  NULL: the same Fortran layout
+ *               (no permutation: Eq. 4 is then an axpby).
+ *   in, out     device pointers aligned to the element size; `in` is not read
+ *               when alpha == 0, `out` is not read when beta == 0 (NaN in
+ *               it does not propagate).  They must not overlap unless alpha
+ *               is 0.
+ *   stream      a hipStream_t (NULL: the default stream); asynchronous.
+ *
+ * Errors: GETT_ERROR_INVALID_VALUE (bad dtype, negative extent or stride,
+ * null or misaligned pointer, overlap), GETT_ERROR_NOT_SUPPORTED (rank above
+ * GETT_MAX_RANK, an offset reaching 2^31, output strides that map two
+ * elements to one address), GETT_ERROR_HIP (launch failure).
+ */
+gett_status_t gett_transpose(gett_dtype_t dtype, int rank, const int64_t *extent,
+                             const int64_t *stride_in, const int64_t *stride_out, double alpha,
+                             const void *in, double beta, void *out, void *stream);
+
+/* ------------------------------------------------------------------------
+ * TTGT: Transpose-Transpose-GEMM-Transpose (Sec. 4, Listing 5)
+ *
+ * The approach GETT is measured against: operands that are not already laid
+ * out as matrices are transposed into a workspace (Eq. 4), one GEMM
+ * (rocBLAS) forms the product, and a last transposition folds it into C when
+ * C is not that matrix.  It computes the same contraction as gett_plan /
+ * gett_contract (same mode strings, extents, strides and alpha/beta
+ * semantics) but needs auxiliary memory.
+ * ------------------------------------------------------------------------ */
+
+typedef struct gett_ttgt_plan_s *gett_ttgt_plan_t;
+
+/*
+ * gett_ttgt_plan -- choose the flattening (Sec. 4, Listing 5).
+ *
+ * Arguments as for gett_plan, plus
+ *   max_workspace_bytes  the largest workspace a candidate may need (Table II,
+ *                        --maxWorkspace); negative: no limit.
+ *
+ * For orders of I_m, I_n, I_k and the eight arrangements of the two operands
+ * (which one is the GEMM's left operand, and whether each is stored with its
+ * free or its contracted indices first) the candidate that transposes the
+ * fewest elements wins; ties go to transpositions that keep each tensor's
+ * stride-one index, then to the smaller workspace.  Errors as for gett_plan;
+ * GETT_ERROR_NOT_SUPPORTED also when every candidate needs more workspace
+ * than allowed or a GEMM dimension exceeds 2^31 - 1.  Host only.
+ */
+gett_status_t gett_ttgt_plan(gett_ttgt_plan_t *plan, gett_dtype_t dtype,
+                             const char *modes_C, const int64_t *extent_C, const int64_t *stride_C,
+                             const char *modes_A, const int64_t *extent_A, const int64_t *stride_A,
+                             const char *modes_B, const int64_t *extent_B, const int64_t *stride_B,
+                             int64_t max_workspace_bytes);
+
+/* gett_ttgt_workspace_size -- bytes of device workspace gett_ttgt_contract
+ * needs (0 when no tensor is transposed). */
+gett_status_t gett_ttgt_workspace_size(const gett_ttgt_plan_t plan, uint64_t *bytes);
+
+/*
+ * gett_ttgt_contract -- C <- alpha * A * B + beta * C by TTGT.
+ *
+ *   workspace        device memory of at least gett_ttgt_workspace_size()
+ *                    bytes, 256-byte aligned, not overlapping A, B or C;
+ *                    owned by the caller; may be NULL when the size is 0.
+ *   workspace_bytes  its size.
+ * Other arguments as for gett_contract.  Calls that share a workspace must
+ * not overlap in time.  Asynchronous on `stream`.
+ */
+gett_status_t gett_ttgt_contract(const gett_ttgt_plan_t plan, double alpha, const void *A,
+                                 const void *B, double beta, void *C, void *workspace,
+                                 uint64_t workspace_bytes, void *stream);
+
+/* gett_ttgt_destroy -- free a TTGT plan.  NULL is accepted and ignored. */
+gett_status_t gett_ttgt_destroy(gett_ttgt_plan_t plan);
+
+/* gett_ttgt_describe -- the chosen candidate as a JSON object (orders of the
+ * index sets, GEMM operands and shapes, transposed tensors, workspace);
+ * valid until gett_ttgt_destroy.  "" for NULL. */
+const char *gett_ttgt_describe(const gett_ttgt_plan_t plan);
 
 #ifdef __cplusplus
 }

@@ -70,6 +70,25 @@ def load_library() -> ctypes.CDLL:
                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.gett_destroy.restype = ctypes.c_int
     lib.gett_destroy.argtypes = [ctypes.c_void_p]
+    lib.gett_transpose.restype = ctypes.c_int
+    lib.gett_transpose.argtypes = [ctypes.c_int, ctypes.c_int, i64p, i64p, i64p, ctypes.c_double,
+                                   ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p,
+                                   ctypes.c_void_p]
+    lib.gett_ttgt_plan.restype = ctypes.c_int
+    lib.gett_ttgt_plan.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int,
+                                   ctypes.c_char_p, i64p, i64p,
+                                   ctypes.c_char_p, i64p, i64p,
+                                   ctypes.c_char_p, i64p, i64p, ctypes.c_int64]
+    lib.gett_ttgt_workspace_size.restype = ctypes.c_int
+    lib.gett_ttgt_workspace_size.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_uint64)]
+    lib.gett_ttgt_contract.restype = ctypes.c_int
+    lib.gett_ttgt_contract.argtypes = [ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p]
+    lib.gett_ttgt_destroy.restype = ctypes.c_int
+    lib.gett_ttgt_destroy.argtypes = [ctypes.c_void_p]
+    lib.gett_ttgt_describe.restype = ctypes.c_char_p
+    lib.gett_ttgt_describe.argtypes = [ctypes.c_void_p]
     lib.gett_status_string.restype = ctypes.c_char_p
     lib.gett_status_string.argtypes = [ctypes.c_int]
     lib.gett_plan_describe.restype = ctypes.c_char_p
@@ -114,6 +133,50 @@ def gett_plan_tune(plan, max_candidates: int, A: int, B: int, C: int, stream: in
 
 def gett_destroy(plan) -> int:
     return load_library().gett_destroy(plan)
+
+
+def gett_transpose(dtype: int, extent, stride_in, stride_out, alpha: float, src: int,
+                   beta: float, dst: int, stream: int = 0) -> int:
+    """Eq. 4 over the iteration space `extent`; the permutation is carried by
+    the output strides.  Device pointers and stream as integers."""
+    return load_library().gett_transpose(int(dtype), len(extent), _arr(extent), _arr(stride_in),
+                                         _arr(stride_out), float(alpha), src or None,
+                                         float(beta), dst or None, stream or None)
+
+
+def gett_ttgt_plan(dtype: int, modes_C: str, extent_C, stride_C, modes_A: str, extent_A,
+                   stride_A, modes_B: str, extent_B, stride_B, max_workspace_bytes: int = -1):
+    """Returns (status, TTGT plan handle or None)."""
+    lib = load_library()
+    h = ctypes.c_void_p()
+    st = lib.gett_ttgt_plan(ctypes.byref(h), int(dtype),
+                            modes_C.encode(), _arr(extent_C), _arr(stride_C),
+                            modes_A.encode(), _arr(extent_A), _arr(stride_A),
+                            modes_B.encode(), _arr(extent_B), _arr(stride_B),
+                            int(max_workspace_bytes))
+    return st, (h.value if st == 0 else None)
+
+
+def gett_ttgt_workspace_size(plan):
+    """Returns (status, bytes)."""
+    n = ctypes.c_uint64()
+    st = load_library().gett_ttgt_workspace_size(plan, ctypes.byref(n))
+    return st, int(n.value)
+
+
+def gett_ttgt_contract(plan, alpha: float, A: int, B: int, beta: float, C: int, workspace: int,
+                       workspace_bytes: int, stream: int = 0) -> int:
+    return load_library().gett_ttgt_contract(plan, float(alpha), A or None, B or None,
+                                             float(beta), C or None, workspace or None,
+                                             int(workspace_bytes), stream or None)
+
+
+def gett_ttgt_destroy(plan) -> int:
+    return load_library().gett_ttgt_destroy(plan)
+
+
+def gett_ttgt_describe(plan) -> str:
+    return load_library().gett_ttgt_describe(plan).decode()
 
 
 def gett_status_string(status: int) -> str:

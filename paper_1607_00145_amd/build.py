@@ -21,6 +21,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIBDIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIBDIR, "libgett.so")
 ARCH = "gfx950"
+ROCM_LIB = "/opt/rocm/lib"
 
 
 def hipcc() -> str:
@@ -65,7 +66,8 @@ def build(jobs: int = 0) -> str:
         objs = list(ex.map(compile_one, srcs))
     os.makedirs(LIBDIR, exist_ok=True)
     tmp = LIB + f".tmp{os.getpid()}"
-    cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + objs
+    cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + objs + \
+        ["-L" + ROCM_LIB, "-lrocblas", "-Wl,-rpath," + ROCM_LIB]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

@@ -114,14 +114,15 @@ int64_t max_offset(const Tensor &t)
     return m;
 }
 
-// Strides that may send two elements of C to one address are refused:
-// sorted by stride, each index must step over the whole span of the
-// previous ones.
-bool c_is_injective(const Tensor &c)
+}  // namespace
+
+// Strides that may send two elements to one address are refused: sorted by
+// stride, each index must step over the whole span of the previous ones.
+bool strides_injective(int n, const int64_t *ext, const int64_t *str)
 {
     std::vector<std::pair<int64_t, int64_t>> v;   // (stride, extent)
-    for (size_t i = 0; i < c.modes.size(); ++i)
-        if (c.ext[i] > 1) v.push_back({c.str[i], c.ext[i]});
+    for (int i = 0; i < n; ++i)
+        if (ext[i] > 1) v.push_back({str[i], ext[i]});
     std::sort(v.begin(), v.end());
     int64_t span = 1;   // one past the largest offset reachable so far
     for (auto &p : v) {
@@ -129,6 +130,13 @@ bool c_is_injective(const Tensor &c)
         span = p.first * (p.second - 1) + span;
     }
     return true;
+}
+
+namespace {
+
+bool c_is_injective(const Tensor &c)
+{
+    return strides_injective((int)c.modes.size(), c.ext.data(), c.str.data());
 }
 
 // Merge p then q (p fastest) when q follows p in memory in every tensor that
@@ -186,10 +194,9 @@ const char *mode_name(int m)
 
 }  // namespace
 
-gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, const int64_t *eC,
-                      const int64_t *sC, const char *mA, const int64_t *eA, const int64_t *sA,
-                      const char *mB, const int64_t *eB, const int64_t *sB, uint32_t flags,
-                      const Choice *force)
+gett_status_t front_end(Analysis &an, gett_dtype_t dtype, const char *mC, const int64_t *eC,
+                        const int64_t *sC, const char *mA, const int64_t *eA, const int64_t *sA,
+                        const char *mB, const int64_t *eB, const int64_t *sB, int rank[3])
 {
     if (dtype != GETT_FLOAT32 && dtype != GETT_FLOAT64) return GETT_ERROR_INVALID_VALUE;
     Tensor A, B, C;
@@ -197,8 +204,10 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     if ((st = load_tensor(mC, eC, sC, C)) != GETT_SUCCESS) return st;
     if ((st = load_tensor(mA, eA, sA, A)) != GETT_SUCCESS) return st;
     if ((st = load_tensor(mB, eB, sB, B)) != GETT_SUCCESS) return st;
+    rank[0] = (int)C.modes.size();
+    rank[1] = (int)A.modes.size();
+    rank[2] = (int)B.modes.size();
 
-    Analysis an;
     // ---- classification (Sec. 2.2; Listing 5: the three intersections) ----
     for (size_t i = 0; i < C.modes.size(); ++i) {
         const int ia = A.find(C.modes[i]), ib = B.find(C.modes[i]);
@@ -258,6 +267,20 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         merge_set(an.In, false, true, true, an.merges);
         merge_set(an.Ik, true, true, false, an.merges);
     }
+
+    return GETT_SUCCESS;
+}
+
+gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, const int64_t *eC,
+                      const int64_t *sC, const char *mA, const int64_t *eA, const int64_t *sA,
+                      const char *mB, const int64_t *eB, const int64_t *sB, uint32_t flags,
+                      const Choice *force)
+{
+    Analysis an;
+    int rank[3];
+    const gett_status_t st =
+        front_end(an, dtype, mC, eC, sC, mA, eA, sA, mB, eB, sB, rank);
+    if (st != GETT_SUCCESS) return st;
 
     // ---- operand roles: C's stride-one index on the column (y) side ----
     bool swap = false;
@@ -517,9 +540,9 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
 
     plan.dtype = dtype;
     plan.flags = flags;
-    plan.rank[0] = (int)C.modes.size();
-    plan.rank[1] = (int)A.modes.size();
-    plan.rank[2] = (int)B.modes.size();
+    plan.rank[0] = rank[0];
+    plan.rank[1] = rank[1];
+    plan.rank[2] = rank[2];
     plan.an = an;
     plan.desc = d;
     plan.descScalar = d;

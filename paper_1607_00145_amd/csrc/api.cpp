@@ -16,7 +16,7 @@
 
 using gett::KDesc;
 
-namespace {
+namespace gett {
 
 bool overlaps(const void *p, int64_t nbytesP, const void *q, int64_t nbytesQ)
 {
@@ -24,6 +24,24 @@ bool overlaps(const void *p, int64_t nbytesP, const void *q, int64_t nbytesQ)
     const uintptr_t b0 = (uintptr_t)q, b1 = b0 + (uintptr_t)nbytesQ;
     return a0 < b1 && b0 < a1;
 }
+
+bool operands_ok(gett_dtype_t dtype, const Analysis &an, bool readAB, const void *A,
+                 const void *B, const void *C)
+{
+    const int64_t item = dtype == GETT_FLOAT32 ? 4 : 8;
+    if (!C || (uintptr_t)C % item) return false;
+    if (!readAB) return true;
+    if (!A || !B || (uintptr_t)A % item || (uintptr_t)B % item) return false;
+    const int64_t bytesC = (an.maxOffC + 1) * item;
+    return !overlaps(C, bytesC, A, (an.maxOffA + 1) * item) &&
+           !overlaps(C, bytesC, B, (an.maxOffB + 1) * item);
+}
+
+}  // namespace gett
+
+namespace {
+
+using gett::overlaps;
 
 // Test hook: GETT_FAULT_INJECT=launch makes gett_contract report a failed
 // launch without touching the GPU, so the error path can be exercised on a
@@ -34,17 +52,9 @@ bool inject_launch_fault()
     return v && strcmp(v, "launch") == 0;
 }
 
-// Null, misaligned or overlapping operand pointers (A and B only matter when
-// they are read).
 bool pointers_ok(const gett_plan_s &P, bool readAB, const void *A, const void *B, const void *C)
 {
-    const int64_t item = P.dtype == GETT_FLOAT32 ? 4 : 8;
-    if (!C || (uintptr_t)C % item) return false;
-    if (!readAB) return true;
-    if (!A || !B || (uintptr_t)A % item || (uintptr_t)B % item) return false;
-    const int64_t bytesC = (P.an.maxOffC + 1) * item;
-    return !overlaps(C, bytesC, A, (P.an.maxOffA + 1) * item) &&
-           !overlaps(C, bytesC, B, (P.an.maxOffB + 1) * item);
+    return gett::operands_ok(P.dtype, P.an, readAB, A, B, C);
 }
 
 // The tuned choice of every descriptor tuned in this process (the paper's

@@ -68,6 +68,22 @@ struct gett_plan_s {
 
 namespace gett {
 
+// Parse and validate the three mode lists, classify the indices into I_m,
+// I_n, I_k, drop extent-1 indices and merge super-indices (shared by GETT and
+// TTGT).  rank receives the number of modes of C, A, B as given.
+gett_status_t front_end(Analysis &an, gett_dtype_t dtype, const char *mC, const int64_t *eC,
+                        const int64_t *sC, const char *mA, const int64_t *eA, const int64_t *sA,
+                        const char *mB, const int64_t *eB, const int64_t *sB, int rank[3]);
+
+// Null, misaligned or overlapping operand pointers are refused (A and B only
+// matter when they are read).
+bool overlaps(const void *p, int64_t nbytesP, const void *q, int64_t nbytesQ);
+bool operands_ok(gett_dtype_t dtype, const Analysis &an, bool readAB, const void *A,
+                 const void *B, const void *C);
+
+// True when no two elements of a strided tensor share an address.
+bool strides_injective(int n, const int64_t *ext, const int64_t *str);
+
 // Analyse and fill a plan; returns a status (the plan is unusable on error).
 gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, const int64_t *eC,
                       const int64_t *sC, const char *mA, const int64_t *eA, const int64_t *sA,

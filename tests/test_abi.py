@@ -27,7 +27,9 @@ def test_library_exports_every_declared_symbol():
     lib = g.load_library()
     names = declared_functions()
     assert names == sorted(["gett_plan", "gett_contract", "gett_plan_tune", "gett_destroy",
-                            "gett_status_string", "gett_plan_describe"])
+                            "gett_status_string", "gett_plan_describe", "gett_transpose",
+                            "gett_ttgt_plan", "gett_ttgt_workspace_size", "gett_ttgt_contract",
+                            "gett_ttgt_destroy", "gett_ttgt_describe"])
     for n in names:
         assert hasattr(lib, n), n
     out = subprocess.run(["nm", "-D", "--defined-only", g.LIB_PATH], capture_output=True,
@@ -301,3 +303,125 @@ def test_fig11_sweep_plans(variant):
         assert d["merges"] == []
         assert d["swapped"] is True
         assert d["size_x"] * d["size_y"] == 1152 * 1152 and d["size_k"] == k
+
+
+# ------------------------------------------------------------------ TTGT ---
+
+def ttgt_plan(mc, ma, mb, ext, dtype=g.GETT_FLOAT32, strides=(None, None, None), cap=-1):
+    shp = lambda m: [ext[x] for x in (m.split(",") if "," in m else list(m)) if x]
+    return g.gett_ttgt_plan(dtype, mc, shp(mc), strides[0], ma, shp(ma), strides[1], mb, shp(mb),
+                            strides[2], cap)
+
+
+def ttgt_describe(*a, **k):
+    st, h = ttgt_plan(*a, **k)
+    assert st == 0, g.gett_status_string(st)
+    d = json.loads(g.gett_ttgt_describe(h))
+    st, ws = g.gett_ttgt_workspace_size(h)
+    assert st == 0 and ws == d["workspace_bytes"]
+    g.gett_ttgt_destroy(h)
+    return d
+
+
+def test_ttgt_listing6_example():
+    """Sec. 4, Listing 6: for C_abc = A_ack B_bk neither operand needs a
+    transposition -- (a,c) is a super-index of A's rows -- and the product
+    (a,c) x b is folded into C."""
+    ext = {"a": 5, "b": 6, "c": 7, "k": 8}
+    d = ttgt_describe("abc", "ack", "bk", ext)
+    assert d["transposed"] == ["C"]
+    assert d["transposed_elements"] == 5 * 6 * 7
+    assert d["order_m"] == "a,c" and d["gemm"]["left"] == "A"
+    assert d["gemm"]["op_left"] == "N" and d["gemm"]["op_right"] == "T"
+    assert (d["gemm"]["m"], d["gemm"]["n"], d["gemm"]["k"]) == (35, 6, 8)
+    assert d["stride_one_changes"] == 0
+    assert d["workspace_bytes"] == ((5 * 6 * 7 * 4 + 255) // 256) * 256
+
+
+def test_ttgt_gemm_shaped_needs_nothing():
+    for mc, ma, mb, ops in (("mn", "mk", "kn", ("N", "N")), ("mn", "km", "kn", ("T", "N")),
+                            ("mn", "mk", "nk", ("N", "T")), ("nm", "mk", "kn", None)):
+        d = ttgt_describe(mc, ma, mb, {"m": 9, "n": 10, "k": 11})
+        assert d["transposed"] == [], (mc, ma, mb)
+        assert d["workspace_bytes"] == 0
+        if ops:
+            assert (d["gemm"]["op_left"], d["gemm"]["op_right"]) == ops
+        else:   # C = X^T: B is the left operand
+            assert d["gemm"]["left"] == "B"
+
+
+def test_ttgt_plans_of_workloads():
+    """The flattening of each workload: the fewest elements transposed.  A
+    tensor whose free and contracted indices interleave (A and B of cc4x4, B
+    and C of ccsdt6, all three of gemm4) must be transposed whatever the
+    arrangement; tm3x2's A (a,k,c) and C (a,b,c) interleave too."""
+    exp = {1: ["A", "C"], 2: ["A", "B"], 3: ["A", "B"], 4: ["B", "C"], 5: ["A", "B", "C"]}
+    for w in wl.WORKLOADS:
+        dt = g.GETT_FLOAT32 if w.dtype == "f32" else g.GETT_FLOAT64
+        d = ttgt_describe(w.modes_C, w.modes_A, w.modes_B, w.extents, dtype=dt)
+        assert sorted(d["transposed"]) == exp[w.number], (w.name, d)
+        na, nb, nc = w.numel("A"), w.numel("B"), w.numel("C")
+        size = {"A": na, "B": nb, "C": nc}
+        assert d["transposed_elements"] == sum(size[t] for t in d["transposed"])
+        m, n, k = d["gemm"]["m"], d["gemm"]["n"], d["gemm"]["k"]
+        assert m * n * k * 2 == wl.flop_count(w)
+
+
+def test_ttgt_workspace_cap():
+    ext = {"a": 5, "b": 6, "c": 7, "k": 8}
+    st, h = ttgt_plan("abc", "ack", "bk", ext, cap=100)
+    assert st == g.GETT_ERROR_NOT_SUPPORTED and h is None
+    st, h = ttgt_plan("mn", "mk", "kn", {"m": 9, "n": 10, "k": 11}, cap=0)
+    assert st == 0
+    g.gett_ttgt_destroy(h)
+
+
+@pytest.mark.parametrize("mc,ma,mb,code", [("ab", "ak", "kb,", 2), ("ab", "ak", "bk", 0),
+                                           ("abk", "ak", "bk", 2), ("ab", "aak", "bk", 2)])
+def test_ttgt_plan_validation(mc, ma, mb, code):
+    st, h = ttgt_plan(mc, ma, mb, {"a": 3, "b": 4, "k": 5, "kb": 5})
+    assert st == code
+    if h:
+        g.gett_ttgt_destroy(h)
+
+
+def test_ttgt_contract_host_side_errors():
+    st, h = ttgt_plan("abc", "ack", "bk", {"a": 5, "b": 6, "c": 7, "k": 8})
+    assert st == 0
+    _, ws = g.gett_ttgt_workspace_size(h)
+    A, B, C, W = 1 << 20, 2 << 20, 3 << 20, 4 << 20
+    try:
+        assert g.gett_ttgt_contract(None, 1, A, B, 0, C, W, ws) == g.GETT_ERROR_INVALID_VALUE
+        assert g.gett_ttgt_contract(h, 1, A, B, 0, C, 0, ws) == g.GETT_ERROR_INVALID_VALUE
+        assert g.gett_ttgt_contract(h, 1, A, B, 0, C, W, ws - 1) == g.GETT_ERROR_INVALID_VALUE
+        assert g.gett_ttgt_contract(h, 1, A, B, 0, C, W + 64, ws) == g.GETT_ERROR_INVALID_VALUE
+        assert g.gett_ttgt_contract(h, 1, A, B, 0, C, C, ws) == g.GETT_ERROR_INVALID_VALUE
+        assert g.gett_ttgt_contract(h, 1, A, B, 0, 0, W, ws) == g.GETT_ERROR_INVALID_VALUE
+        assert g.gett_ttgt_contract(h, 1, A, B + 2, 0, C, W, ws) == g.GETT_ERROR_INVALID_VALUE
+    finally:
+        g.gett_ttgt_destroy(h)
+    st, h = ttgt_plan("abc", "ack", "bk", {"a": 0, "b": 6, "c": 7, "k": 8})
+    assert st == 0
+    assert g.gett_ttgt_contract(h, 1, 0, 0, 0, 0, 0, 0) == g.GETT_SUCCESS   # empty C
+    g.gett_ttgt_destroy(h)
+    assert g.gett_ttgt_describe(None) == ""
+    assert g.gett_ttgt_destroy(None) == g.GETT_SUCCESS
+
+
+def test_transpose_host_side_errors():
+    P, Q = 1 << 20, 2 << 20
+    f32 = g.GETT_FLOAT32
+    E = g.GETT_ERROR_INVALID_VALUE
+    assert g.gett_transpose(7, [2, 3], None, [3, 1], 1, P, 0, Q) == E
+    assert g.gett_transpose(f32, [2, -3], None, None, 1, P, 0, Q) == E
+    assert g.gett_transpose(f32, [2, 3], [0, 2], None, 1, P, 0, Q) == E
+    assert g.gett_transpose(f32, [2, 3], None, [3, 1], 1, P, 0, 0) == E
+    assert g.gett_transpose(f32, [2, 3], None, [3, 1], 1, 0, 0, Q) == E
+    assert g.gett_transpose(f32, [2, 3], None, [3, 1], 1, P + 2, 0, Q) == E
+    assert g.gett_transpose(f32, [2, 3], None, [3, 1], 1, P, 0, P + 8) == E        # overlap
+    assert g.gett_transpose(f32, [2] * 13, None, None, 1, P, 0, Q) == g.GETT_ERROR_NOT_SUPPORTED
+    assert g.gett_transpose(f32, [2, 2], None, [1, 1], 1, P, 0, Q) == \
+        g.GETT_ERROR_NOT_SUPPORTED                                                 # not injective
+    assert g.gett_transpose(f32, [1 << 16, 1 << 16], None, None, 1, P, 0, Q) == \
+        g.GETT_ERROR_NOT_SUPPORTED                                                 # offset >= 2^31
+    assert g.gett_transpose(f32, [2, 0, 3], None, None, 1, P, 0, Q) == g.GETT_SUCCESS   # empty
