@@ -17,9 +17,10 @@ stdout.  The line also carries:
                 sample of the same workload;
   workloads     every workload with cold-cache kernel times (minimum and
                 median over runs, each after a 1 GiB cache flush), GFLOP/s,
-                GB/s, fraction of its bound, and an equal-size GEMM (torch ->
-                hipBLASLt/rocBLAS) timed the same way (Sec. 7: the GEMM of
-                sizes S_Im x S_In x S_Ik).
+                GB/s, fraction of its bound, the same contraction by TTGT
+                (Sec. 4) and an equal-size GEMM (torch -> hipBLASLt/rocBLAS)
+                timed the same way (Sec. 7: the GEMM of sizes
+                S_Im x S_In x S_Ik).
 """
 from __future__ import annotations
 
@@ -104,6 +105,36 @@ class Problem:
         self.g.gett_destroy(self.h)
 
 
+class TtgtProblem:
+    """The same workload run by TTGT (Sec. 4): explicit transpositions into a
+    workspace, one rocBLAS GEMM, a fold into C."""
+
+    def __init__(self, p: Problem):
+        import torch
+        g, w = p.g, p.w
+        self.p, self.g = p, g
+        dt = g.GETT_FLOAT32 if w.dtype == "f32" else g.GETT_FLOAT64
+        st, self.h = g.gett_ttgt_plan(dt, w.modes_C, w.shape("C"), None, w.modes_A, w.shape("A"),
+                                      None, w.modes_B, w.shape("B"), None, -1)
+        if st != 0:
+            raise RuntimeError(f"gett_ttgt_plan: {g.gett_status_string(st)}")
+        _, self.nws = g.gett_ttgt_workspace_size(self.h)
+        self.ws = torch.empty(max(self.nws, 1), dtype=torch.uint8, device=p.dev)
+        self.plan = json.loads(g.gett_ttgt_describe(self.h))
+
+    def launch(self, stream):
+        p = self.p
+        st = self.g.gett_ttgt_contract(self.h, p.w.alpha, p.A.data_ptr(), p.B.data_ptr(), p.w.beta,
+                                       p.C.data_ptr(), self.ws.data_ptr(), self.nws,
+                                       stream.cuda_stream)
+        if st != 0:
+            raise RuntimeError(f"gett_ttgt_contract: {self.g.gett_status_string(st)}")
+
+    def close(self):
+        self.g.gett_ttgt_destroy(self.h)
+        del self.ws
+
+
 def time_launches(fn, n, stream, flush=None):
     """Per-launch HIP event times (ms) on `stream`, optionally after a flush."""
     import torch
@@ -183,6 +214,16 @@ def report_workload(w, dev, stream, runs, flush):
                                            "gather_x", "gather_y", "c_vector")}
     rec["plan"]["tile"] = [p.plan["tile"]["mt"], p.plan["tile"]["nt"], p.plan["tile"]["kt"]]
     rec["plan"]["workgroups"] = p.plan["grid"]["workgroups"]
+    t = TtgtProblem(p)
+    for _ in range(3):
+        t.launch(stream)
+    tt = min(time_launches(lambda: t.launch(stream), runs, stream, flush))
+    rec["ttgt_ms_min"] = round(tt, 5)
+    rec["ttgt_gflops"] = round(flops / (tt * 1e-3) / 1e9, 1)
+    rec["ttgt_transposed"] = t.plan["transposed"]
+    rec["ttgt_workspace_bytes"] = t.plan["workspace_bytes"]
+    rec["gett_speedup_over_ttgt"] = round(tt / tmin, 3)
+    t.close()
     p.close()
     M, N, K = p.plan["size_x"], p.plan["size_y"], p.plan["size_k"]
     del p
@@ -215,11 +256,55 @@ def time_gemm(M, N, K, w, dev, stream, runs, flush):
     return gmin
 
 
+TRANSPOSE_CASES = [   # (name, dtype, extents, perm): Eq. 4 with alpha 1, beta 0
+    ("t4_rev_fp32", "f32", [112, 112, 112, 112], [3, 2, 1, 0]),
+    ("t4_keep_fp32", "f32", [112, 112, 112, 112], [0, 2, 3, 1]),
+    ("t6_rev_fp64", "f64", [24] * 6, [5, 4, 3, 2, 1, 0]),
+    ("t2_fp32", "f32", [8192, 8192], [1, 0]),
+]
+
+
+def report_transpose(dev, stream, runs, flush):
+    """The Eq. 4 kernel alone: bytes read + written per launch over its cold time."""
+    import torch
+
+    import paper_1607_00145_amd as g
+    out = []
+    for name, dtype, ext, perm in TRANSPOSE_CASES:
+        tdt = torch.float32 if dtype == "f32" else torch.float64
+        n = int(np.prod(ext))
+        src = torch.rand(n, dtype=tdt, device=dev)
+        dst = torch.empty(n, dtype=tdt, device=dev)
+        sin = list(np.cumprod([1] + ext[:-1]))
+        oext = [ext[p] for p in perm]
+        ostr = list(np.cumprod([1] + oext[:-1]))
+        sout = [0] * len(ext)
+        for j, d in enumerate(perm):
+            sout[d] = int(ostr[j])
+        code = g.GETT_FLOAT32 if dtype == "f32" else g.GETT_FLOAT64
+
+        def fn():
+            st = g.gett_transpose(code, ext, sin, sout, 1.0, src.data_ptr(), 0.0, dst.data_ptr(),
+                                  stream.cuda_stream)
+            if st != 0:
+                raise RuntimeError(g.gett_status_string(st))
+        for _ in range(3):
+            fn()
+        t = min(time_launches(fn, runs, stream, flush))
+        nbytes = 2 * n * src.element_size()
+        out.append({"case": name, "extents": ext, "perm": perm, "ms_min": round(t, 5),
+                    "gbs": round(nbytes / (t * 1e-3) / 1e9, 1),
+                    "frac_hbm_peak": round(nbytes / (t * 1e-3) / (PEAK["hbm_GBs"] * 1e9), 4)})
+        del src, dst
+        torch.cuda.empty_cache()
+    return out
+
+
 def sweep_fig11(dev, stream, runs, flush, max_candidates):
     """Sec. 7.3, Fig. 11 (and the candidate-search study of Fig. 13): both
     contractions, both precisions, S_Ik from 8 to 1024.  One JSON line per
     point: GETT with the model's choice, GETT after gett_plan_tune over the
-    best `max_candidates` candidates, and the equal-size GEMM, all cold."""
+    best `max_candidates` candidates, TTGT, and the equal-size GEMM, all cold."""
     for dtype in ("f32", "f64"):
         peak = (PEAK["f32_TFLOPs"] if dtype == "f32" else PEAK["f64_TFLOPs"]) * 1e12
         for variant in ("a", "b"):
@@ -238,6 +323,11 @@ def sweep_fig11(dev, stream, runs, flush, max_candidates):
                 tt = min(time_launches(lambda: p.launch(stream), runs, stream, flush))
                 tuned_tile = tile()
                 M, N, K = p.plan["size_x"], p.plan["size_y"], p.plan["size_k"]
+                t = TtgtProblem(p)
+                for _ in range(3):
+                    t.launch(stream)
+                tx = min(time_launches(lambda: t.launch(stream), runs, stream, flush))
+                t.close()
                 p.close()
                 del p
                 tg = time_gemm(M, N, K, w, dev, stream, runs, flush)
@@ -250,11 +340,12 @@ def sweep_fig11(dev, stream, runs, flush, max_candidates):
                        "tuned_gflops": round(flops / (tt * 1e-3) / 1e9, 1),
                        "model_of_best": round(best / tm, 4),
                        "frac_mfma_peak": round(flops / (best * 1e-3) / peak, 4),
+                       "ttgt_ms": round(tx, 5), "ttgt_gflops": round(flops / (tx * 1e-3) / 1e9, 1),
                        "gemm_ms": round(tg, 5),
                        "gemm_gflops": round(flops / (tg * 1e-3) / 1e9, 1),
                        "vs_equal_size_gemm": round(tg / best, 4)}
                 log(f"[sweep] {w.name}: model {tm*1e3:.1f} us, tuned {tt*1e3:.1f} us, "
-                    f"gemm {tg*1e3:.1f} us")
+                    f"ttgt {tx*1e3:.1f} us, gemm {tg*1e3:.1f} us")
                 print(json.dumps(rec), flush=True)
 
 
@@ -355,6 +446,8 @@ def main():
             log(f"[bench] report {ww.name}")
             reps.append(report_workload(ww, dev, stream, args.report_runs, flush))
         out["workloads"] = reps
+        log("[bench] report transpose")
+        out["transpose"] = report_transpose(dev, stream, args.report_runs, flush)
         del flush_buf
         torch.cuda.empty_cache()
 

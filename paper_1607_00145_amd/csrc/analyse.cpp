@@ -384,11 +384,13 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     // ---- tile shape: the paper ranks candidates with a performance model
     //      (Sec. 3.4: macro-kernel time from flops / (peak * penalty), packing
     //      and unpacking time from bytes / bandwidth).  Here: MFMA time of the
-    //      busiest compute unit (tiles are dealt to 256 CUs in rounds, each
-    //      tile including its padding) against the C stream through HBM at
-    //      the bandwidth the tile sustains; the longer one bounds the time. ----
+    //      busiest SIMD (the tiles' wavefronts are dealt to the 1024 SIMDs of
+    //      256 CUs; each wavefront's share of a tile, padding included, runs
+    //      at the sustained fraction of one SIMD's peak) against the C stream
+    //      through HBM at the bandwidth the tile sustains; the longer one
+    //      bounds the time. ----
     const double itemB = dtype == GETT_FLOAT32 ? 4.0 : 8.0;
-    const double peakCU = (dtype == GETT_FLOAT32 ? 157.3e12 : 78.6e12) / 256.0;
+    const double peakSimd = (dtype == GETT_FLOAT32 ? 157.3e12 : 78.6e12) / 1024.0;
     const double bytesX = itemB * (double)sizeX * (double)an.sizeK;
     const double bytesY = itemB * (double)sizeY * (double)an.sizeK;
     const double bytesC = itemB * (double)sizeX * (double)sizeY;
@@ -399,9 +401,11 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         const Box b = box_for(c.kt);
         const double tx = (double)((sizeX + c.mt - 1) / c.mt);
         const double ty = (double)((sizeY + c.nt - 1) / c.nt);
-        const double rounds = std::ceil(tx * ty / 256.0);
+        const double waves = tx * ty * c.wm * c.wn * c.ks;
+        const double perSimd = std::ceil(waves / 1024.0);
         const double kpad = (double)std::max<int64_t>(b.nsteps, 1) * c.kt;
-        const double tMfma = rounds * (double)c.mt * c.nt * kpad * 2.0 / (peakCU * c.eff);
+        const double waveFlops = (double)(c.mt / c.wm) * (c.nt / c.wn) * kpad * 2.0 / c.ks;
+        const double tMfma = perSimd * waveFlops / (peakSimd * c.eff);
         // The persistent streaming kernel needs the contracted set in one box.
         const bool canStream = c.stream && b.nsteps <= 1;
         for (int k = 0; k < (canStream ? 2 : 1); ++k) {
@@ -525,7 +529,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     d.nsteps = nsteps;
     const int64_t tilesX = (sizeX + ts.mt - 1) / ts.mt;
     const int64_t tilesY = (sizeY + ts.nt - 1) / ts.nt;
-    if (!an.emptyC && (tilesX * tilesY * ts.wm * ts.wn * 64 >= (int64_t)UINT32_MAX || sizeX >= INT32_MAX ||
+    if (!an.emptyC && (tilesX * tilesY * ts.wm * ts.wn * ts.ks * 64 >= (int64_t)UINT32_MAX || sizeX >= INT32_MAX ||
                        sizeY >= INT32_MAX || nsteps >= INT32_MAX))
         return GETT_ERROR_NOT_SUPPORTED;
     d.tilesX = (int32_t)tilesX;
@@ -581,7 +585,8 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     names("k_order", Ik);
     o << ",\"size_x\":" << sizeX << ",\"size_y\":" << sizeY << ",\"size_k\":" << an.sizeK;
     o << ",\"tile\":{\"id\":" << tile << ",\"mt\":" << ts.mt << ",\"nt\":" << ts.nt << ",\"kt\":" << ts.kt
-      << ",\"waves\":[" << ts.wm << "," << ts.wn << "],\"reads\":[" << ts.rx << "," << ts.ry
+      << ",\"waves\":[" << ts.wm << "," << ts.wn << "],\"k_groups\":" << ts.ks
+      << ",\"reads\":[" << ts.rx << "," << ts.ry
       << "],\"chosen_by\":\"" << how << "\",\"model_us\":" << pick.cost * 1e6 << "}";
     o << ",\"candidates\":[";
     for (size_t i = 0; i < ranked.size(); ++i)
@@ -595,7 +600,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     o << ",\"gather_x\":\"" << mode_name(xmode) << "\",\"gather_y\":\"" << mode_name(ymode)
       << "\",\"c_vector\":" << (cvec ? "true" : "false");
     o << ",\"grid\":{\"tiles_x\":" << tilesX << ",\"tiles_y\":" << tilesY << ",\"workgroups\":"
-      << tilesX * tilesY << ",\"threads\":" << ts.wm * ts.wn * 64 << "}";
+      << tilesX * tilesY << ",\"threads\":" << ts.wm * ts.wn * ts.ks * 64 << "}";
     o << ",\"empty_c\":" << (an.emptyC ? "true" : "false") << ",\"empty_sum\":"
       << (an.emptySum ? "true" : "false");
     char buf[64];
