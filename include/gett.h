@@ -255,6 +255,54 @@ gett_status_t gett_ttgt_destroy(gett_ttgt_plan_t plan);
  * valid until gett_ttgt_destroy.  "" for NULL. */
 const char *gett_ttgt_describe(const gett_ttgt_plan_t plan);
 
+/* ------------------------------------------------------------------------
+ * LoG: Loops-over-GEMM (Sec. 5, Listing 7)
+ *
+ * The second approach GETT is measured against: 2D slices of the operands
+ * are multiplied in place by a GEMM (rocBLAS, strided-batched over one loop
+ * index), with the remaining indices looped over.  No workspace.  Not every
+ * contraction admits it.
+ * ------------------------------------------------------------------------ */
+
+typedef struct gett_log_plan_s *gett_log_plan_t;
+
+/*
+ * gett_log_plan -- choose the GEMM slice and the loops (Sec. 5, Listing 7).
+ *
+ * Arguments as for gett_plan.  The stride-one indices of A, B and C must all
+ * be GEMM indices; when C's stride-one index belongs to B the operands are
+ * exchanged.  A set without a stride-one index contributes its largest
+ * (possibly merged) index, which maximises the GEMM's flop count, the
+ * paper's selection metric.  Returns GETT_ERROR_NOT_SUPPORTED when one index
+ * set holds two stride-one indices (the slices would need strides in both
+ * dimensions), when a slice has no unit-stride dimension or a leading
+ * dimension below its row count, or when a GEMM dimension exceeds 2^31 - 1;
+ * other errors as for gett_plan.  Host only.
+ */
+gett_status_t gett_log_plan(gett_log_plan_t *plan, gett_dtype_t dtype,
+                            const char *modes_C, const int64_t *extent_C, const int64_t *stride_C,
+                            const char *modes_A, const int64_t *extent_A, const int64_t *stride_A,
+                            const char *modes_B, const int64_t *extent_B, const int64_t *stride_B);
+
+/*
+ * gett_log_contract -- C <- alpha * A * B + beta * C by LoG.
+ *
+ * Arguments and pointer rules as for gett_contract.  Enqueues one
+ * strided-batched GEMM per combination of the host-side loop indices on
+ * `stream` (contracted loop indices accumulate: beta is applied by the first
+ * GEMM that touches a slice of C, the others add with beta 1).
+ */
+gett_status_t gett_log_contract(const gett_log_plan_t plan, double alpha, const void *A,
+                                const void *B, double beta, void *C, void *stream);
+
+/* gett_log_destroy -- free a LoG plan.  NULL is accepted and ignored. */
+gett_status_t gett_log_destroy(gett_log_plan_t plan);
+
+/* gett_log_describe -- the chosen GEMM indices, operations, leading
+ * dimensions, batch index and loops as a JSON object; valid until
+ * gett_log_destroy.  "" for NULL. */
+const char *gett_log_describe(const gett_log_plan_t plan);
+
 #ifdef __cplusplus
 }
 #endif

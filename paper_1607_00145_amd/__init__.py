@@ -89,6 +89,19 @@ def load_library() -> ctypes.CDLL:
     lib.gett_ttgt_destroy.argtypes = [ctypes.c_void_p]
     lib.gett_ttgt_describe.restype = ctypes.c_char_p
     lib.gett_ttgt_describe.argtypes = [ctypes.c_void_p]
+    lib.gett_log_plan.restype = ctypes.c_int
+    lib.gett_log_plan.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int,
+                                  ctypes.c_char_p, i64p, i64p,
+                                  ctypes.c_char_p, i64p, i64p,
+                                  ctypes.c_char_p, i64p, i64p]
+    lib.gett_log_contract.restype = ctypes.c_int
+    lib.gett_log_contract.argtypes = [ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p,
+                                      ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p,
+                                      ctypes.c_void_p]
+    lib.gett_log_destroy.restype = ctypes.c_int
+    lib.gett_log_destroy.argtypes = [ctypes.c_void_p]
+    lib.gett_log_describe.restype = ctypes.c_char_p
+    lib.gett_log_describe.argtypes = [ctypes.c_void_p]
     lib.gett_status_string.restype = ctypes.c_char_p
     lib.gett_status_string.argtypes = [ctypes.c_int]
     lib.gett_plan_describe.restype = ctypes.c_char_p
@@ -177,6 +190,32 @@ def gett_ttgt_destroy(plan) -> int:
 
 def gett_ttgt_describe(plan) -> str:
     return load_library().gett_ttgt_describe(plan).decode()
+
+
+def gett_log_plan(dtype: int, modes_C: str, extent_C, stride_C, modes_A: str, extent_A,
+                  stride_A, modes_B: str, extent_B, stride_B):
+    """Returns (status, LoG plan handle or None); status 3 when LoG does not apply."""
+    lib = load_library()
+    h = ctypes.c_void_p()
+    st = lib.gett_log_plan(ctypes.byref(h), int(dtype),
+                           modes_C.encode(), _arr(extent_C), _arr(stride_C),
+                           modes_A.encode(), _arr(extent_A), _arr(stride_A),
+                           modes_B.encode(), _arr(extent_B), _arr(stride_B))
+    return st, (h.value if st == 0 else None)
+
+
+def gett_log_contract(plan, alpha: float, A: int, B: int, beta: float, C: int,
+                      stream: int = 0) -> int:
+    return load_library().gett_log_contract(plan, float(alpha), A or None, B or None,
+                                            float(beta), C or None, stream or None)
+
+
+def gett_log_destroy(plan) -> int:
+    return load_library().gett_log_destroy(plan)
+
+
+def gett_log_describe(plan) -> str:
+    return load_library().gett_log_describe(plan).decode()
 
 
 def gett_status_string(status: int) -> str:

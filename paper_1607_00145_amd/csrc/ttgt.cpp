@@ -23,13 +23,12 @@
 #include <string.h>
 
 #include <algorithm>
-#include <map>
-#include <mutex>
 #include <new>
 #include <sstream>
 #include <string>
 #include <vector>
 
+#include "blas.hpp"
 #include "plan.hpp"
 #include "transpose.hpp"
 
@@ -280,36 +279,23 @@ void describe(gett_ttgt_plan_s &P)
     P.text = o.str();
 }
 
-std::mutex g_blasMutex;
-std::map<int, rocblas_handle> g_handles;   // one per device, kept for the process
-
 gett_status_t gemm(const gett_ttgt_plan_s &P, double alpha, const void *L, const void *R,
                    double beta, void *X, hipStream_t stream)
 {
     const Flattening &b = P.best;
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return GETT_ERROR_HIP;
-    std::lock_guard<std::mutex> lock(g_blasMutex);
-    rocblas_handle &h = g_handles[dev];
-    if (!h && rocblas_create_handle(&h) != rocblas_status_success) {
-        h = nullptr;
-        return GETT_ERROR_HIP;
-    }
-    if (rocblas_set_stream(h, stream) != rocblas_status_success) return GETT_ERROR_HIP;
     const rocblas_operation ta = b.L.opT ? rocblas_operation_transpose : rocblas_operation_none;
     const rocblas_operation tb = b.R.opT ? rocblas_operation_transpose : rocblas_operation_none;
-    rocblas_status s;
-    if (P.dtype == GETT_FLOAT32) {
-        const float a = (float)alpha, c = (float)beta;
-        s = rocblas_sgemm(h, ta, tb, (rocblas_int)P.M, (rocblas_int)P.N, (rocblas_int)P.K, &a,
-                          (const float *)L, (rocblas_int)b.L.ld, (const float *)R, (rocblas_int)b.R.ld,
-                          &c, (float *)X, (rocblas_int)b.ldX);
-    } else {
-        s = rocblas_dgemm(h, ta, tb, (rocblas_int)P.M, (rocblas_int)P.N, (rocblas_int)P.K, &alpha,
-                          (const double *)L, (rocblas_int)b.L.ld, (const double *)R,
-                          (rocblas_int)b.R.ld, &beta, (double *)X, (rocblas_int)b.ldX);
-    }
-    return s == rocblas_status_success ? GETT_SUCCESS : GETT_ERROR_HIP;
+    const rocblas_int m = (rocblas_int)P.M, n = (rocblas_int)P.N, k = (rocblas_int)P.K;
+    const rocblas_int lda = (rocblas_int)b.L.ld, ldb = (rocblas_int)b.R.ld, ldc = (rocblas_int)b.ldX;
+    return with_blas(stream, [&](rocblas_handle h) {
+        if (P.dtype == GETT_FLOAT32) {
+            const float a = (float)alpha, c = (float)beta;
+            return rocblas_sgemm(h, ta, tb, m, n, k, &a, (const float *)L, lda, (const float *)R,
+                                 ldb, &c, (float *)X, ldc);
+        }
+        return rocblas_dgemm(h, ta, tb, m, n, k, &alpha, (const double *)L, lda,
+                             (const double *)R, ldb, &beta, (double *)X, ldc);
+    });
 }
 
 gett_status_t run_move(const gett_ttgt_plan_s &P, const Move &m, double alpha, const void *src,

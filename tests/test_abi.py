@@ -29,7 +29,8 @@ def test_library_exports_every_declared_symbol():
     assert names == sorted(["gett_plan", "gett_contract", "gett_plan_tune", "gett_destroy",
                             "gett_status_string", "gett_plan_describe", "gett_transpose",
                             "gett_ttgt_plan", "gett_ttgt_workspace_size", "gett_ttgt_contract",
-                            "gett_ttgt_destroy", "gett_ttgt_describe"])
+                            "gett_ttgt_destroy", "gett_ttgt_describe", "gett_log_plan",
+                            "gett_log_contract", "gett_log_destroy", "gett_log_describe"])
     for n in names:
         assert hasattr(lib, n), n
     out = subprocess.run(["nm", "-D", "--defined-only", g.LIB_PATH], capture_output=True,
@@ -425,3 +426,98 @@ def test_transpose_host_side_errors():
     assert g.gett_transpose(f32, [1 << 16, 1 << 16], None, None, 1, P, 0, Q) == \
         g.GETT_ERROR_NOT_SUPPORTED                                                 # offset >= 2^31
     assert g.gett_transpose(f32, [2, 0, 3], None, None, 1, P, 0, Q) == g.GETT_SUCCESS   # empty
+
+
+# ------------------------------------------------------------------- LoG ---
+
+def log_plan(mc, ma, mb, ext, dtype=g.GETT_FLOAT32, strides=(None, None, None)):
+    shp = lambda m: [ext[x] for x in (m.split(",") if "," in m else list(m)) if x]
+    return g.gett_log_plan(dtype, mc, shp(mc), strides[0], ma, shp(ma), strides[1], mb, shp(mb),
+                           strides[2])
+
+
+def log_describe(*a, **k):
+    st, h = log_plan(*a, **k)
+    assert st == 0, g.gett_status_string(st)
+    d = json.loads(g.gett_log_describe(h))
+    g.gett_log_destroy(h)
+    return d
+
+
+def test_log_listing8_plan():
+    """Sec. 5, Listing 8: the LoG code printed for C_abcijk = A_ijmc B_mkab
+    (all 24) -- operands exchanged, GEMM C_(ab),(ij) = B^T A^T with the
+    listing's sizes and leading dimensions, loops over c and k."""
+    gold = json.load(open(os.path.join(GOLDEN, "listing8_log.json")))
+    c = gold["contraction"]
+    d = log_describe(c["C"], c["A"], c["B"], {x: c["extent"] for x in "abcijkm"})
+    gm = d["gemm"]
+    assert d["swapped"] is True
+    assert (gm["m"], gm["n"], gm["k"]) == (gold["gemm"]["m"], gold["gemm"]["n"], gold["gemm"]["k"])
+    assert (gm["op_left"], gm["op_right"]) == (gold["gemm"]["transA"], gold["gemm"]["transB"])
+    ld = gold["leading_dims"]
+    assert (gm["lda"], gm["ldb"], gm["ldc"]) == (ld["lda_on_B"], ld["ldb_on_A"], ld["ldc"])
+    assert (gm["m_index"], gm["n_index"], gm["k_index"]) == ("(a,b)", "(i,j)", "m")
+    loops = sorted([d["batch"]["index"]] + d["free_loops"] + d["contracted_loops"])
+    assert loops == sorted(gold["loops"])
+    off = gold["offsets"]
+    per = {"k": (off["B_per_k"], off["C_per_k"]), "c": (off["A_per_c"], off["C_per_c"])}
+    b = d["batch"]
+    assert (b["stride_left"] or b["stride_right"], b["stride_c"]) == per[b["index"]]
+    assert d["gemm_calls"] == 24
+
+
+def test_log_not_applicable():
+    """Listing 7: two stride-one indices in one set (a of C and c of A are
+    both in I_m) leave no slice with one unit-stride dimension."""
+    st, h = log_plan("abc", "cak", "kb", {"a": 4, "b": 5, "c": 6, "k": 7})
+    assert st == g.GETT_ERROR_NOT_SUPPORTED and h is None
+    st, h = log_plan("ab", "ka", "kb", {"a": 4, "b": 5, "k": 7}, strides=(None, [9, 1], None))
+    assert st == 0   # A's stride-one index k is contracted, as B's: same index, allowed
+    g.gett_log_destroy(h)
+
+
+def test_log_gemm_and_swap():
+    d = log_describe("mn", "mk", "kn", {"m": 9, "n": 10, "k": 11})
+    assert d["batch"] is None and d["free_loops"] == [] and d["gemm_calls"] == 1
+    assert (d["gemm"]["op_left"], d["gemm"]["op_right"]) == ("N", "N")
+    d = log_describe("nm", "mk", "kn", {"m": 9, "n": 10, "k": 11})
+    assert d["swapped"] is True        # C's stride-one index n belongs to B
+    assert d["gemm"]["m_index"] == "n"
+
+
+@pytest.mark.parametrize("variant", ["a", "b"])
+def test_log_fig11_slices(variant):
+    """Sec. 7.3: for i1 j i2 - i1 k i2 - j k the GEMM's n is S_j = 1152; for
+    i1 j1 i2 j2 - i1 k i2 - j1 k j2 it is only S_j1 (smaller GEMMs)."""
+    w = wl.fig11(variant, 64)
+    d = log_describe(w.modes_C, w.modes_A, w.modes_B, w.extents)
+    assert d["gemm"]["m_index"] == "i1" and d["gemm"]["k_index"] == "k"
+    if variant == "a":
+        assert d["gemm"]["n"] == 1152 and d["batch"]["index"] == "i2" and d["gemm_calls"] == 1
+    else:
+        assert d["gemm"]["n_index"] == "j1" and d["gemm"]["n"] == 32
+        assert d["gemm_calls"] == 36
+
+
+def test_log_plans_of_workloads():
+    for w in wl.WORKLOADS:
+        dt = g.GETT_FLOAT32 if w.dtype == "f32" else g.GETT_FLOAT64
+        d = log_describe(w.modes_C, w.modes_A, w.modes_B, w.extents, dtype=dt)
+        gm = d["gemm"]
+        batch = d["batch"]["count"] if d["batch"] else 1
+        assert 2 * gm["m"] * gm["n"] * gm["k"] * batch * d["gemm_calls"] == wl.flop_count(w), w.name
+
+
+def test_log_contract_host_side_errors():
+    st, h = log_plan("abc", "akc", "kb", {"a": 5, "b": 6, "c": 7, "k": 8})
+    assert st == 0
+    try:
+        assert g.gett_log_contract(None, 1, 1 << 20, 2 << 20, 0, 3 << 20) == g.GETT_ERROR_INVALID_VALUE
+        assert g.gett_log_contract(h, 1, 1 << 20, 2 << 20, 0, 0) == g.GETT_ERROR_INVALID_VALUE
+        assert g.gett_log_contract(h, 1, 0, 2 << 20, 0, 3 << 20) == g.GETT_ERROR_INVALID_VALUE
+        assert g.gett_log_contract(h, 1, 1 << 20, 2 << 20, 0, (1 << 20) + 4) == \
+            g.GETT_ERROR_INVALID_VALUE
+    finally:
+        g.gett_log_destroy(h)
+    assert g.gett_log_describe(None) == "" and g.gett_log_destroy(None) == 0
