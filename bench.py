@@ -18,7 +18,7 @@ stdout.  The line also carries:
   workloads     every workload with cold-cache kernel times (minimum and
                 median over runs, each after a 1 GiB cache flush), GFLOP/s,
                 GB/s, fraction of its bound, the same contraction by TTGT
-                (Sec. 4) and an equal-size GEMM (torch -> hipBLASLt/rocBLAS)
+                (Sec. 4) and by LoG (Sec. 5), and an equal-size GEMM (torch -> hipBLASLt/rocBLAS)
                 timed the same way (Sec. 7: the GEMM of sizes
                 S_Im x S_In x S_Ik).
 """
@@ -47,10 +47,17 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+# Sources that decide what the GETT kernel does for a given contraction (the
+# analyser's plan, the launch and the kernel templates).  The committed HBM
+# traffic figure is used only while these are unchanged.
+KERNEL_SOURCES = ("analyse.cpp", "api.cpp", "desc.hpp", "kernel.hpp", "launch.hpp",
+                  "launch_f32.hip", "launch_f64.hip", "plan.hpp", "tiles.hpp")
+
+
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_1607_00145_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in KERNEL_SOURCES:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
@@ -133,6 +140,47 @@ class TtgtProblem:
     def close(self):
         self.g.gett_ttgt_destroy(self.h)
         del self.ws
+
+
+class LogProblem:
+    """The same workload run by Loops-over-GEMM (Sec. 5): GEMMs on 2D slices,
+    strided-batched over one loop index.  `ok` is False when LoG does not
+    apply (Listing 7)."""
+
+    def __init__(self, p: Problem):
+        g, w = p.g, p.w
+        self.p, self.g = p, g
+        dt = g.GETT_FLOAT32 if w.dtype == "f32" else g.GETT_FLOAT64
+        st, self.h = g.gett_log_plan(dt, w.modes_C, w.shape("C"), None, w.modes_A, w.shape("A"),
+                                     None, w.modes_B, w.shape("B"), None)
+        self.ok = st == 0
+        if st not in (0, g.GETT_ERROR_NOT_SUPPORTED):
+            raise RuntimeError(f"gett_log_plan: {g.gett_status_string(st)}")
+        self.plan = json.loads(g.gett_log_describe(self.h)) if self.ok else None
+
+    def launch(self, stream):
+        p = self.p
+        st = self.g.gett_log_contract(self.h, p.w.alpha, p.A.data_ptr(), p.B.data_ptr(), p.w.beta,
+                                      p.C.data_ptr(), stream.cuda_stream)
+        if st != 0:
+            raise RuntimeError(f"gett_log_contract: {self.g.gett_status_string(st)}")
+
+    def close(self):
+        if self.ok:
+            self.g.gett_log_destroy(self.h)
+
+
+def time_log(p: Problem, stream, runs, flush):
+    """Cold minimum (ms) of the LoG run of a problem, or None when LoG does not apply."""
+    lp = LogProblem(p)
+    if not lp.ok:
+        return None, None
+    for _ in range(2):
+        lp.launch(stream)
+    t = min(time_launches(lambda: lp.launch(stream), runs, stream, flush))
+    calls = lp.plan["gemm_calls"]
+    lp.close()
+    return t, calls
 
 
 def time_launches(fn, n, stream, flush=None):
@@ -224,6 +272,10 @@ def report_workload(w, dev, stream, runs, flush):
     rec["ttgt_workspace_bytes"] = t.plan["workspace_bytes"]
     rec["gett_speedup_over_ttgt"] = round(tt / tmin, 3)
     t.close()
+    tl, calls = time_log(p, stream, runs, flush)
+    rec["log_ms_min"] = round(tl, 5) if tl else None
+    rec["log_gemm_calls"] = calls
+    rec["gett_speedup_over_log"] = round(tl / tmin, 3) if tl else None
     p.close()
     M, N, K = p.plan["size_x"], p.plan["size_y"], p.plan["size_k"]
     del p
@@ -304,7 +356,8 @@ def sweep_fig11(dev, stream, runs, flush, max_candidates):
     """Sec. 7.3, Fig. 11 (and the candidate-search study of Fig. 13): both
     contractions, both precisions, S_Ik from 8 to 1024.  One JSON line per
     point: GETT with the model's choice, GETT after gett_plan_tune over the
-    best `max_candidates` candidates, TTGT, and the equal-size GEMM, all cold."""
+    best `max_candidates` candidates, TTGT, LoG and the equal-size GEMM, all
+    cold."""
     for dtype in ("f32", "f64"):
         peak = (PEAK["f32_TFLOPs"] if dtype == "f32" else PEAK["f64_TFLOPs"]) * 1e12
         for variant in ("a", "b"):
@@ -328,6 +381,7 @@ def sweep_fig11(dev, stream, runs, flush, max_candidates):
                     t.launch(stream)
                 tx = min(time_launches(lambda: t.launch(stream), runs, stream, flush))
                 t.close()
+                tl, _ = time_log(p, stream, runs, flush)
                 p.close()
                 del p
                 tg = time_gemm(M, N, K, w, dev, stream, runs, flush)
@@ -341,11 +395,14 @@ def sweep_fig11(dev, stream, runs, flush, max_candidates):
                        "model_of_best": round(best / tm, 4),
                        "frac_mfma_peak": round(flops / (best * 1e-3) / peak, 4),
                        "ttgt_ms": round(tx, 5), "ttgt_gflops": round(flops / (tx * 1e-3) / 1e9, 1),
+                       "log_ms": round(tl, 5) if tl else None,
+                       "log_gflops": round(flops / (tl * 1e-3) / 1e9, 1) if tl else None,
                        "gemm_ms": round(tg, 5),
                        "gemm_gflops": round(flops / (tg * 1e-3) / 1e9, 1),
                        "vs_equal_size_gemm": round(tg / best, 4)}
                 log(f"[sweep] {w.name}: model {tm*1e3:.1f} us, tuned {tt*1e3:.1f} us, "
-                    f"ttgt {tx*1e3:.1f} us, gemm {tg*1e3:.1f} us")
+                    f"ttgt {tx*1e3:.1f} us, log {tl*1e3 if tl else float('nan'):.1f} us, "
+                    f"gemm {tg*1e3:.1f} us")
                 print(json.dumps(rec), flush=True)
 
 
