@@ -11,7 +11,7 @@
 //   * indices are split into three groups: P, the input's fastest indices
 //     (their product reaches the tile edge), Q, the output's fastest
 //     indices among the rest, and R, everything else;
-//   * one workgroup moves a TE x TE tile of the (P, Q) plane for one point of
+//   * one workgroup moves a TP x TQ tile of the (P, Q) plane for one point of
 //     R.  Reads run along P (contiguous in the input), the tile passes
 //     through LDS, and writes run along Q (contiguous in the output) -- or
 //     along P when the output's stride-one index is itself in P;
@@ -19,6 +19,8 @@
 //     per workgroup into small LDS tables, so the copy loops do no index
 //     arithmetic beyond two table reads.
 #include <hip/hip_runtime.h>
+
+#include <stdint.h>
 
 #include <algorithm>
 #include <vector>
@@ -28,9 +30,10 @@
 namespace gett {
 namespace {
 
-constexpr int kTE = 64;        // tile edge (elements)
-constexpr int kThreads = 256;  // 4 waves
-constexpr int kRows = kThreads / kTE;
+// Tile edges along P and Q (elements) and threads per workgroup.
+template <typename T> struct Shape;
+template <> struct Shape<float> { static constexpr int TP = 128, TQ = 128, TH = 512; };
+template <> struct Shape<double> { static constexpr int TP = 64, TQ = 64, TH = 256; };
 
 struct TDesc {
     int32_t n[3];                    // indices in P, Q, R
@@ -56,12 +59,24 @@ __device__ inline void decode(const TDesc &d, int g, int32_t lin, int32_t &oi, i
     }
 }
 
-template <typename T>
-__global__ __launch_bounds__(kThreads) void transpose_kernel(const TDesc d, const T *__restrict__ in,
-                                                             T *__restrict__ out, T alpha, T beta)
+template <typename T> struct Vec;
+template <> struct Vec<float> { typedef float __attribute__((ext_vector_type(4))) type; static constexpr int n = 4; };
+template <> struct Vec<double> { typedef double __attribute__((ext_vector_type(2))) type; static constexpr int n = 2; };
+
+// VL / VS: 16-byte vector reads along P / writes along the output's
+// stride-one side (the host has checked that every vector lies within one
+// index run and is aligned); ALONGP: the output's stride-one index is in P.
+template <typename T, bool VL, bool VS, bool ALONGP>
+__global__ __launch_bounds__(Shape<T>::TH) void transpose_kernel(const TDesc d, const T *__restrict__ in,
+                                                                 T *__restrict__ out, T alpha, T beta)
 {
-    __shared__ T tile[kTE][kTE + 1];   // [q][p]
-    __shared__ int32_t pin[kTE], pout[kTE], qin[kTE], qout[kTE];
+    constexpr int kTP = Shape<T>::TP, kTQ = Shape<T>::TQ, kThreads = Shape<T>::TH;
+    typedef typename Vec<T>::type vec;
+    constexpr int VW = Vec<T>::n;
+    constexpr int RL = VL ? VW : 1;   // elements per read
+    constexpr int RS = VS ? VW : 1;   // elements per write
+    __shared__ T tile[kTQ][kTP + 1];   // [q][p]
+    __shared__ int32_t pin[kTP], pout[kTP], qin[kTQ], qout[kTQ];
 
     const uint32_t b = blockIdx.x;
     const int32_t tp = (int32_t)(b % (uint32_t)d.tiles[0]);
@@ -72,63 +87,112 @@ __global__ __launch_bounds__(kThreads) void transpose_kernel(const TDesc d, cons
     decode(d, 2, r, rin, rout);
 
     const int t = threadIdx.x;
-    if (t < kTE) {
-        const int32_t p = tp * kTE + t;
+    static_assert(kTP + kTQ <= kThreads, "one table entry per thread");
+    if (t < kTP) {
+        const int32_t p = tp * kTP + t;
         int32_t oi = -1, oo = -1;
         if (p < d.size[0]) decode(d, 0, p, oi, oo);
         pin[t] = oi;
         pout[t] = oo;
-    } else if (t < 2 * kTE) {
-        const int32_t q = tq * kTE + (t - kTE);
+    } else if (t < kTP + kTQ) {
+        const int32_t q = tq * kTQ + (t - kTP);
         int32_t oi = -1, oo = -1;
         if (q < d.size[1]) decode(d, 1, q, oi, oo);
-        qin[t - kTE] = oi;
-        qout[t - kTE] = oo;
+        qin[t - kTP] = oi;
+        qout[t - kTP] = oo;
     }
     __syncthreads();
 
     const T *src = in + rin;
     T *dst = out + rout;
-    const int lane = t % kTE, row = t / kTE;
     const bool readIn = alpha != T(0);
-    // read along P: lanes take consecutive P positions
+    const bool readOut = beta != T(0);
+    // read along P: a thread takes RL consecutive P positions of one Q row
     if (readIn) {
-        const int32_t oi = pin[lane];
+        constexpr int PER = kTP / RL;   // threads per Q row
+        constexpr int N = kTQ * PER / kThreads;
+        const int pl = (t % PER) * RL;
+        const int32_t oi = pin[pl];
+        T v[N][RL];
 #pragma unroll
-        for (int j = 0; j < kTE / kRows; ++j) {
-            const int ql = row + kRows * j;
+        for (int j = 0; j < N; ++j) {
+            const int ql = t / PER + (kThreads / PER) * j;
             const int32_t qo = qin[ql];
-            T v = T(0);
-            if (oi >= 0 && qo >= 0) v = src[oi + qo];
-            tile[ql][lane] = v;
+            if (oi >= 0 && qo >= 0) {
+                if constexpr (VL) {
+                    const vec x = *reinterpret_cast<const vec *>(src + oi + qo);
+#pragma unroll
+                    for (int e = 0; e < RL; ++e) v[j][e] = x[e];
+                } else {
+                    v[j][0] = src[oi + qo];
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < RL; ++e) v[j][e] = T(0);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < N; ++j) {
+            const int ql = t / PER + (kThreads / PER) * j;
+#pragma unroll
+            for (int e = 0; e < RL; ++e) tile[ql][pl + e] = v[j][e];
         }
     }
     __syncthreads();
-    if (d.alongP) {   // write along P
-        const int32_t oo = pout[lane];
-        if (oo < 0) return;
+    // write: a thread takes RS consecutive positions along the output's
+    // stride-one side (P when ALONGP, else Q)
+    constexpr int LEN = ALONGP ? kTP : kTQ;   // tile edge along the write direction
+    constexpr int PER = LEN / RS;
+    constexpr int N = (kTP * kTQ / LEN) * PER / kThreads;
+    const int a = (t % PER) * RS;   // position along the write direction
 #pragma unroll
-        for (int j = 0; j < kTE / kRows; ++j) {
-            const int ql = row + kRows * j;
-            const int32_t qo = qout[ql];
-            if (qo < 0) continue;
-            T v = readIn ? alpha * tile[ql][lane] : T(0);
-            if (beta != T(0)) v = beta * dst[oo + qo] + v;
-            dst[oo + qo] = v;
-        }
-    } else {          // write along Q: lanes take consecutive Q positions
-        const int32_t qo = qout[lane];
-        if (qo < 0) return;
+    for (int j = 0; j < N; ++j) {
+        const int c = t / PER + (kThreads / PER) * j;   // position across it
+        const int pl = ALONGP ? a : c, ql = ALONGP ? c : a;
+        const int32_t oo = pout[pl], qo = qout[ql];
+        if (oo < 0 || qo < 0) continue;
+        T *o = dst + oo + qo;
+        T w[RS];
 #pragma unroll
-        for (int j = 0; j < kTE / kRows; ++j) {
-            const int pl = row + kRows * j;
-            const int32_t oo = pout[pl];
-            if (oo < 0) continue;
-            T v = readIn ? alpha * tile[lane][pl] : T(0);
-            if (beta != T(0)) v = beta * dst[oo + qo] + v;
-            dst[oo + qo] = v;
+        for (int e = 0; e < RS; ++e)
+            w[e] = readIn ? alpha * (ALONGP ? tile[ql][pl + e] : tile[ql + e][pl]) : T(0);
+        if constexpr (VS) {
+            vec x;
+            if (readOut) {
+                const vec old = *reinterpret_cast<const vec *>(o);
+#pragma unroll
+                for (int e = 0; e < RS; ++e) x[e] = beta * old[e] + w[e];
+            } else {
+#pragma unroll
+                for (int e = 0; e < RS; ++e) x[e] = w[e];
+            }
+            *reinterpret_cast<vec *>(o) = x;
+        } else {
+            *o = readOut ? beta * *o + w[0] : w[0];
         }
     }
+}
+
+template <typename T, bool VL, bool VS>
+void launch_t(bool alongP, unsigned blocks, hipStream_t s, const TDesc &d, const void *in, void *out,
+              double alpha, double beta)
+{
+    if (alongP)
+        hipLaunchKernelGGL((transpose_kernel<T, VL, VS, true>), dim3(blocks), dim3(Shape<T>::TH), 0, s, d,
+                           static_cast<const T *>(in), static_cast<T *>(out), (T)alpha, (T)beta);
+    else
+        hipLaunchKernelGGL((transpose_kernel<T, VL, VS, false>), dim3(blocks), dim3(Shape<T>::TH), 0, s, d,
+                           static_cast<const T *>(in), static_cast<T *>(out), (T)alpha, (T)beta);
+}
+
+template <typename T>
+void launch_typed(bool vl, bool vs, bool alongP, unsigned blocks, hipStream_t s, const TDesc &d,
+                  const void *in, void *out, double alpha, double beta)
+{
+    if (vl && vs) launch_t<T, true, true>(alongP, blocks, s, d, in, out, alpha, beta);
+    else if (vl) launch_t<T, true, false>(alongP, blocks, s, d, in, out, alpha, beta);
+    else if (vs) launch_t<T, false, true>(alongP, blocks, s, d, in, out, alpha, beta);
+    else launch_t<T, false, false>(alongP, blocks, s, d, in, out, alpha, beta);
 }
 
 struct Idx {
@@ -160,19 +224,21 @@ gett_status_t transpose_launch(gett_dtype_t dtype, int rank, const int64_t *ext,
                 }
             }
     }
+    const int kTP = dtype == GETT_FLOAT32 ? Shape<float>::TP : Shape<double>::TP;
+    const int kTQ = dtype == GETT_FLOAT32 ? Shape<float>::TQ : Shape<double>::TQ;
     // P: by input stride until the tile edge is covered; Q: by output stride
     std::vector<Idx> byIn = v, P, Q, R;
     std::stable_sort(byIn.begin(), byIn.end(), [](const Idx &a, const Idx &b) { return a.sin < b.sin; });
     int64_t sp = 1, sq = 1;
     size_t i = 0;
-    for (; i < byIn.size() && sp < kTE; ++i) {
+    for (; i < byIn.size() && sp < kTP; ++i) {
         P.push_back(byIn[i]);
         sp *= byIn[i].ext;
     }
     std::vector<Idx> others(byIn.begin() + i, byIn.end());
     std::stable_sort(others.begin(), others.end(), [](const Idx &a, const Idx &b) { return a.sout < b.sout; });
     size_t j = 0;
-    for (; j < others.size() && sq < kTE; ++j) {
+    for (; j < others.size() && sq < kTQ; ++j) {
         Q.push_back(others[j]);
         sq *= others[j].ext;
     }
@@ -201,8 +267,8 @@ gett_status_t transpose_launch(gett_dtype_t dtype, int rank, const int64_t *ext,
     d.size[0] = (int32_t)sp;
     d.size[1] = (int32_t)sq;
     d.size[2] = (int32_t)sr;
-    d.tiles[0] = (int32_t)((sp + kTE - 1) / kTE);
-    d.tiles[1] = (int32_t)((sq + kTE - 1) / kTE);
+    d.tiles[0] = (int32_t)((sp + kTP - 1) / kTP);
+    d.tiles[1] = (int32_t)((sq + kTQ - 1) / kTQ);
     // the output's smallest stride decides the write direction
     int64_t minOut = INT64_MAX;
     bool inP = true;
@@ -216,14 +282,26 @@ gett_status_t transpose_launch(gett_dtype_t dtype, int rank, const int64_t *ext,
     const int64_t blocks = (int64_t)d.tiles[0] * d.tiles[1] * sr;
     if (blocks >= INT32_MAX) return GETT_ERROR_NOT_SUPPORTED;
     if (blocks == 0) return GETT_SUCCESS;
+    // 16-byte vectors: the run's first index is stride-one with an extent that
+    // is a multiple of the vector, every other stride is a multiple of it, and
+    // the base pointer is 16-byte aligned -- then no vector straddles an index
+    // boundary or the end of a ragged tile, and every vector is aligned.
+    const int vw = dtype == GETT_FLOAT32 ? 4 : 2;
+    auto vec_ok = [&](const std::vector<Idx> &lead, bool inSide, const void *base) {
+        if (lead.empty() || ((uintptr_t)base % 16)) return false;
+        const Idx &f = lead[0];
+        if ((inSide ? f.sin : f.sout) != 1 || f.ext % vw) return false;
+        for (auto *g : {&P, &Q, &R})
+            for (auto &x : *g)
+                if (&x != &f && (inSide ? x.sin : x.sout) % vw) return false;
+        return true;
+    };
+    const bool vl = alpha != 0.0 && vec_ok(P, true, in);
+    const bool vs = vec_ok(d.alongP ? P : Q, false, out);
     if (dtype == GETT_FLOAT32)
-        hipLaunchKernelGGL(transpose_kernel<float>, dim3((unsigned)blocks), dim3(kThreads), 0, stream,
-                           d, static_cast<const float *>(in), static_cast<float *>(out),
-                           (float)alpha, (float)beta);
+        launch_typed<float>(vl, vs, d.alongP != 0, (unsigned)blocks, stream, d, in, out, alpha, beta);
     else
-        hipLaunchKernelGGL(transpose_kernel<double>, dim3((unsigned)blocks), dim3(kThreads), 0,
-                           stream, d, static_cast<const double *>(in), static_cast<double *>(out),
-                           alpha, beta);
+        launch_typed<double>(vl, vs, d.alongP != 0, (unsigned)blocks, stream, d, in, out, alpha, beta);
     return hipGetLastError() == hipSuccess ? GETT_SUCCESS : GETT_ERROR_HIP;
 }
 

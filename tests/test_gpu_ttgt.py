@@ -80,6 +80,10 @@ def test_transpose_random(gpu, seed, dtype):
     ([1000], [0]),                    # one index: an axpby
     ([70, 90], [0, 1]),               # the output's stride-one index is the input's
     ([2, 2, 2, 2, 2, 2, 2, 2, 2, 2, 2, 2], [11, 10, 9, 8, 7, 6, 5, 4, 3, 2, 1, 0]),
+    ([132, 68], [1, 0]),              # 16-byte reads and writes, ragged tiles
+    ([68, 5, 7], [0, 2, 1]),          # vector writes along the shared stride-one index
+    ([8, 12, 20], [2, 0, 1]),         # vector reads over a compound tile side
+    ([36, 6, 10], [1, 2, 0]),
 ])
 def test_transpose_shapes(gpu, dtype, shape, perm):
     rng = np.random.default_rng(61_000 + sum(shape))
