@@ -36,6 +36,7 @@ constexpr TileShape kTilesF32[] = {
     {128, 128, 16, 2, 2, 4, 4, 3, 1, 2, 2, 0.71f, 0.675f, 0.64f},
     {64, 256, 16, 1, 4, 4, 4, 3, 1, 2, 2, 0.70f, 0.70f, 0.63f},
     {64, 64, 32, 2, 2, 2, 2, 2, 2, 2, 0, 0.70f, 0.35f, 0.0f, 2},
+    {128, 128, 32, 2, 2, 4, 4, 1, 1, 2, 0, 0.806f, 0.61f, 0.0f},
 };
 constexpr TileShape kTilesF64[] = {
     {128, 128, 16, 2, 2, 2, 2, 1, 2, 2, 0, 0.56f, 0.34f, 0.0f},
