@@ -408,8 +408,11 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         const double tMfma = perSimd * waveFlops / (peakSimd * c.eff);
         // The persistent streaming kernel needs the contracted set in one box.
         const bool canStream = c.stream && b.nsteps <= 1;
+        // A stream carried by fewer workgroups than CUs gets that share of the
+        // bandwidth (each CU's memory pipeline has its own limit).
+        const double cuShare = std::min(1.0, tx * ty / 256.0);
         for (int k = 0; k < (canStream ? 2 : 1); ++k) {
-            const double bwFrac = k ? c.sbw : c.bw;
+            const double bwFrac = (k ? c.sbw : c.bw) * cuShare;
             const double tMem =
                 (bytesC + 0.05 * (bytesX * ty + bytesY * tx)) / (8.0e12 * bwFrac);
             Candidate cd;
