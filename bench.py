@@ -200,29 +200,45 @@ def time_launches(fn, n, stream, flush=None):
     return ts
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, target_s=15.0):
-    """The oracle on a bounded, evenly spaced sample of C's elements."""
+    """The oracle on a bounded, evenly spaced sample of C's elements, with all
+    host threads, and on a smaller sample with one thread."""
     import oracle
     A, B, Cin = wl.make_inputs(w)
     nC = w.numel("C")
     flops_per_elem = wl.flop_count(w) / nC
     threads = oracle.max_threads()
+
+    def run(n, nthreads):
+        pts = np.linspace(0, nC - 1, n).astype(np.int64)
+        t = time.perf_counter()
+        oracle.contract(w.modes_C, w.modes_A, w.modes_B, A, B, w.alpha, w.beta, Cin,
+                        shape_C=w.shape("C"), points=pts, nthreads=nthreads)
+        return time.perf_counter() - t
+
     # calibrate on a small sample, then size the measured sample to ~target_s
     n0 = min(nC, 200_000)
-    pts = np.linspace(0, nC - 1, n0).astype(np.int64)
-    t = time.perf_counter()
-    oracle.contract(w.modes_C, w.modes_A, w.modes_B, A, B, w.alpha, w.beta, Cin,
-                    shape_C=w.shape("C"), points=pts)
-    dt0 = time.perf_counter() - t
+    dt0 = run(n0, threads)
     n = int(min(nC, max(n0, n0 * target_s / max(dt0, 1e-6))))
-    pts = np.linspace(0, nC - 1, n).astype(np.int64)
-    t = time.perf_counter()
-    oracle.contract(w.modes_C, w.modes_A, w.modes_B, A, B, w.alpha, w.beta, Cin,
-                    shape_C=w.shape("C"), points=pts)
-    dt = time.perf_counter() - t
+    dt = run(n, threads)
+    n1 = min(nC, 2_000_000)
+    dt1 = run(n1, 1)
     return {"value": round(flops_per_elem * n / dt / 1e9, 4), "unit": "GFLOP/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"{n} of {nC} elements of C ({w.name}), evenly spaced; {dt:.1f} s"}
+            "sample": f"{n} of {nC} elements of C ({w.name}), evenly spaced; {dt:.1f} s",
+            "cpu_model": cpu_model(),
+            "single_thread_value": round(flops_per_elem * n1 / dt1 / 1e9, 4),
+            "single_thread_sample": f"{n1} elements, {dt1:.1f} s"}
 
 
 def traffic_for(kernel_name: str, workload: str):
