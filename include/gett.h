@@ -50,7 +50,7 @@ typedef enum {
      * between tensors */
     GETT_ERROR_INVALID_INDICES = 2,
     /* rank above GETT_MAX_RANK; C strides that may map two elements of C to
-     * one address; a tensor whose largest element offset reaches 2^31 */
+     * one address; a tensor whose largest element offset reaches 2^31 - 1 */
     GETT_ERROR_NOT_SUPPORTED = 3,
     /* a HIP runtime call (kernel launch) or a rocBLAS call failed */
     GETT_ERROR_HIP = 4,
@@ -188,7 +188,7 @@ const char *gett_plan_describe(const gett_plan_t plan);
  *
  * Errors: GETT_ERROR_INVALID_VALUE (bad dtype, negative extent or stride,
  * null or misaligned pointer, overlap), GETT_ERROR_NOT_SUPPORTED (rank above
- * GETT_MAX_RANK, an offset reaching 2^31, output strides that map two
+ * GETT_MAX_RANK, an offset reaching 2^31 - 1, output strides that map two
  * elements to one address), GETT_ERROR_HIP (launch failure).
  */
 gett_status_t gett_transpose(gett_dtype_t dtype, int rank, const int64_t *extent,

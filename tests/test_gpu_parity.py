@@ -225,3 +225,40 @@ def test_streaming_kernel_many_tiles_per_workgroup(gpu, monkeypatch, number):
     rng = np.random.default_rng(w.seed + 7)
     check_case(gpu, rng, (w.modes_C, w.modes_A, w.modes_B),
                (w.shape("C"), w.shape("A"), w.shape("B")), w.np_dtype, w.alpha, w.beta)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_largest_supported_offsets(gpu, dtype):
+    """C with 2^31 - 2^16 elements (element offsets up to just below 2^31, the
+    largest the plan accepts): every element written, sampled values against
+    the oracle, the far corner included.  One more row of C is refused."""
+    import torch
+    m, n, k = 65536, 32767, 8
+    tdt = torch.float32 if dtype == np.float32 else torch.float64
+    code = g.GETT_FLOAT32 if dtype == np.float32 else g.GETT_FLOAT64
+    st, h = g.gett_plan(code, "mn", [m, n + 1], None, "mk", [m, k], None, "kn", [k, n + 1], None, 0)
+    assert st == g.GETT_ERROR_NOT_SUPPORTED      # its last offset m * (n + 1) - 1 = 2^31 - 1
+    rng = np.random.default_rng(70_000)
+    A = rng.uniform(-1, 1, (m, k)).astype(dtype)
+    B = rng.uniform(-1, 1, (k, n)).astype(dtype)
+    tA = torch.from_numpy(np.asfortranarray(A).reshape(-1, order="F")).to(gpu)
+    tB = torch.from_numpy(np.asfortranarray(B).reshape(-1, order="F")).to(gpu)
+    tC = torch.full((m * n,), float("nan"), dtype=tdt, device=gpu)
+    st, h = g.gett_plan(code, "mn", [m, n], None, "mk", [m, k], None, "kn", [k, n], None, 0)
+    assert st == 0
+    try:
+        st = g.gett_contract(h, 1.0, tA.data_ptr(), tB.data_ptr(), 0.0, tC.data_ptr(),
+                             torch.cuda.current_stream().cuda_stream)
+        assert st == 0
+        torch.cuda.synchronize()
+    finally:
+        g.gett_destroy(h)
+    assert bool(torch.isfinite(tC).all()), "some element of C was not written"
+    nC = m * n
+    pts = np.concatenate([rng.integers(0, nC, 2040),
+                          [0, 1, m - 1, m, nC // 2, nC - m, nC - 2, nC - 1]])
+    got = tC[torch.from_numpy(pts).to(gpu)].cpu().numpy()
+    del tC
+    torch.cuda.empty_cache()
+    ref = oracle.contract("mn", "mk", "kn", A, B, 1.0, 0.0, None, shape_C=[m, n], points=pts)
+    assert oracle.rel_error(got, ref) <= TOL[dtype]

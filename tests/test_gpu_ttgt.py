@@ -224,3 +224,25 @@ def test_ttgt_alpha_zero_and_empty_sum(gpu, dtype):
     ext["k"] = 0
     check_ttgt(gpu, rng, ("abc", "akc", "kb"), (shp("abc"), shp("akc"), shp("kb")), dtype, 1.0,
                0.5, ("gapped",) * 3)
+
+
+def test_transpose_largest_supported_offsets(gpu):
+    """An 8.6 GB fp32 matrix (offsets just below 2^31 - 1) transposed: every
+    output element written, sampled elements exact."""
+    import torch
+    m, n = 65536, 32767
+    src = torch.rand(m * n, dtype=torch.float32, device=gpu)
+    dst = torch.full((m * n,), float("nan"), dtype=torch.float32, device=gpu)
+    st = g.gett_transpose(g.GETT_FLOAT32, [m, n], [1, m], [n, 1], 1.0, src.data_ptr(), 0.0,
+                          dst.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    assert st == 0
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(dst).all())
+    rng = np.random.default_rng(71_000)
+    i = np.concatenate([rng.integers(0, m, 2000), [0, m - 1, m - 1, 0]])
+    j = np.concatenate([rng.integers(0, n, 2000), [0, n - 1, 0, n - 1]])
+    a = src[torch.from_numpy(i + j * m).to(gpu)].cpu().numpy()
+    b = dst[torch.from_numpy(j + i * n).to(gpu)].cpu().numpy()
+    assert np.array_equal(a, b)
+    assert g.gett_transpose(g.GETT_FLOAT32, [m, n + 1], [1, m], [n + 1, 1], 1.0, src.data_ptr(),
+                            0.0, dst.data_ptr(), 0) == g.GETT_ERROR_NOT_SUPPORTED
