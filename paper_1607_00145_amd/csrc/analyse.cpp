@@ -401,10 +401,10 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         const Box b = box_for(c.kt);
         const double tx = (double)((sizeX + c.mt - 1) / c.mt);
         const double ty = (double)((sizeY + c.nt - 1) / c.nt);
-        const double waves = tx * ty * c.wm * c.wn * c.ks;
+        const double waves = tx * ty * c.wm * c.wn;
         const double perSimd = std::ceil(waves / 1024.0);
         const double kpad = (double)std::max<int64_t>(b.nsteps, 1) * c.kt;
-        const double waveFlops = (double)(c.mt / c.wm) * (c.nt / c.wn) * kpad * 2.0 / c.ks;
+        const double waveFlops = (double)(c.mt / c.wm) * (c.nt / c.wn) * kpad * 2.0;
         const double tMfma = perSimd * waveFlops / (peakSimd * c.eff);
         // The persistent streaming kernel needs the contracted set in one box.
         const bool canStream = c.stream && b.nsteps <= 1;
@@ -532,7 +532,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     d.nsteps = nsteps;
     const int64_t tilesX = (sizeX + ts.mt - 1) / ts.mt;
     const int64_t tilesY = (sizeY + ts.nt - 1) / ts.nt;
-    if (!an.emptyC && (tilesX * tilesY * ts.wm * ts.wn * ts.ks * 64 >= (int64_t)UINT32_MAX || sizeX >= INT32_MAX ||
+    if (!an.emptyC && (tilesX * tilesY * ts.wm * ts.wn * 64 >= (int64_t)UINT32_MAX || sizeX >= INT32_MAX ||
                        sizeY >= INT32_MAX || nsteps >= INT32_MAX))
         return GETT_ERROR_NOT_SUPPORTED;
     d.tilesX = (int32_t)tilesX;
@@ -588,8 +588,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     names("k_order", Ik);
     o << ",\"size_x\":" << sizeX << ",\"size_y\":" << sizeY << ",\"size_k\":" << an.sizeK;
     o << ",\"tile\":{\"id\":" << tile << ",\"mt\":" << ts.mt << ",\"nt\":" << ts.nt << ",\"kt\":" << ts.kt
-      << ",\"waves\":[" << ts.wm << "," << ts.wn << "],\"k_groups\":" << ts.ks
-      << ",\"reads\":[" << ts.rx << "," << ts.ry
+      << ",\"waves\":[" << ts.wm << "," << ts.wn << "],\"reads\":[" << ts.rx << "," << ts.ry
       << "],\"chosen_by\":\"" << how << "\",\"model_us\":" << pick.cost * 1e6 << "}";
     o << ",\"candidates\":[";
     for (size_t i = 0; i < ranked.size(); ++i)
@@ -603,7 +602,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     o << ",\"gather_x\":\"" << mode_name(xmode) << "\",\"gather_y\":\"" << mode_name(ymode)
       << "\",\"c_vector\":" << (cvec ? "true" : "false");
     o << ",\"grid\":{\"tiles_x\":" << tilesX << ",\"tiles_y\":" << tilesY << ",\"workgroups\":"
-      << tilesX * tilesY << ",\"threads\":" << ts.wm * ts.wn * ts.ks * 64 << "}";
+      << tilesX * tilesY << ",\"threads\":" << ts.wm * ts.wn * 64 << "}";
     o << ",\"empty_c\":" << (an.emptyC ? "true" : "false") << ",\"empty_sum\":"
       << (an.emptySum ? "true" : "false");
     char buf[64];

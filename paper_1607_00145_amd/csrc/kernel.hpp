@@ -300,10 +300,8 @@ __device__ __forceinline__ void box_tables(const KDesc &d, int tid, int *kX, int
     }
 }
 
-// The register tile of one wavefront and the operations on it.  With KS > 1
-// the workgroup holds KS groups of WM x WN wavefronts; group kg multiplies
-// positions [kg * KT / KS, (kg + 1) * KT / KS) of every K box.
-template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int KS = 1>
+// The register tile of one wavefront and the operations on it.
+template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY>
 struct WaveTile {
     static constexpr int VW = Traits<T>::VW;
     static constexpr int WTM = MT / WM;   // wave tile rows
@@ -316,7 +314,6 @@ struct WaveTile {
     static_assert(RY == 1 || RY == 2 || RY == 4, "read width");
     static_assert(RX <= VW && RY <= VW, "at most 16 bytes per LDS read");
     static_assert(KT % 4 == 0, "K tile must be a multiple of the MFMA depth");
-    static_assert((KT / 4) % KS == 0, "each wave group takes whole MFMA steps of the box");
     static constexpr int NR = 4 * RX;       // rows of one epilogue group owned by a lane
     static constexpr bool kVecC = RY == VW; // a lane owns VW consecutive columns
     static constexpr int CGV = CB / RY;     // column groups per wave
@@ -326,16 +323,14 @@ struct WaveTile {
     typedef RVec<T, RY> YV;
 
     accv acc[RB][CB];
-    int wm, wn, kg, l16, g;
+    int wm, wn, l16, g;
 
     __device__ __forceinline__ void init(int tid)
     {
         const int lane = tid & 63;
         const int wave = tid >> 6;
-        const int sw = wave % (WM * WN);
-        kg = wave / (WM * WN);
-        wm = sw % WM;
-        wn = sw / WM;
+        wm = wave % WM;
+        wn = wave / WM;
         l16 = lane & 15;
         g = lane >> 4;
     }
@@ -354,11 +349,10 @@ struct WaveTile {
     template <int PX, int PY>
     __device__ __forceinline__ void macro(const T *xs, const T *ys)
     {
-        constexpr int KSL = KT / KS;   // positions of this wave group's slice
-        const T *xt = xs + wm * WTM + RX * l16 + (KS > 1 ? kg * KSL * PX : 0);
-        const T *yt = ys + wn * WTN + RY * l16 + (KS > 1 ? kg * KSL * PY : 0);
+        const T *xt = xs + wm * WTM + RX * l16;
+        const T *yt = ys + wn * WTN + RY * l16;
 #pragma unroll
-        for (int ks = 0; ks < KSL / 4; ++ks) {
+        for (int ks = 0; ks < KT / 4; ++ks) {
             const int k = 4 * ks + g;
             typename XV::type av[RB / RX];
             typename YV::type bv[CB / RY];
@@ -374,35 +368,6 @@ struct WaveTile {
                 for (int b = 0; b < CB; ++b)
                     acc[a][b] = mfma16x16x4(XV::at(av[a / RX], a % RX), YV::at(bv[b / RY], b % RY),
                                             acc[a][b]);
-        }
-    }
-
-    // Adds the partial tiles of wave groups 1..KS-1 into group 0 through LDS
-    // (red: MT * NT elements), in group order.  Called by every thread.
-    __device__ __forceinline__ void reduce(T *red, int tid)
-    {
-        constexpr int NTH1 = WM * WN * 64;
-        const int slot = tid % NTH1;
-#pragma unroll
-        for (int src = 1; src < KS; ++src) {
-            if (kg == src) {
-#pragma unroll
-                for (int a = 0; a < RB; ++a)
-#pragma unroll
-                    for (int b = 0; b < CB; ++b)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) red[((a * CB + b) * 4 + r) * NTH1 + slot] = acc[a][b][r];
-            }
-            __syncthreads();
-            if (kg == 0) {
-#pragma unroll
-                for (int a = 0; a < RB; ++a)
-#pragma unroll
-                    for (int b = 0; b < CB; ++b)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) acc[a][b][r] += red[((a * CB + b) * 4 + r) * NTH1 + slot];
-            }
-            if (src + 1 < KS) __syncthreads();
         }
     }
 
@@ -493,25 +458,20 @@ struct WaveTile {
 // s+2 are issued before the MFMAs of box s, so a gather has two boxes' worth
 // of MFMA time to arrive before its values are written to LDS.
 template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int WPE, int PF,
-          int NBUF, int KS, int XMODE, int YMODE>
-__global__ void __launch_bounds__(WM *WN *KS * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
+          int NBUF, int XMODE, int YMODE>
+__global__ void __launch_bounds__(WM *WN * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
                   T *__restrict__ C, const T alpha, const T beta)
 {
     static_assert(PF == 1 || PF == 2, "prefetch depth");
     static_assert(NBUF == 2 || (NBUF == 1 && PF == 1), "one LDS buffer goes with one stage");
-    constexpr int NTH = WM * WN * KS * 64;
+    constexpr int NTH = WM * WN * 64;
     typedef Gather<T, MT, KT, XMODE, NTH, PF> GX;
     typedef Gather<T, NT, KT, YMODE, NTH, PF> GY;
-    typedef WaveTile<T, MT, NT, KT, WM, WN, RX, RY, KS> WT;
+    typedef WaveTile<T, MT, NT, KT, WM, WN, RX, RY> WT;
 
-    // Packed panels; after the last box the same memory holds the partial
-    // tiles of the wave groups (KS > 1).
-    constexpr int kPanels = NBUF * KT * (GX::PITCH + GY::PITCH);
-    constexpr int kPool = (KS > 1 && MT * NT > kPanels) ? MT * NT : kPanels;
-    __shared__ __attribute__((aligned(16))) T pool[kPool];
-    T(*xs)[KT * GX::PITCH] = reinterpret_cast<T(*)[KT * GX::PITCH]>(pool);
-    T(*ys)[KT * GY::PITCH] = reinterpret_cast<T(*)[KT * GY::PITCH]>(pool + NBUF * KT * GX::PITCH);
+    __shared__ __attribute__((aligned(16))) T xs[NBUF][KT * GX::PITCH];
+    __shared__ __attribute__((aligned(16))) T ys[NBUF][KT * GY::PITCH];
     // Element offsets fit in 31 bits (the plan refuses larger tensors); -1 marks
     // a row or column outside the tensor.
     __shared__ int rowX[MT], rowY[NT], offCx[MT], offCy[NT];
@@ -587,11 +547,6 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
             step(S0(), s);
             if (s + 1 < nsteps) step(S1(), s + 1);
         }
-    }
-    if constexpr (KS > 1) {
-        // every wavefront has passed the last barrier after its final reads of the panels
-        w.reduce(pool, tid);
-        if (w.kg != 0) return;   // group 0 unpacks the sum
     }
     w.unpack(C, offCx, offCy, alpha, beta, d.cvec != 0);
 }

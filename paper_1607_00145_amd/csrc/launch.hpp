@@ -39,16 +39,15 @@ hipError_t launch_one(const KDesc &d, const void *X, const void *Y, void *C, dou
     constexpr TileShape t = TileTable<T>::tiles[TI];
     const unsigned tiles = (unsigned)d.tilesX * (unsigned)d.tilesY;
     if (tiles == 0) return hipSuccess;
-    const int threads = t.wm * t.wn * t.ks * 64;
+    const int threads = t.wm * t.wn * 64;
     if constexpr (KIND == 0) {
         hipLaunchKernelGGL(
-            (gett_macro_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.wpe, t.pf, t.nbuf,
-                               t.ks, XM, YM>),
+            (gett_macro_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.wpe, t.pf, t.nbuf, XM,
+                               YM>),
             dim3(tiles), dim3(threads), 0, stream, d, static_cast<const T *>(X),
             static_cast<const T *>(Y), static_cast<T *>(C), static_cast<T>(alpha),
             static_cast<T>(beta));
     } else {
-        static_assert(t.ks == 1, "the streaming kernel has one wave group");
         auto k = gett_stream_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.stream, XM, YM>;
         const unsigned grid = persistent_grid(k, threads, tiles);
         if (grid == 0) return hipErrorInvalidValue;

@@ -6,8 +6,7 @@
 // m_C, n_C, k_C (Sec. 3.3); the register tile of one wavefront,
 // (MT/WM) x (NT/WN) built from 16x16 MFMA blocks, plays the role of
 // m_R x n_R (Sec. 3.1).  RX / RY are the rows each lane reads from LDS at
-// once on the x / y side (1, or 16 bytes' worth).  A workgroup has
-// WM x WN x KS wavefronts.  `eff` and `bw` feed the
+// once on the x / y side (1, or 16 bytes' worth).  `eff` and `bw` feed the
 // analyser's cost model; they were measured on MI355X with the workloads of
 // the benchmark.
 #pragma once
@@ -24,10 +23,6 @@ struct TileShape {
     float eff;   // fraction of the MFMA peak sustained when compute-bound
     float bw;    // fraction of the HBM peak sustained when streaming C (macro-kernel)
     float sbw;   // the same for the streaming kernel
-    int ks = 1;  // wavefront groups sharing each K box: group g multiplies the
-                 // g-th slice of the box's KT positions, and the partial tiles
-                 // are added in LDS before the unpack (more wavefronts for
-                 // tiles that are few but deep in K)
 };
 
 constexpr TileShape kTilesF32[] = {
@@ -35,8 +30,9 @@ constexpr TileShape kTilesF32[] = {
     {64, 64, 16, 1, 1, 4, 4, 1, 1, 2, 0, 0.67f, 0.62f, 0.0f},
     {128, 128, 16, 2, 2, 4, 4, 3, 1, 2, 2, 0.71f, 0.675f, 0.64f},
     {64, 256, 16, 1, 4, 4, 4, 3, 1, 2, 2, 0.70f, 0.70f, 0.63f},
-    {64, 64, 32, 2, 2, 2, 2, 2, 2, 2, 0, 0.70f, 0.35f, 0.0f, 2},
     {128, 128, 32, 2, 2, 4, 4, 1, 1, 2, 0, 0.806f, 0.61f, 0.0f},
+    {64, 32, 32, 2, 2, 2, 1, 2, 2, 2, 0, 0.64f, 0.35f, 0.0f},
+    {32, 64, 32, 2, 2, 1, 2, 2, 2, 2, 0, 0.65f, 0.35f, 0.0f},
 };
 constexpr TileShape kTilesF64[] = {
     {128, 128, 16, 2, 2, 2, 2, 1, 2, 2, 0, 0.56f, 0.34f, 0.0f},
@@ -51,7 +47,8 @@ constexpr TileShape kTilesF64[] = {
     {128, 64, 24, 2, 2, 2, 2, 3, 1, 1, 0, 0.50f, 0.615f, 0.0f},
     {64, 128, 24, 1, 4, 2, 2, 3, 1, 1, 0, 0.50f, 0.59f, 0.0f},
     {64, 128, 24, 2, 2, 2, 2, 3, 1, 1, 0, 0.50f, 0.668f, 0.0f},
-    {64, 64, 32, 2, 2, 2, 2, 2, 2, 2, 0, 0.43f, 0.34f, 0.0f, 2},
+    {64, 32, 16, 2, 2, 2, 1, 2, 2, 2, 0, 0.60f, 0.485f, 0.0f},
+    {32, 64, 16, 2, 2, 1, 2, 2, 2, 2, 0, 0.60f, 0.49f, 0.0f},
 };
 constexpr int kNumTilesF32 = sizeof(kTilesF32) / sizeof(kTilesF32[0]);
 constexpr int kNumTilesF64 = sizeof(kTilesF64) / sizeof(kTilesF64[0]);
