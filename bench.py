@@ -3,7 +3,7 @@
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-report]
                     [--no-cpu-baseline]
-    python bench.py --sweep fig11 [--max-candidates N] [--report-runs R]
+    python bench.py --sweep fig11|appendix_a [--max-candidates N] [--report-runs R]
 
 A step is one contraction C <- alpha*A*B + beta*C of the headline workload
 (bw4x3_fp32: C[a,b,c,d] = A[a,e,b] * B[e,d,c], a..d = 112, e = 16,
@@ -72,18 +72,28 @@ def bound_of(w) -> str:
 class Problem:
     """One workload on the device, planned."""
 
-    def __init__(self, w, dev):
+    def __init__(self, w, dev, on_device: bool = False):
         import torch
 
         import paper_1607_00145_amd as g
         self.w, self.g, self.dev = w, g, dev
-        A, B, Cin = wl.make_inputs(w)
-        self.host = (A, B, Cin)
-        flat = lambda t: torch.from_numpy(np.asfortranarray(t).reshape(-1, order="F")).to(dev)
-        self.A, self.B = flat(A), flat(B)
-        self.C0 = flat(Cin) if Cin is not None else None
-        self.C = self.C0.clone() if Cin is not None else torch.zeros(w.numel("C"), dtype=self.A.dtype,
-                                                                     device=dev)
+        if on_device:
+            # timing only: U[-1,1] drawn on the device (seeded), no host copy
+            gen = torch.Generator(device=dev)
+            gen.manual_seed(w.seed)
+            dt = torch.float32 if w.dtype == "f32" else torch.float64
+            draw = lambda n: torch.rand(n, generator=gen, dtype=dt, device=dev) * 2 - 1
+            self.host = None
+            self.A, self.B = draw(w.numel("A")), draw(w.numel("B"))
+            self.C0 = draw(w.numel("C")) if w.beta != 0 else None
+        else:
+            A, B, Cin = wl.make_inputs(w)
+            self.host = (A, B, Cin)
+            flat = lambda t: torch.from_numpy(np.asfortranarray(t).reshape(-1, order="F")).to(dev)
+            self.A, self.B = flat(A), flat(B)
+            self.C0 = flat(Cin) if Cin is not None else None
+        self.C = self.C0.clone() if self.C0 is not None else torch.zeros(
+            w.numel("C"), dtype=self.A.dtype, device=dev)
         dt = g.GETT_FLOAT32 if w.dtype == "f32" else g.GETT_FLOAT64
         st, self.h = g.gett_plan(dt, w.modes_C, w.shape("C"), None, w.modes_A, w.shape("A"), None,
                                  w.modes_B, w.shape("B"), None, 0)
@@ -368,58 +378,72 @@ def report_transpose(dev, stream, runs, flush):
     return out
 
 
-def sweep_fig11(dev, stream, runs, flush, max_candidates):
-    """Sec. 7.3, Fig. 11 (and the candidate-search study of Fig. 13): both
-    contractions, both precisions, S_Ik from 8 to 1024.  One JSON line per
-    point: GETT with the model's choice, GETT after gett_plan_tune over the
-    best `max_candidates` candidates, TTGT, LoG and the equal-size GEMM, all
-    cold."""
-    for dtype in ("f32", "f64"):
+def sweep_points(sweep):
+    """(tag, workload) pairs of a sweep: Fig. 11 (Sec. 7.3) or the benchmark
+    of Appendix A (Tables III / IV)."""
+    if sweep == "fig11":
+        for dtype in ("f32", "f64"):
+            for variant in ("a", "b"):
+                for k in wl.FIG11_K:
+                    yield "fig11", wl.fig11(variant, k, dtype)
+    else:
+        from workloads.appendix_a import appendix_workloads
+        for dtype in ("f32", "f64"):
+            for w in appendix_workloads(dtype):
+                yield "appendix_a", w
+
+
+def sweep_run(sweep, dev, stream, runs, flush, max_candidates):
+    """One JSON line per point: GETT with the model's choice, GETT after
+    gett_plan_tune over the best `max_candidates` candidates, TTGT, LoG (when
+    it applies) and the equal-size GEMM, all cold."""
+    for tag, w in sweep_points(sweep):
+        dtype = w.dtype
         peak = (PEAK["f32_TFLOPs"] if dtype == "f32" else PEAK["f64_TFLOPs"]) * 1e12
-        for variant in ("a", "b"):
-            for k in wl.FIG11_K:
-                w = wl.fig11(variant, k, dtype)
-                flops = wl.flop_count(w)
-                p = Problem(w, dev)
-                tile = lambda: [p.plan["tile"][x] for x in ("mt", "nt", "kt")] + [p.plan["kernel"]]
-                model_tile = tile()
-                for _ in range(3):
-                    p.launch(stream)
-                tm = min(time_launches(lambda: p.launch(stream), runs, stream, flush))
-                p.tune(max_candidates)
-                for _ in range(3):
-                    p.launch(stream)
-                tt = min(time_launches(lambda: p.launch(stream), runs, stream, flush))
-                tuned_tile = tile()
-                M, N, K = p.plan["size_x"], p.plan["size_y"], p.plan["size_k"]
-                t = TtgtProblem(p)
-                for _ in range(3):
-                    t.launch(stream)
-                tx = min(time_launches(lambda: t.launch(stream), runs, stream, flush))
-                t.close()
-                tl, _ = time_log(p, stream, runs, flush)
-                p.close()
-                del p
-                tg = time_gemm(M, N, K, w, dev, stream, runs, flush)
-                best = min(tm, tt)
-                rec = {"sweep": "fig11", "contraction": w.name, "expression": w.expression(),
-                       "dtype": dtype, "S_Ik": k, "bound": bound_of(w),
-                       "model_ms": round(tm, 5), "model_tile": model_tile,
-                       "model_gflops": round(flops / (tm * 1e-3) / 1e9, 1),
-                       "tuned_ms": round(tt, 5), "tuned_tile": tuned_tile,
-                       "tuned_gflops": round(flops / (tt * 1e-3) / 1e9, 1),
-                       "model_of_best": round(best / tm, 4),
-                       "frac_mfma_peak": round(flops / (best * 1e-3) / peak, 4),
-                       "ttgt_ms": round(tx, 5), "ttgt_gflops": round(flops / (tx * 1e-3) / 1e9, 1),
-                       "log_ms": round(tl, 5) if tl else None,
-                       "log_gflops": round(flops / (tl * 1e-3) / 1e9, 1) if tl else None,
-                       "gemm_ms": round(tg, 5),
-                       "gemm_gflops": round(flops / (tg * 1e-3) / 1e9, 1),
-                       "vs_equal_size_gemm": round(tg / best, 4)}
-                log(f"[sweep] {w.name}: model {tm*1e3:.1f} us, tuned {tt*1e3:.1f} us, "
-                    f"ttgt {tx*1e3:.1f} us, log {tl*1e3 if tl else float('nan'):.1f} us, "
-                    f"gemm {tg*1e3:.1f} us")
-                print(json.dumps(rec), flush=True)
+        k = w.extents.get("k")
+        flops = wl.flop_count(w)
+        p = Problem(w, dev, on_device=True)
+        tile = lambda: [p.plan["tile"][x] for x in ("mt", "nt", "kt")] + [p.plan["kernel"]]
+        model_tile = tile()
+        for _ in range(3):
+            p.launch(stream)
+        tm = min(time_launches(lambda: p.launch(stream), runs, stream, flush))
+        p.tune(max_candidates)
+        for _ in range(3):
+            p.launch(stream)
+        tt = min(time_launches(lambda: p.launch(stream), runs, stream, flush))
+        tuned_tile = tile()
+        M, N, K = p.plan["size_x"], p.plan["size_y"], p.plan["size_k"]
+        t = TtgtProblem(p)
+        for _ in range(3):
+            t.launch(stream)
+        tx = min(time_launches(lambda: t.launch(stream), runs, stream, flush))
+        t.close()
+        tl, _ = time_log(p, stream, runs, flush)
+        p.close()
+        del p
+        tg = time_gemm(M, N, K, w, dev, stream, runs, flush)
+        best = min(tm, tt)
+        rec = {"sweep": tag, "contraction": w.name, "expression": w.expression(),
+               "dtype": dtype, "S_Ik": k if tag == "fig11" else None, "bound": bound_of(w),
+               "model_ms": round(tm, 5), "model_tile": model_tile,
+               "model_gflops": round(flops / (tm * 1e-3) / 1e9, 1),
+               "tuned_ms": round(tt, 5), "tuned_tile": tuned_tile,
+               "tuned_gflops": round(flops / (tt * 1e-3) / 1e9, 1),
+               "model_of_best": round(best / tm, 4),
+               "frac_mfma_peak": round(flops / (best * 1e-3) / peak, 4),
+               "frac_hbm_peak": round(wl.algorithmic_bytes(w) / (best * 1e-3) /
+                                      (PEAK["hbm_GBs"] * 1e9), 4),
+               "ttgt_ms": round(tx, 5), "ttgt_gflops": round(flops / (tx * 1e-3) / 1e9, 1),
+               "log_ms": round(tl, 5) if tl else None,
+               "log_gflops": round(flops / (tl * 1e-3) / 1e9, 1) if tl else None,
+               "gemm_ms": round(tg, 5),
+               "gemm_gflops": round(flops / (tg * 1e-3) / 1e9, 1),
+               "vs_equal_size_gemm": round(tg / best, 4)}
+        log(f"[sweep] {w.name}: model {tm*1e3:.1f} us, tuned {tt*1e3:.1f} us, "
+            f"ttgt {tx*1e3:.1f} us, log {tl*1e3 if tl else float('nan'):.1f} us, "
+            f"gemm {tg*1e3:.1f} us")
+        print(json.dumps(rec), flush=True)
 
 
 def main():
@@ -431,8 +455,9 @@ def main():
     ap.add_argument("--report-runs", type=int, default=20)
     ap.add_argument("--no-report", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--sweep", choices=["fig11"], default=None,
-                    help="run the S_Ik sweep of Fig. 11 instead (one JSON line per point)")
+    ap.add_argument("--sweep", choices=["fig11", "appendix_a"], default=None,
+                    help="run a sweep instead: the S_Ik sweep of Fig. 11 or the 48-contraction "
+                         "benchmark of Appendix A (one JSON line per point)")
     ap.add_argument("--max-candidates", type=int, default=16,
                     help="candidates gett_plan_tune times in the sweep")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -463,7 +488,8 @@ def main():
         return
     if args.sweep:
         flush_buf = torch.empty(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
-        sweep_fig11(dev, stream, args.report_runs, lambda: flush_buf.zero_(), args.max_candidates)
+        sweep_run(args.sweep, dev, stream, args.report_runs, lambda: flush_buf.zero_(),
+                  args.max_candidates)
         return
     w = wl.BY_NAME[args.workload]
 
