@@ -71,6 +71,14 @@ typedef struct gett_plan_s *gett_plan_t;
 /* Use element-wise gathers for A and B and element-wise C accesses even
  * where 16-byte vector accesses are possible (a slower reference variant). */
 #define GETT_FLAG_SCALAR 2u
+/* Do not split an index in two to keep a second stride-one run inside the
+ * tiles (Sec. 3.2.1: the sub-tensors keep the stride-one index of every
+ * tensor).  By default, when C's stride-one index and the column operand's
+ * stride-one index are different free indices, or A's and B's stride-one
+ * indices are different contracted indices, a block of one is placed before
+ * the other so that both are read (written) in runs; with this flag the
+ * tiles follow the (merged) indices whole. */
+#define GETT_FLAG_NO_SPLIT 4u
 
 /*
  * gett_plan -- analyse a contraction and choose its kernel (Sec. 3.2-3.3).

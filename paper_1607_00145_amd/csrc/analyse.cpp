@@ -189,7 +189,11 @@ void json_set(std::ostringstream &o, const char *key, const std::vector<Index> &
 
 const char *mode_name(int m)
 {
-    return m == kGatherRowVec ? "row-vector" : m == kGatherKVec ? "k-vector" : "scalar";
+    return m == kGatherRowVec         ? "row-vector"
+           : m == kGatherKVec         ? "k-vector"
+           : m == kGatherRowVecStrided ? "row-vector-strided"
+           : m == kGatherKVecStrided  ? "k-vector-strided"
+                                      : "scalar";
 }
 
 }  // namespace
@@ -334,7 +338,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     const int VW = dtype == GETT_FLOAT32 ? 4 : 2;
     const int64_t sizeX = swap ? an.sizeN : an.sizeM;
     const int64_t sizeY = swap ? an.sizeM : an.sizeN;
-    const int nk = (int)Ik.size();
+    int nk = (int)Ik.size();
     // A contracted stride-one run gathered as vectors needs whole vectors per block.
     auto kvec_ok = [&](auto strOf) {
         if (strOf(Ik[0]) != 1) return false;
@@ -344,6 +348,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         return true;
     };
     const bool wantKvec = !(flags & GETT_FLAG_SCALAR) && (kvec_ok(sX) || kvec_ok(sY));
+    int kvecIdx = 0;   // contracted index that vector gathers run along (1 after a K split)
     struct Box {
         int kj;
         int64_t tj, kbox, nblk, nsteps;
@@ -365,11 +370,12 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
                 if (Ik[b.kj].extent % t == 0) { best = t; break; }
             if (best * 2 > tj) tj = best;
         }
-        if (wantKvec && b.kj == 0 && tj % VW) {
+        // The block of the index that vectors run along holds whole vectors.
+        if (b.kj == kvecIdx && (wantKvec || kvecIdx > 0) && tj % VW) {
             const int64_t t2 = (tj / VW) * VW;
             if (t2 >= VW) {
                 tj = t2;
-                while (Ik[0].extent % tj && tj > VW) tj -= VW;   // keep it dividing when possible
+                while (Ik[b.kj].extent % tj && tj > VW) tj -= VW;   // keep it dividing when possible
             }
         }
         b.tj = tj;
@@ -456,6 +462,124 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     const int kind = pick.kind;
     const double bestMfma = pick.tMfma, bestMem = pick.tMem;
     const TileShape &ts = tile_shape(dtype, tile);
+
+    // ---- index splitting (Sec. 3.2.1, Fig. 5: the sub-tensors keep the
+    //      stride-one index of every tensor; Examples 1-2: one index read as
+    //      two).  The tiles are linear ranges of each set in its order, so a
+    //      set whose first index is one tensor's stride-one index and whose
+    //      second is another's holds both runs only when the first is
+    //      blocked: (u, v, ...) becomes (u_in, v, u_out, ...) with u_in of
+    //      extent f.  Two cases:
+    //        columns -- C's stride-one index u and the column operand's
+    //                   stride-one index v are different free indices of
+    //                   the column set: C is written in runs of f elements,
+    //                   Y is read in 16-byte vectors along v;
+    //        K box   -- the row operand's stride-one index u and the column
+    //                   operand's v are different contracted indices: X is
+    //                   read in vectors along u_in, Y along v.
+    //      f is a power of two dividing S_u; the vectors of Y then gather
+    //      elements f rows (K positions) apart. ----
+    int ysplit = 0;   // 0, kGatherRowVecStrided or kGatherKVecStrided
+    int yes = 1;
+    auto split_front = [](std::vector<Index> &set, size_t u, size_t v, int64_t f) {
+        Index in = set[u], out = set[u];
+        in.extent = f;
+        in.name = set[u].name + "<" + std::to_string(f);
+        out.extent = set[u].extent / f;
+        out.name = set[u].name + ">" + std::to_string(f);
+        out.strA *= f;
+        out.strB *= f;
+        out.strC *= f;
+        std::vector<Index> next;
+        next.push_back(in);
+        next.push_back(set[v]);
+        if (out.extent > 1) next.push_back(out);
+        for (size_t i = 0; i < set.size(); ++i)
+            if (i != u && i != v) next.push_back(set[i]);
+        set.swap(next);
+    };
+    auto pow2_part = [](int64_t e) { return e & -e; };
+    if (!(flags & (GETT_FLAG_SCALAR | GETT_FLAG_NO_SPLIT)) && !an.emptyC && !an.emptySum) {
+        // which set holds each operand's stride-one index
+        auto unit_in = [](const std::vector<Index> &set, auto strOf) -> int {
+            for (size_t i = 0; i < set.size(); ++i)
+                if (strOf(set[i]) == 1 && set[i].extent > 1) return (int)i;
+            return -1;
+        };
+        const int yRow = unit_in(Iy, sY), yK = unit_in(Ik, sY), xK = unit_in(Ik, sX);
+        auto aligned = [&](const std::vector<Index> &set, auto strOf, int skip) {
+            for (size_t i = 0; i < set.size(); ++i)
+                if ((int)i != skip && strOf(set[i]) % VW) return false;
+            return true;
+        };
+        if (yRow > 0 && Iy[0].strC == 1 && Iy[yRow].extent % VW == 0 &&
+            (int)Iy.size() < kMaxDims) {
+            // Columns.  A tile then writes C in runs of f elements and reads Y
+            // in runs of NT/f elements along v; in the whole-index order it
+            // writes runs of up to NT along u and reads Y in runs of NT over
+            // the extents before v.  Runs are priced per byte: a read run of
+            // L bytes at max(1, 64 / L), a write run at max(1, 128 / L)^2
+            // (partial lines are far costlier to write than to read: on
+            // MI355X, C runs under 64 bytes slowed the column-split
+            // contractions of Appendix A 1.4-3.5x, 32-byte read runs did not).
+            // f minimises Y's plus C's price; the whole-index order is kept
+            // where it is cheaper (a Y that is small next to C).
+            const double Ybytes = itemB * (double)sizeY * (double)an.sizeK;
+            const double Cbytes = itemB * (double)sizeX * (double)sizeY;
+            auto readPrice = [](double L) { return std::max(1.0, 64.0 / L); };
+            auto writePrice = [](double L) {
+                const double r = std::max(1.0, 128.0 / L);
+                return r * r;
+            };
+            auto runs = [&](double elems, double cap) { return std::max(1.0, std::min(elems, cap)); };
+            double before = 1;
+            for (int i = 0; i < yRow; ++i) before *= (double)Iy[i].extent;
+            const double vExt = (double)Iy[yRow].extent, uExt = (double)Iy[0].extent;
+            double best = Ybytes * readPrice(itemB * runs(ts.nt / before, vExt)) +
+                          Cbytes * writePrice(itemB * runs(std::min<double>(ts.nt, uExt), uExt));
+            int64_t f = 0;
+            for (int64_t t = VW; t <= pow2_part(Iy[0].extent) && t * itemB <= 128; t *= 2) {
+                if (ts.nt % (t * VW)) continue;
+                const double c = Ybytes * readPrice(itemB * runs((double)ts.nt / t, vExt)) +
+                                 Cbytes * writePrice(itemB * t);
+                if (c < best) { best = c; f = t; }
+            }
+            if (const char *fs = getenv("GETT_SPLIT_F")) f = atoi(fs);   // tuning hook
+            std::vector<Index> trial = Iy;
+            if (f >= VW && (f & (f - 1)) == 0 && Iy[0].extent % f == 0 && ts.nt % (f * VW) == 0) {
+                split_front(trial, 0, (size_t)yRow, f);
+                if (aligned(trial, sY, 1) && aligned(Ik, sY, -1)) {
+                    Iy.swap(trial);
+                    ysplit = kGatherRowVecStrided;
+                    yes = (int)f;
+                }
+            }
+        } else if (xK >= 0 && yK >= 0 && xK != yK && Ik[yK].extent % VW == 0 &&
+                   (int)Ik.size() < kMaxDims) {
+            // K box: X runs of f (a multiple of VW), at least two vectors of v
+            // per box line when the box allows
+            int64_t cap = 1;
+            while (cap * 2 * VW <= ts.kt) cap *= 2;
+            int64_t f = std::min<int64_t>(pow2_part(Ik[xK].extent), cap);
+            while (f > VW && f * VW * 2 > ts.kt) f /= 2;
+            std::vector<Index> trial = Ik;
+            split_front(trial, (size_t)xK, (size_t)yK, f);
+            if (f >= VW && ts.kt % (f * VW) == 0 && aligned(trial, sY, 1) && aligned(Iy, sY, -1)) {
+                Ik.swap(trial);
+                nk = (int)Ik.size();
+                kvecIdx = 1;
+                // the streaming kernel takes the contracted set in one box
+                if (kind == 1 && box_for(ts.kt).nsteps > 1) {
+                    Ik.swap(trial);
+                    nk = (int)Ik.size();
+                    kvecIdx = 0;
+                } else {
+                    ysplit = kGatherKVecStrided;
+                    yes = (int)f;
+                }
+            }
+        }
+    }
     const Box box = box_for(ts.kt);
     // A contraction bound by the C stream walks C in memory order: x indices
     // by C stride (the row operand's stride-one index stays first when it is
@@ -494,7 +618,8 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     if (!(flags & GETT_FLAG_SCALAR)) {
         if (row_vec_ok(Ix, sX)) xmode = kGatherRowVec;
         else if (k_vec_ok(Ix, sX)) xmode = kGatherKVec;
-        if (row_vec_ok(Iy, sY)) ymode = kGatherRowVec;
+        if (ysplit) ymode = ysplit;
+        else if (row_vec_ok(Iy, sY)) ymode = kGatherRowVec;
         else if (k_vec_ok(Iy, sY)) ymode = kGatherKVec;
     }
     bool cvec = !(flags & GETT_FLAG_SCALAR) && Iy[0].strC == 1 && Iy[0].extent % VW == 0;
@@ -544,6 +669,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     d.cvec = cvec ? 1 : 0;
     d.xscalar_kfast = sX(Ik[0]) < sX(Ix[0]) ? 1 : 0;
     d.yscalar_kfast = sY(Ik[0]) < sY(Iy[0]) ? 1 : 0;
+    d.yes = yes;
 
     plan.dtype = dtype;
     plan.flags = flags;
@@ -600,7 +726,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     o << ",\"kbox\":{\"kj\":" << kj << ",\"tj\":" << tj << ",\"elements\":" << kbox << ",\"blocks\":" << nblk
       << ",\"steps\":" << nsteps << "}";
     o << ",\"gather_x\":\"" << mode_name(xmode) << "\",\"gather_y\":\"" << mode_name(ymode)
-      << "\",\"c_vector\":" << (cvec ? "true" : "false");
+      << "\",\"c_vector\":" << (cvec ? "true" : "false") << ",\"y_vector_stride\":" << yes;
     o << ",\"grid\":{\"tiles_x\":" << tilesX << ",\"tiles_y\":" << tilesY << ",\"workgroups\":"
       << tilesX * tilesY << ",\"threads\":" << ts.wm * ts.wn * 64 << "}";
     o << ",\"empty_c\":" << (an.emptyC ? "true" : "false") << ",\"empty_sum\":"

@@ -22,7 +22,14 @@ constexpr int kMaxDims = 12;   // per index set (== GETT_MAX_RANK)
 enum GatherMode : int {
     kGatherRowVec = 0,   // 16-byte vectors along the tile's free index (stride-one there)
     kGatherKVec = 1,     // 16-byte vectors along the contracted index (stride-one there)
-    kGatherScalar = 2    // one element per access
+    kGatherScalar = 2,   // one element per access
+    // Column operand only: 16-byte vectors along the operand's stride-one
+    // index when that index is the second of the tile's free indices (after
+    // a block of C's stride-one index) or the second of the K box (after a
+    // block of the row operand's stride-one index); consecutive elements of a
+    // vector are KDesc::yes tile rows or K positions apart.
+    kGatherRowVecStrided = 3,
+    kGatherKVecStrided = 4
 };
 
 struct KDesc {
@@ -55,6 +62,8 @@ struct KDesc {
     int32_t cvec;                  // 1: C accesses may use 16-byte vectors along y
     int32_t xscalar_kfast;         // scalar gather of X: 1 = contracted index fastest
     int32_t yscalar_kfast;         // scalar gather of Y: 1 = contracted index fastest
+    int32_t yes;                   // strided vector gathers of Y: distance between the
+                                   // elements of one vector (extent of the first index)
 };
 
 }  // namespace gett

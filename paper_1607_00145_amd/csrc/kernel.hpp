@@ -120,10 +120,23 @@ __device__ __forceinline__ int box_origin(const KDesc &d, uint32_t s, int &ox, i
 // Per-thread description of the part of one operand tile it gathers.  Item
 // `it` of thread `tid` is element (or 16-byte vector) tid + it * NTH of the
 // tile in the mode's order; items past the tile's end are idle.
+//
+// The strided modes gather a tile whose rows (or K positions) are ordered
+// (u, v, ...) with u of extent `es` fastest and the operand's stride-one index
+// v second: the VW elements of one vector are es rows (K positions) apart in
+// the packed layout and are written to LDS one by one.  Within a line of
+// ROWS rows (KT positions) an item is (q, c): vector q along v (fastest, so
+// that neighbouring lanes read neighbouring 16-byte pieces) at u = c; the
+// analyser guarantees es * VW divides ROWS (KT) and that v's extent and, in
+// the K box, its block length are multiples of VW, so a vector is valid or
+// outside the tensor as a whole.
 template <typename T, int ROWS, int KT, int MODE, int NTH, int STAGES = 1>
 struct Gather {
     static constexpr int VW = Traits<T>::VW;
     static constexpr int PITCH = ROWS + VW;   // LDS row pitch (elements) of the [k][row] layout
+    static constexpr bool kRowV = MODE == kGatherRowVec || MODE == kGatherRowVecStrided;
+    static constexpr bool kKV = MODE == kGatherKVec || MODE == kGatherKVecStrided;
+    static constexpr bool kStrided = MODE == kGatherRowVecStrided || MODE == kGatherKVecStrided;
     static constexpr int W = (MODE == kGatherScalar) ? 1 : VW;
     static_assert(MODE == kGatherScalar || (ROWS % VW == 0 && KT % VW == 0), "vector gathers");
     static constexpr int ITEMS = ROWS * KT / W;
@@ -132,23 +145,26 @@ struct Gather {
     // Consecutive items of one thread sit a fixed LDS distance apart when the
     // workgroup covers whole rows (or whole K lines) per item round.
     static constexpr bool kConst =
-        NI <= 1 || (kFull && (MODE == kGatherRowVec ? NTH % (ROWS / VW) == 0
-                              : MODE == kGatherKVec ? NTH % (KT / VW) == 0
-                                                    : NTH % KT == 0 && NTH % ROWS == 0));
+        NI <= 1 || (kFull && (kRowV ? NTH % (ROWS / VW) == 0
+                              : kKV ? NTH % (KT / VW) == 0
+                                    : NTH % KT == 0 && NTH % ROWS == 0));
     typedef typename Traits<T>::vec vec;
 
     int goff[NI];                 // element offset in the operand (without the box origin)
     int kc[NI];                   // position along index kj inside the box; kInvalidK: never valid
     int lds[kConst ? 1 : NI];     // LDS slot of each item (of item 0 when kConst); -1: idle
     int lstep;                    // LDS distance between consecutive items (kConst)
+    int estep;                    // LDS distance between the elements of a strided vector
     T val[STAGES][NI][W];         // staged values, one set per stage in flight
 
     // rowoff: LDS table of operand offsets per tile row (-1 = outside the tensor)
     // koff/kco: LDS tables of offsets / kj-positions per box element
+    // es: extent of the first row (K) index in the strided modes
     __device__ __forceinline__ void setup(int tid, const int *rowoff, const int *koff,
-                                          const int *kco, int kfast)
+                                          const int *kco, int kfast, int es = 1)
     {
         lstep = 0;
+        estep = MODE == kGatherKVecStrided ? es * PITCH : es;
 #pragma unroll
         for (int it = 0; it < NI; ++it) {
             const int i = tid + it * NTH;
@@ -158,6 +174,14 @@ struct Gather {
                 kk = i / (ROWS / VW);
             } else if (MODE == kGatherKVec) {
                 kk = (i % (KT / VW)) * VW;
+                r = i / (KT / VW);
+            } else if (MODE == kGatherRowVecStrided) {
+                const int j = i % (ROWS / VW), nq = ROWS / (VW * es);
+                r = (j / nq) + (j % nq) * es * VW;
+                kk = i / (ROWS / VW);
+            } else if (MODE == kGatherKVecStrided) {
+                const int j = i % (KT / VW), nq = KT / (VW * es);
+                kk = (j / nq) + (j % nq) * es * VW;
                 r = i / (KT / VW);
             } else if (kfast) {
                 kk = i % KT;
@@ -216,6 +240,9 @@ struct Gather {
             } else if (MODE == kGatherKVec) {
 #pragma unroll
                 for (int e = 0; e < W; ++e) dst[e * PITCH] = val[B][it][e];
+            } else if (kStrided) {
+#pragma unroll
+                for (int e = 0; e < W; ++e) dst[e * estep] = val[B][it][e];
             } else {
                 *dst = val[B][it][0];
             }
@@ -488,7 +515,7 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     GX gx;
     GY gy;
     gx.setup(tid, rowX, kX, kco, d.xscalar_kfast);
-    gy.setup(tid, rowY, kY, kco, d.yscalar_kfast);
+    gy.setup(tid, rowY, kY, kco, d.yscalar_kfast, d.yes);
     WT w;
     w.init(tid);
     w.zero();
@@ -601,7 +628,7 @@ gett_stream_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
     w.init(tid);
     if (withK) {
         gx.setup(tid, rowX[0], kX, kco, d.xscalar_kfast);
-        gy.setup(tid, rowY[0], kY, kco, d.yscalar_kfast);
+        gy.setup(tid, rowY[0], kY, kco, d.yscalar_kfast, d.yes);
         gx.load(Xb, lim);
         gy.load(Yb, lim);
         gx.store(xs);
@@ -620,7 +647,7 @@ gett_stream_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
         __syncthreads();
         if (more && withK) {
             gx.setup(tid, rowX[cur ^ 1], kX, kco, d.xscalar_kfast);
-            gy.setup(tid, rowY[cur ^ 1], kY, kco, d.yscalar_kfast);
+            gy.setup(tid, rowY[cur ^ 1], kY, kco, d.yscalar_kfast, d.yes);
             gx.load(Xb, lim);
             gy.load(Yb, lim);
         }

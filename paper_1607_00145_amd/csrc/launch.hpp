@@ -68,9 +68,9 @@ LaunchFn pick_modes(int xm, int ym, int kind)
         if (kStream) return &launch_one<T, TI, a, b, kStream ? 1 : 0>;                       \
         return nullptr;                                                                       \
     }
-    GETT_CASE(0, 0) GETT_CASE(0, 1) GETT_CASE(0, 2)
-    GETT_CASE(1, 0) GETT_CASE(1, 1) GETT_CASE(1, 2)
-    GETT_CASE(2, 0) GETT_CASE(2, 1) GETT_CASE(2, 2)
+    GETT_CASE(0, 0) GETT_CASE(0, 1) GETT_CASE(0, 2) GETT_CASE(0, 3) GETT_CASE(0, 4)
+    GETT_CASE(1, 0) GETT_CASE(1, 1) GETT_CASE(1, 2) GETT_CASE(1, 3) GETT_CASE(1, 4)
+    GETT_CASE(2, 0) GETT_CASE(2, 1) GETT_CASE(2, 2) GETT_CASE(2, 3) GETT_CASE(2, 4)
 #undef GETT_CASE
     return nullptr;
 }

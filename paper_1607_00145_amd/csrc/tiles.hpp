@@ -52,6 +52,6 @@ constexpr TileShape kTilesF64[] = {
 };
 constexpr int kNumTilesF32 = sizeof(kTilesF32) / sizeof(kTilesF32[0]);
 constexpr int kNumTilesF64 = sizeof(kTilesF64) / sizeof(kTilesF64[0]);
-constexpr int kNumGatherModes = 3;
+constexpr int kNumGatherModes = 5;
 
 }  // namespace gett
