@@ -34,6 +34,14 @@ KSPLIT = {
                        {"a": 13, "b": 6, "c": 10, "d": 5, "e": 16, "f": 12}),
 }
 CASES = {**COLUMN, **KSPLIT}
+# The Y gather the analyser's run-length price model picks at these extents: a
+# column split where C keeps long enough write runs, the whole-index order
+# where Y is small next to C (abcdef-dega-gfbc: |A| = |C| / 7.5, so shorter C
+# runs would cost more than Y's longer read runs save).
+EXPECT = {**{n: "row-vector-strided" for n in COLUMN}, **{n: "k-vector-strided" for n in KSPLIT}}
+EXPECT["abcdef-dega-gfbc"] = "scalar"
+# a block length forced through the tuning hook, for a pattern the model keeps whole
+FORCED = {"abcdef-dega-gfbc": 8}
 
 
 def shapes_of(modes, ext):
@@ -57,10 +65,23 @@ def describe(modes, ext, dtype, flags=0):
 def test_default_plan(gpu, name, dtype):
     modes, ext = CASES[name]
     d = describe(modes, ext, dtype)
-    want = "row-vector-strided" if name in COLUMN else "k-vector-strided"
-    assert d["gather_y"] == want
-    rng = np.random.default_rng(hash(name) % 1000)
+    assert d["gather_y"] == EXPECT[name]
+    rng = np.random.default_rng(sum(map(ord, name)))
     check_case(gpu, rng, modes, shapes_of(modes, ext), dtype, 1.5, -0.5)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("name", list(FORCED))
+def test_forced_split(gpu, monkeypatch, name, dtype):
+    """The split the model declines, forced: the strided gathers still agree
+    with the oracle, with and without beta."""
+    monkeypatch.setenv("GETT_SPLIT_F", str(FORCED[name]))
+    modes, ext = CASES[name]
+    assert describe(modes, ext, dtype)["gather_y"] == "row-vector-strided"
+    rng = np.random.default_rng(5)
+    check_case(gpu, rng, modes, shapes_of(modes, ext), dtype, 1.5, -0.5)
+    got, ref = check_case(gpu, rng, modes, shapes_of(modes, ext), dtype, 1.0, 0.0, dist="int")
+    np.testing.assert_array_equal(got.astype(np.float64), ref.out64)
 
 
 @pytest.mark.parametrize("dtype,tile", [(dt, t) for dt in DTYPES for t in range(TILES[dt])])

@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 import paper_1607_00145_amd as g
-from test_gpu_split import CASES, COLUMN, KSPLIT, TILES, describe, shapes_of
+from test_gpu_split import CASES, COLUMN, EXPECT, FORCED, KSPLIT, TILES, describe, shapes_of
 
 VW = {np.float32: 4, np.float64: 2}
 
@@ -39,7 +39,7 @@ def check_invariants(d, dtype, name):
 def test_default_plans_split(name, dtype):
     modes, ext = CASES[name]
     d = describe(modes, ext, dtype)
-    assert d["gather_y"] == ("row-vector-strided" if name in COLUMN else "k-vector-strided")
+    assert d["gather_y"] == EXPECT[name]
     check_invariants(d, dtype, name)
     if name in KSPLIT:
         # the row operand reads vectors along the block of its stride-one index
@@ -48,6 +48,17 @@ def test_default_plans_split(name, dtype):
         d = describe(modes, ext, dtype, flags)
         assert d["y_vector_stride"] == 1
         assert not any("<" in n for n in d["y_order"] + d["k_order"])
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float64])
+@pytest.mark.parametrize("name", list(FORCED))
+def test_forced_split_plan(monkeypatch, name, dtype):
+    monkeypatch.setenv("GETT_SPLIT_F", str(FORCED[name]))
+    modes, ext = CASES[name]
+    d = describe(modes, ext, dtype)
+    assert d["gather_y"] == "row-vector-strided"
+    assert d["y_vector_stride"] == FORCED[name]
+    check_invariants(d, dtype, name)
 
 
 @pytest.mark.parametrize("dtype", [np.float32, np.float64])
