@@ -353,38 +353,93 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         int kj;
         int64_t tj, kbox, nblk, nsteps;
     };
-    auto box_for = [&](int kt) {
+    // K box of depth kt over the contracted set K (in walk order); kvi is the
+    // index that contracted vector gathers run along.
+    auto box_on = [&](const std::vector<Index> &K, int kvi, int kt) {
+        const int nK = (int)K.size();
         Box b;
         b.kj = 0;
         int64_t prefix = 1;
-        while (b.kj < nk - 1 && prefix * Ik[b.kj].extent <= kt) {
-            prefix *= Ik[b.kj].extent;
+        while (b.kj < nK - 1 && prefix * K[b.kj].extent <= kt) {
+            prefix *= K[b.kj].extent;
             ++b.kj;
         }
-        int64_t tj = std::max<int64_t>(1, std::min<int64_t>(Ik[b.kj].extent, kt / prefix));
+        int64_t tj = std::max<int64_t>(1, std::min<int64_t>(K[b.kj].extent, kt / prefix));
         // Prefer a block length that divides the index (no ragged last block)
         // unless that would lose more than half of the box.
         {
             int64_t best = tj;
             for (int64_t t = tj; t >= 1; --t)
-                if (Ik[b.kj].extent % t == 0) { best = t; break; }
+                if (K[b.kj].extent % t == 0) { best = t; break; }
             if (best * 2 > tj) tj = best;
         }
         // The block of the index that vectors run along holds whole vectors.
-        if (b.kj == kvecIdx && (wantKvec || kvecIdx > 0) && tj % VW) {
+        if (b.kj == kvi && (wantKvec || kvi > 0) && tj % VW) {
             const int64_t t2 = (tj / VW) * VW;
             if (t2 >= VW) {
                 tj = t2;
-                while (Ik[b.kj].extent % tj && tj > VW) tj -= VW;   // keep it dividing when possible
+                while (K[b.kj].extent % tj && tj > VW) tj -= VW;   // keep it dividing when possible
             }
         }
         b.tj = tj;
         b.kbox = prefix * tj;
-        b.nblk = (Ik[b.kj].extent + tj - 1) / tj;
+        b.nblk = (K[b.kj].extent + tj - 1) / tj;
         b.nsteps = b.nblk;
-        for (int i = b.kj + 1; i < nk; ++i) b.nsteps *= Ik[i].extent;
+        for (int i = b.kj + 1; i < nK; ++i) b.nsteps *= K[i].extent;
         if (an.emptySum) b.nsteps = 0;
         return b;
+    };
+    auto box_for = [&](int kt) { return box_on(Ik, kvecIdx, kt); };
+
+    // ---- index splitting helpers (used by the model and by the plan; see
+    //      the splitting step below) ----
+    auto split_front = [](std::vector<Index> &set, size_t u, size_t v, int64_t f) {
+        Index in = set[u], out = set[u];
+        in.extent = f;
+        in.name = set[u].name + "<" + std::to_string(f);
+        out.extent = set[u].extent / f;
+        out.name = set[u].name + ">" + std::to_string(f);
+        out.strA *= f;
+        out.strB *= f;
+        out.strC *= f;
+        std::vector<Index> next;
+        next.push_back(in);
+        next.push_back(set[v]);
+        if (out.extent > 1) next.push_back(out);
+        for (size_t i = 0; i < set.size(); ++i)
+            if (i != u && i != v) next.push_back(set[i]);
+        set.swap(next);
+    };
+    auto pow2_part = [](int64_t e) { return e & -e; };
+    auto unit_in = [](const std::vector<Index> &set, auto strOf) -> int {
+        for (size_t i = 0; i < set.size(); ++i)
+            if (strOf(set[i]) == 1 && set[i].extent > 1) return (int)i;
+        return -1;
+    };
+    auto aligned = [&](const std::vector<Index> &set, auto strOf, int skip) {
+        for (size_t i = 0; i < set.size(); ++i)
+            if ((int)i != skip && strOf(set[i]) % VW) return false;
+        return true;
+    };
+    const bool maySplit = !(flags & (GETT_FLAG_SCALAR | GETT_FLAG_NO_SPLIT)) && !an.emptyC &&
+                          !an.emptySum;
+    const int splitXK = unit_in(Ik, sX), splitYK = unit_in(Ik, sY);
+    // K-box split for a box of depth kt: X's stride-one contracted index u
+    // blocked by f in front of Y's stride-one contracted index v.  X runs of f
+    // (a multiple of VW), at least two vectors of v per box line when the
+    // box allows.  Returns f (0: no split) and the split set in `trial`.
+    auto k_split = [&](int kt, std::vector<Index> &trial) -> int64_t {
+        if (!maySplit || splitXK < 0 || splitYK < 0 || splitXK == splitYK ||
+            Ik[splitYK].extent % VW || (int)Ik.size() >= kMaxDims)
+            return 0;
+        int64_t cap = 1;
+        while (cap * 2 * VW <= kt) cap *= 2;
+        int64_t f = std::min<int64_t>(pow2_part(Ik[splitXK].extent), cap);
+        while (f > VW && f * VW * 2 > kt) f /= 2;
+        trial = Ik;
+        split_front(trial, (size_t)splitXK, (size_t)splitYK, f);
+        if (f >= VW && kt % (f * VW) == 0 && aligned(trial, sY, 1) && aligned(Iy, sY, -1)) return f;
+        return 0;
     };
 
     // ---- tile shape: the paper ranks candidates with a performance model
@@ -400,27 +455,45 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     const double bytesX = itemB * (double)sizeX * (double)an.sizeK;
     const double bytesY = itemB * (double)sizeY * (double)an.sizeK;
     const double bytesC = itemB * (double)sizeX * (double)sizeY;
+    // When the row and column operands are stride-one along different
+    // contracted indices, the K box is split between them (below) and both
+    // are gathered in short runs whose cache lines are reused only many
+    // boxes later; without a second LDS buffer the gather latency of every
+    // box is exposed (measured on MI355X: 1.4-1.8x slower than the
+    // double-buffered tiles of the same depth).
+    // Each tile's K box is priced on the contracted order that tile gets.
     // Every (tile, kernel kind) pair is a candidate; the model ranks them.
     std::vector<Candidate> ranked;
     for (int t = 0; t < num_tiles(dtype); ++t) {
         const TileShape &c = tile_shape(dtype, t);
-        const Box b = box_for(c.kt);
+        std::vector<Index> ksplit;
+        const bool kSplitAhead = k_split(c.kt, ksplit) > 0;
+        const Box b = kSplitAhead ? box_on(ksplit, 1, c.kt) : box_for(c.kt);
         const double tx = (double)((sizeX + c.mt - 1) / c.mt);
         const double ty = (double)((sizeY + c.nt - 1) / c.nt);
-        const double waves = tx * ty * c.wm * c.wn;
-        const double perSimd = std::ceil(waves / 1024.0);
+        // Busiest SIMD: a workgroup of four or more wavefronts is spread over
+        // the four SIMDs of one CU (ceil(w / 4) on the busiest), so a CU's
+        // load is counted in workgroups; smaller workgroups share SIMDs.
+        const int wpt = c.wm * c.wn;
+        const double waves = tx * ty * wpt;
+        const double perSimd = wpt >= 4 ? std::ceil(tx * ty / 256.0) * std::ceil(wpt / 4.0)
+                                        : std::ceil(waves / 1024.0);
         const double kpad = (double)std::max<int64_t>(b.nsteps, 1) * c.kt;
         const double waveFlops = (double)(c.mt / c.wm) * (c.nt / c.wn) * kpad * 2.0;
-        const double tMfma = perSimd * waveFlops / (peakSimd * c.eff);
+        const double tMfma = perSimd * waveFlops / (peakSimd * c.eff) *
+                             (kSplitAhead && c.nbuf == 1 && b.nsteps > 1 ? 1.4 : 1.0);
         // The persistent streaming kernel needs the contracted set in one box.
         const bool canStream = c.stream && b.nsteps <= 1;
         // A stream carried by fewer workgroups than CUs gets that share of the
         // bandwidth (each CU's memory pipeline has its own limit).
-        const double cuShare = std::min(1.0, tx * ty / 256.0);
+        const double cuShare = std::min(1.0, std::max(tx * ty, 1.0) / 256.0);
         for (int k = 0; k < (canStream ? 2 : 1); ++k) {
             const double bwFrac = (k ? c.sbw : c.bw) * cuShare;
-            const double tMem =
-                (bytesC + 0.05 * (bytesX * ty + bytesY * tx)) / (8.0e12 * bwFrac);
+            // compulsory bytes (each operand read once, C written once) plus
+            // the operand panels re-read by other tiles, mostly from L2
+            const double tMem = (bytesC + bytesX + bytesY +
+                                 0.05 * (bytesX * (ty - 1) + bytesY * (tx - 1))) /
+                                (8.0e12 * bwFrac);
             Candidate cd;
             cd.tile = t;
             cd.kind = k;
@@ -481,37 +554,9 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     //      elements f rows (K positions) apart. ----
     int ysplit = 0;   // 0, kGatherRowVecStrided or kGatherKVecStrided
     int yes = 1;
-    auto split_front = [](std::vector<Index> &set, size_t u, size_t v, int64_t f) {
-        Index in = set[u], out = set[u];
-        in.extent = f;
-        in.name = set[u].name + "<" + std::to_string(f);
-        out.extent = set[u].extent / f;
-        out.name = set[u].name + ">" + std::to_string(f);
-        out.strA *= f;
-        out.strB *= f;
-        out.strC *= f;
-        std::vector<Index> next;
-        next.push_back(in);
-        next.push_back(set[v]);
-        if (out.extent > 1) next.push_back(out);
-        for (size_t i = 0; i < set.size(); ++i)
-            if (i != u && i != v) next.push_back(set[i]);
-        set.swap(next);
-    };
-    auto pow2_part = [](int64_t e) { return e & -e; };
-    if (!(flags & (GETT_FLAG_SCALAR | GETT_FLAG_NO_SPLIT)) && !an.emptyC && !an.emptySum) {
+    if (maySplit) {
         // which set holds each operand's stride-one index
-        auto unit_in = [](const std::vector<Index> &set, auto strOf) -> int {
-            for (size_t i = 0; i < set.size(); ++i)
-                if (strOf(set[i]) == 1 && set[i].extent > 1) return (int)i;
-            return -1;
-        };
-        const int yRow = unit_in(Iy, sY), yK = unit_in(Ik, sY), xK = unit_in(Ik, sX);
-        auto aligned = [&](const std::vector<Index> &set, auto strOf, int skip) {
-            for (size_t i = 0; i < set.size(); ++i)
-                if ((int)i != skip && strOf(set[i]) % VW) return false;
-            return true;
-        };
+        const int yRow = unit_in(Iy, sY);
         if (yRow > 0 && Iy[0].strC == 1 && Iy[yRow].extent % VW == 0 &&
             (int)Iy.size() < kMaxDims) {
             // Columns.  A tile then writes C in runs of f elements and reads Y
@@ -554,17 +599,10 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
                     yes = (int)f;
                 }
             }
-        } else if (xK >= 0 && yK >= 0 && xK != yK && Ik[yK].extent % VW == 0 &&
-                   (int)Ik.size() < kMaxDims) {
-            // K box: X runs of f (a multiple of VW), at least two vectors of v
-            // per box line when the box allows
-            int64_t cap = 1;
-            while (cap * 2 * VW <= ts.kt) cap *= 2;
-            int64_t f = std::min<int64_t>(pow2_part(Ik[xK].extent), cap);
-            while (f > VW && f * VW * 2 > ts.kt) f /= 2;
-            std::vector<Index> trial = Ik;
-            split_front(trial, (size_t)xK, (size_t)yK, f);
-            if (f >= VW && ts.kt % (f * VW) == 0 && aligned(trial, sY, 1) && aligned(Iy, sY, -1)) {
+        } else {
+            std::vector<Index> trial;
+            const int64_t f = k_split(ts.kt, trial);
+            if (f > 0) {
                 Ik.swap(trial);
                 nk = (int)Ik.size();
                 kvecIdx = 1;

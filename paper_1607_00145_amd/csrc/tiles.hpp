@@ -35,20 +35,20 @@ constexpr TileShape kTilesF32[] = {
     {32, 64, 32, 2, 2, 1, 2, 2, 2, 2, 0, 0.65f, 0.35f, 0.0f},
 };
 constexpr TileShape kTilesF64[] = {
-    {128, 128, 16, 2, 2, 2, 2, 1, 2, 2, 0, 0.56f, 0.34f, 0.0f},
-    {64, 64, 16, 1, 1, 2, 2, 1, 2, 2, 0, 0.40f, 0.32f, 0.0f},
-    {144, 144, 16, 3, 3, 1, 1, 1, 2, 2, 0, 0.547f, 0.36f, 0.0f},
-    {128, 64, 8, 2, 2, 2, 2, 3, 1, 2, 2, 0.41f, 0.53f, 0.53f},
-    {128, 64, 24, 2, 2, 2, 2, 2, 1, 2, 2, 0.50f, 0.49f, 0.51f},
-    {64, 64, 16, 2, 2, 2, 2, 2, 2, 2, 0, 0.65f, 0.34f, 0.0f},
-    {64, 128, 16, 2, 2, 2, 2, 2, 2, 2, 0, 0.688f, 0.34f, 0.0f},
-    {128, 64, 16, 2, 2, 2, 2, 2, 2, 2, 0, 0.68f, 0.34f, 0.0f},
-    {96, 128, 16, 2, 2, 1, 2, 2, 2, 2, 0, 0.735f, 0.34f, 0.0f},
-    {128, 64, 24, 2, 2, 2, 2, 3, 1, 1, 0, 0.50f, 0.615f, 0.0f},
-    {64, 128, 24, 1, 4, 2, 2, 3, 1, 1, 0, 0.50f, 0.59f, 0.0f},
-    {64, 128, 24, 2, 2, 2, 2, 3, 1, 1, 0, 0.50f, 0.668f, 0.0f},
-    {64, 32, 16, 2, 2, 2, 1, 2, 2, 2, 0, 0.60f, 0.485f, 0.0f},
-    {32, 64, 16, 2, 2, 1, 2, 2, 2, 2, 0, 0.60f, 0.49f, 0.0f},
+    {128, 128, 16, 2, 2, 2, 2, 1, 2, 2, 0, 0.65f, 0.34f, 0.0f},
+    {64, 64, 16, 1, 1, 2, 2, 1, 2, 2, 0, 0.59f, 0.32f, 0.0f},
+    {144, 144, 16, 3, 3, 1, 1, 1, 2, 2, 0, 0.79f, 0.36f, 0.0f},
+    {128, 64, 8, 2, 2, 2, 2, 3, 1, 2, 2, 0.70f, 0.53f, 0.53f},
+    {128, 64, 24, 2, 2, 2, 2, 2, 1, 2, 2, 0.69f, 0.49f, 0.51f},
+    {64, 64, 16, 2, 2, 2, 2, 2, 2, 2, 0, 0.75f, 0.34f, 0.0f},
+    {64, 128, 16, 2, 2, 2, 2, 2, 2, 2, 0, 0.785f, 0.34f, 0.0f},
+    {128, 64, 16, 2, 2, 2, 2, 2, 2, 2, 0, 0.785f, 0.34f, 0.0f},
+    {96, 128, 16, 2, 2, 1, 2, 2, 2, 2, 0, 0.79f, 0.34f, 0.0f},
+    {128, 64, 24, 2, 2, 2, 2, 3, 1, 1, 0, 0.785f, 0.615f, 0.0f},
+    {64, 128, 24, 1, 4, 2, 2, 3, 1, 1, 0, 0.775f, 0.59f, 0.0f},
+    {64, 128, 24, 2, 2, 2, 2, 3, 1, 1, 0, 0.785f, 0.668f, 0.0f},
+    {64, 32, 16, 2, 2, 2, 1, 2, 2, 2, 0, 0.70f, 0.485f, 0.0f},
+    {32, 64, 16, 2, 2, 1, 2, 2, 2, 2, 0, 0.71f, 0.49f, 0.0f},
 };
 constexpr int kNumTilesF32 = sizeof(kTilesF32) / sizeof(kTilesF32[0]);
 constexpr int kNumTilesF64 = sizeof(kTilesF64) / sizeof(kTilesF64[0]);
