@@ -288,6 +288,7 @@ def report_workload(w, dev, stream, runs, flush):
                                            "gather_x", "gather_y", "c_vector")}
     rec["plan"]["tile"] = [p.plan["tile"]["mt"], p.plan["tile"]["nt"], p.plan["tile"]["kt"]]
     rec["plan"]["workgroups"] = p.plan["grid"]["workgroups"]
+    rec["plan"]["kslices"] = p.plan["kslices"]
     t = TtgtProblem(p)
     for _ in range(3):
         t.launch(stream)
@@ -403,7 +404,8 @@ def sweep_run(sweep, dev, stream, runs, flush, max_candidates):
         k = w.extents.get("k")
         flops = wl.flop_count(w)
         p = Problem(w, dev, on_device=True)
-        tile = lambda: [p.plan["tile"][x] for x in ("mt", "nt", "kt")] + [p.plan["kernel"]]
+        tile = lambda: [p.plan["tile"][x] for x in ("mt", "nt", "kt")] + [
+            p.plan["kernel"] if p.plan["kslices"] == 1 else f"kslices{p.plan['kslices']}"]
         model_tile = tile()
         for _ in range(3):
             p.launch(stream)

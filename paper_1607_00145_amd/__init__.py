@@ -26,6 +26,7 @@ GETT_FLAG_NONE = 0
 GETT_FLAG_NO_SWAP = 1
 GETT_FLAG_SCALAR = 2
 GETT_FLAG_NO_SPLIT = 4
+GETT_FLAG_DETERMINISTIC = 8
 GETT_MAX_RANK = 12
 GETT_SUCCESS = 0
 GETT_ERROR_INVALID_VALUE = 1

@@ -187,6 +187,12 @@ void json_set(std::ostringstream &o, const char *key, const std::vector<Index> &
     o << "]";
 }
 
+}  // namespace
+
+const char *kind_name(int k) { return k == 1 ? "stream" : k == 2 ? "kslices" : "macro"; }
+
+namespace {
+
 const char *mode_name(int m)
 {
     return m == kGatherRowVec         ? "row-vector"
@@ -487,6 +493,23 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         // A stream carried by fewer workgroups than CUs gets that share of the
         // bandwidth (each CU's memory pipeline has its own limit).
         const double cuShare = std::min(1.0, std::max(tx * ty, 1.0) / 256.0);
+        // Latency chain: a wavefront walks its K boxes one after another and
+        // waits about 1.2 us for each box's gathers when nothing else covers
+        // them (measured on MI355X with one wavefront per SIMD); the busiest
+        // SIMD walks perSimd wavefronts' boxes, up to four of them resident
+        // and waiting together.
+        auto chain = [&](double wgs, double boxes) {
+            const double ps = std::max(1.0, wpt >= 4 ? std::ceil(wgs / 256.0) * std::ceil(wpt / 4.0)
+                                                     : std::ceil(wgs * wpt / 1024.0));
+            return ps * boxes * 1.2e-6 / std::min(ps, 4.0);
+        };
+        const double tChain = chain(tx * ty, (double)std::max<int64_t>(b.nsteps, 1));
+        // the larger of throughput and latency bound, with near-ties broken
+        // by the other (a 4-norm)
+        auto bound = [](double tput, double lat) {
+            const double a = tput * tput, b = lat * lat;
+            return std::sqrt(std::sqrt(a * a + b * b));
+        };
         for (int k = 0; k < (canStream ? 2 : 1); ++k) {
             const double bwFrac = (k ? c.sbw : c.bw) * cuShare;
             // compulsory bytes (each operand read once, C written once) plus
@@ -499,8 +522,48 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
             cd.kind = k;
             cd.tMfma = tMfma;
             cd.tMem = tMem;
-            cd.cost = std::max(tMfma, tMem);
+            cd.cost = bound(std::max(tMfma, tMem), tChain);
             ranked.push_back(cd);
+        }
+        // K slices: when a contracted set of many boxes meets too few tiles to
+        // give every SIMD two wavefronts, P workgroups share each tile's
+        // boxes and add their partial tiles into C with atomics, after one
+        // pass that sets C to beta * C.  Priced like the macro-kernel on
+        // tiles * P workgroups with ceil(boxes / P) boxes each plus two
+        // boxes' worth of set-up and epilogue per workgroup, plus P atomic
+        // read-modify-writes of C, which add to the time (measured on
+        // MI355X: float atomics on distinct addresses sustain about
+        // 1.7 TB/s counting the read and the write), the scaling pass and
+        // its launch.  Each slice keeps at least eight boxes.
+        if (!(flags & GETT_FLAG_DETERMINISTIC) && !an.emptyC && waves < 2048.0 &&
+            b.nsteps >= 16) {
+            Candidate best;
+            best.tile = -1;
+            for (int P = 2; P <= 256 && b.nsteps / P >= 8; P *= 2) {
+                const double wgs = tx * ty * P;
+                const double perSimdP = wpt >= 4 ? std::ceil(wgs / 256.0) * std::ceil(wpt / 4.0)
+                                                 : std::ceil(wgs * wpt / 1024.0);
+                const double kpadP = (std::ceil((double)b.nsteps / P) + 2.0) * c.kt;
+                const double tM = perSimdP * (double)(c.mt / c.wm) * (c.nt / c.wn) * kpadP * 2.0 /
+                                  (peakSimd * c.eff) *
+                                  (kSplitAhead && c.nbuf == 1 ? 1.4 : 1.0);
+                const double shareP = std::min(1.0, wgs / 256.0);
+                const double tMemP = (bytesC + bytesX + bytesY +
+                                      0.05 * (bytesX * (ty - 1) + bytesY * (tx - 1))) /
+                                     (8.0e12 * c.bw * shareP);
+                const double tAtomic = bytesC * 2.0 * P / 1.7e12;
+                const double tChainP = chain(wgs, std::ceil((double)b.nsteps / P));
+                const double cost = bound(std::max(tM, tMemP), tChainP) + tAtomic + 3.0e-6;
+                if (best.tile < 0 || cost < best.cost) {
+                    best.tile = t;
+                    best.kind = 2;
+                    best.slices = P;
+                    best.tMfma = tM;
+                    best.tMem = tMemP;
+                    best.cost = cost;
+                }
+            }
+            if (best.tile >= 0) ranked.push_back(best);
         }
     }
     std::stable_sort(ranked.begin(), ranked.end(),
@@ -531,8 +594,20 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
             how = "forced";
         }
     }
+    // tuning hook: this many K slices on the chosen tile
+    // (1: none), unless the plan must be deterministic
+    if (const char *fs = getenv("GETT_FORCE_KSLICES")) {
+        const int P = atoi(fs);
+        if (P == 1 && pick.kind == 2) {
+            if (const Candidate *c = find(pick.tile, 0)) pick = *c;
+        } else if (P > 1 && pick.kind != 1 && !an.emptyC && !(flags & GETT_FLAG_DETERMINISTIC)) {
+            pick.kind = 2;
+            pick.slices = P;
+        }
+    }
     const int tile = pick.tile;
     const int kind = pick.kind;
+    const int kslices = kind == 2 ? pick.slices : 1;
     const double bestMfma = pick.tMfma, bestMem = pick.tMem;
     const TileShape &ts = tile_shape(dtype, tile);
 
@@ -708,6 +783,9 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     d.xscalar_kfast = sX(Ik[0]) < sX(Ix[0]) ? 1 : 0;
     d.yscalar_kfast = sY(Ik[0]) < sY(Iy[0]) ? 1 : 0;
     d.yes = yes;
+    d.kslices = kslices;
+    if (!an.emptyC && tilesX * tilesY * kslices * ts.wm * ts.wn * 64 >= (int64_t)UINT32_MAX)
+        return GETT_ERROR_NOT_SUPPORTED;
 
     plan.dtype = dtype;
     plan.flags = flags;
@@ -755,12 +833,15 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
       << ",\"waves\":[" << ts.wm << "," << ts.wn << "],\"reads\":[" << ts.rx << "," << ts.ry
       << "],\"chosen_by\":\"" << how << "\",\"model_us\":" << pick.cost * 1e6 << "}";
     o << ",\"candidates\":[";
-    for (size_t i = 0; i < ranked.size(); ++i)
+    for (size_t i = 0; i < ranked.size(); ++i) {
         o << (i ? "," : "") << "{\"tile\":" << ranked[i].tile << ",\"kind\":\""
-          << (ranked[i].kind ? "stream" : "macro") << "\",\"model_us\":" << ranked[i].cost * 1e6 << "}";
+          << kind_name(ranked[i].kind) << "\"";
+        if (ranked[i].kind == 2) o << ",\"kslices\":" << ranked[i].slices;
+        o << ",\"model_us\":" << ranked[i].cost * 1e6 << "}";
+    }
     o << "]";
     o << ",\"streaming\":" << (streaming ? "true" : "false");
-    o << ",\"kernel\":\"" << (kind ? "stream" : "macro") << "\"";
+    o << ",\"kernel\":\"" << (kind == 1 ? "stream" : "macro") << "\",\"kslices\":" << kslices;
     o << ",\"kbox\":{\"kj\":" << kj << ",\"tj\":" << tj << ",\"elements\":" << kbox << ",\"blocks\":" << nblk
       << ",\"steps\":" << nsteps << "}";
     o << ",\"gather_x\":\"" << mode_name(xmode) << "\",\"gather_y\":\"" << mode_name(ymode)

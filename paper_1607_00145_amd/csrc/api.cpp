@@ -169,12 +169,22 @@ gett_status_t gett_contract(const gett_plan_t plan, double alpha, const void *A,
     if (d.xcdremap < 0) d.xcdremap = (d.order == 1 && beta != 0.0) ? 0 : 1;
     if (!readAB) {   // alpha == 0 or empty sum: C <- beta * C, A and B untouched
         d.nsteps = 0;
+        d.kslices = 1;
         X = nullptr;
         Y = nullptr;
     }
-    gett::LaunchFn fn = gett::launch_fn(P.dtype, P.tile, xmode, ymode, P.kind);
+    gett::LaunchFn fn = gett::launch_fn(P.dtype, P.tile, xmode, ymode, P.kind == 1 ? 1 : 0);
     if (!fn) return GETT_ERROR_NOT_SUPPORTED;
     if (inject_launch_fault()) return GETT_ERROR_HIP;
+    if (d.kslices > 1 && beta != 1.0) {
+        // K slices add into C: first C <- beta * C (C <- 0, unread, when
+        // beta == 0) by the same kernel over no K boxes with alpha = 0
+        KDesc d0 = d;
+        d0.nsteps = 0;
+        d0.kslices = 1;
+        const hipError_t e0 = fn(d0, nullptr, nullptr, C, 0.0, beta, (hipStream_t)stream);
+        if (e0 != hipSuccess) return GETT_ERROR_HIP;
+    }
     const hipError_t e = fn(d, X, Y, C, alpha, beta, (hipStream_t)stream);
     return e == hipSuccess ? GETT_SUCCESS : GETT_ERROR_HIP;
 }
@@ -227,7 +237,7 @@ gett_status_t gett_plan_tune(gett_plan_t plan, int max_candidates, const void *A
         }
         ms /= 3.0f;
         log << (i ? "," : "") << "{\"tile\":" << ranked[i].tile << ",\"kind\":\""
-            << (ranked[i].kind ? "stream" : "macro") << "\",\"model_us\":" << ranked[i].cost * 1e6
+            << gett::kind_name(ranked[i].kind) << "\",\"model_us\":" << ranked[i].cost * 1e6
             << ",\"measured_us\":" << ms * 1e3 << "}";
         if (best < 0 || ms < bestMs) {
             best = (int)i;

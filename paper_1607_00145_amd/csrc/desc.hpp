@@ -64,6 +64,8 @@ struct KDesc {
     int32_t yscalar_kfast;         // scalar gather of Y: 1 = contracted index fastest
     int32_t yes;                   // strided vector gathers of Y: distance between the
                                    // elements of one vector (extent of the first index)
+    int32_t kslices;               // workgroups per tile, each summing an equal share of
+                                   // the K boxes into C with atomics (1: one per tile)
 };
 
 }  // namespace gett

@@ -75,10 +75,8 @@ constexpr int kInvalidK = 0x7fffffff;
 // contractions), or walk y fastest, so that the workgroups running at one time
 // write neighbouring stretches of C (streaming contractions, where DRAM page
 // locality of the C stream decides the bandwidth).
-__device__ __forceinline__ void tile_of_block(const KDesc &d, int &tx, int &ty)
+__device__ __forceinline__ void tile_of_block(const KDesc &d, int bid, int nwg, int &tx, int &ty)
 {
-    const int nwg = (int)gridDim.x;
-    const int bid = (int)blockIdx.x;
     const int full = nwg & ~7;
     int logical = bid;
     if (d.xcdremap && bid < full) logical = (bid & 7) * (full >> 3) + (bid >> 3);
@@ -476,6 +474,29 @@ struct WaveTile {
             }
         }
     }
+
+    // One K slice's share of the tile: C += alpha * acc with hardware float
+    // atomics (C was set to beta * C beforehand; the slices of a tile add in
+    // whatever order they finish).
+    __device__ __forceinline__ void unpack_atomic(T *__restrict__ C, const int *offCx,
+                                                  const int *offCy, T alpha) const
+    {
+#pragma unroll
+        for (int grp = 0; grp < RB / RX; ++grp) {
+            int ox[NR];
+            rows_of(offCx, grp, ox);
+            int oy[CB];
+#pragma unroll
+            for (int b = 0; b < CB; ++b) oy[b] = offCy[wn * WTN + block_row<RY>(b, l16)];
+#pragma unroll
+            for (int q = 0; q < NR; ++q)
+#pragma unroll
+                for (int b = 0; b < CB; ++b) {
+                    if (ox[q] < 0 || oy[b] < 0) continue;
+                    unsafeAtomicAdd(C + ox[q] + oy[b], alpha * acc[grp * RX + q / 4][b][q % 4]);
+                }
+        }
+    }
 };
 
 // ---------------------------------------------------------------------------
@@ -506,8 +527,16 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     __shared__ int kco[KT];
 
     const int tid = (int)threadIdx.x;
+    // K slices: workgroup b computes slice b / tiles of tile b % tiles.
+    const int slices = d.kslices > 1 ? d.kslices : 1;
+    int bid = (int)blockIdx.x, nwg = (int)gridDim.x, slice = 0;
+    if (slices > 1) {
+        nwg = d.tilesX * d.tilesY;
+        slice = bid / nwg;
+        bid -= slice * nwg;
+    }
     int tx, ty;
-    tile_of_block(d, tx, ty);
+    tile_of_block(d, bid, nwg, tx, ty);
     tile_tables<MT, NT, NTH>(d, tx, ty, tid, rowX, offCx, rowY, offCy);
     box_tables<KT, NTH>(d, tid, kX, kY, kco);
     __syncthreads();
@@ -520,11 +549,13 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     w.init(tid);
     w.zero();
 
-    const uint32_t nsteps = (uint32_t)d.nsteps;
+    // boxes [s0, s0 + nsteps) of the contracted set: all of them, or this slice's share
+    const uint32_t s0 = (uint32_t)((uint64_t)d.nsteps * slice / slices);
+    const uint32_t nsteps = (uint32_t)((uint64_t)d.nsteps * (slice + 1) / slices) - s0;
     auto fetch = [&](auto stage, uint32_t s) {
         constexpr int B = decltype(stage)::value;
         int ox, oy;
-        const int lim = box_origin(d, s, ox, oy);
+        const int lim = box_origin(d, s0 + s, ox, oy);
         gx.template load<B>(X + ox, lim);
         gy.template load<B>(Y + oy, lim);
     };
@@ -575,7 +606,10 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
             if (s + 1 < nsteps) step(S1(), s + 1);
         }
     }
-    w.unpack(C, offCx, offCy, alpha, beta, d.cvec != 0);
+    if (slices > 1)
+        w.unpack_atomic(C, offCx, offCy, alpha);
+    else
+        w.unpack(C, offCx, offCy, alpha, beta, d.cvec != 0);
 }
 
 // ---------------------------------------------------------------------------

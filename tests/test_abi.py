@@ -249,7 +249,8 @@ def test_candidates_are_ranked_by_the_model():
         assert all(c > 0 for c in costs)
         assert len({(c["tile"], c["kind"]) for c in cands}) == len(cands)
         assert d["tile"]["chosen_by"] == "model"
-        assert (cands[0]["tile"], cands[0]["kind"]) == (d["tile"]["id"], d["kernel"])
+        kind = "kslices" if d["kslices"] > 1 else d["kernel"]
+        assert (cands[0]["tile"], cands[0]["kind"]) == (d["tile"]["id"], kind)
         assert d["tile"]["model_us"] == costs[0]
 
 

@@ -14,6 +14,11 @@ from gpu_util import TOL, make_operand, reference, result_view, split
 pytestmark = pytest.mark.gpu
 
 
+def kind_of(d):
+    """The candidate kind of a described plan."""
+    return "kslices" if d["kslices"] > 1 else d["kernel"]
+
+
 def _plan(modes, ops, dt):
     mc, ma, mb = modes
     C, A, B = ops
@@ -55,7 +60,7 @@ def test_tuned_plan_matches_oracle(gpu, name, ext):
         assert [(t["tile"], t["kind"]) for t in timed] == \
             [(c["tile"], c["kind"]) for c in before["candidates"][:len(timed)]]
         best = min(timed, key=lambda t: t["measured_us"])
-        assert (d["tile"]["id"], d["kernel"]) == (best["tile"], best["kind"])
+        assert (d["tile"]["id"], kind_of(d)) == (best["tile"], best["kind"])
         assert all(t["measured_us"] > 0 for t in timed)
         # the tuned plan, with the caller's alpha and beta, against the oracle
         Cin = C.flat.copy()
@@ -73,7 +78,8 @@ def test_tuned_plan_matches_oracle(gpu, name, ext):
         d2 = json.loads(g.gett_plan_describe(h2))
         g.gett_destroy(h2)
         assert d2["tile"]["chosen_by"] == "remembered"
-        assert (d2["tile"]["id"], d2["kernel"]) == (d["tile"]["id"], d["kernel"])
+        assert (d2["tile"]["id"], kind_of(d2)) == (d["tile"]["id"], kind_of(d))
+        assert d2["kslices"] == d["kslices"]
         # another layout of C is another descriptor
         C2 = make_operand(rng, w.shape("C"), dtype, "dense")
         h3 = _plan(modes, (C2, A, B), dt)
@@ -101,7 +107,7 @@ def test_tune_one_candidate_keeps_the_model_choice(gpu):
         assert st == 0
         d = json.loads(g.gett_plan_describe(h))
         assert len(d["tuning"]) == 1
-        assert (d["tile"]["id"], d["kernel"]) == (d0["tile"]["id"], d0["kernel"])
+        assert (d["tile"]["id"], kind_of(d)) == (d0["tile"]["id"], kind_of(d0))
         # C was overwritten with alpha 1, beta 0
         torch.cuda.synchronize()
         got = result_view(bufC.cpu().numpy(), C)
