@@ -468,10 +468,25 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     // box is exposed (measured on MI355X: 1.4-1.8x slower than the
     // double-buffered tiles of the same depth).
     // Each tile's K box is priced on the contracted order that tile gets.
+    const char *ft = getenv("GETT_FORCE_TILE");
+    const char *fk = getenv("GETT_FORCE_KIND");
+    // An operand gathers in vectors when its stride-one index leads its free
+    // order or the contracted order (before any index split).
+    auto vecable = [&](const std::vector<Index> &I, auto strOf) {
+        return strOf(I[0]) == 1 || strOf(Ik[0]) == 1;
+    };
+    const bool slowGather = (flags & GETT_FLAG_SCALAR) || !vecable(Ix, sX) || !vecable(Iy, sY);
     // Every (tile, kernel kind) pair is a candidate; the model ranks them.
     std::vector<Candidate> ranked;
     for (int t = 0; t < num_tiles(dtype); ++t) {
         const TileShape &c = tile_shape(dtype, t);
+        // a one-box tile is ranked only for a contracted set in one box whose
+        // operands are both gathered in vectors: it waits for each operand's
+        // gathers in turn, which element-wise gathers make long (it still
+        // runs any plan it is forced onto)
+        if (c.onebox && (box_for(c.kt).nsteps > 1 || slowGather) && !(ft && atoi(ft) == t) &&
+            !(force && force->tile == t))
+            continue;
         std::vector<Index> ksplit;
         const bool kSplitAhead = k_split(c.kt, ksplit) > 0;
         const Box b = kSplitAhead ? box_on(ksplit, 1, c.kt) : box_for(c.kt);
@@ -522,7 +537,10 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
             cd.kind = k;
             cd.tMfma = tMfma;
             cd.tMem = tMem;
-            cd.cost = bound(std::max(tMfma, tMem), tChain);
+            // element-wise gathers into a single LDS buffer (the streaming
+            // kernel too) wait with nothing to overlap them, as in the K split
+            const double single = (slowGather && (c.nbuf == 1 || k == 1)) ? 1.4 : 1.0;
+            cd.cost = bound(std::max(tMfma, tMem), tChain) * single;
             ranked.push_back(cd);
         }
         // K slices: when a contracted set of many boxes meets too few tiles to
@@ -577,8 +595,6 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     };
     // tuning and test hooks; a choice being timed by gett_plan_tune overrides
     // them, a remembered one does not
-    const char *ft = getenv("GETT_FORCE_TILE");
-    const char *fk = getenv("GETT_FORCE_KIND");
     if (force && (force->timing || !(ft || fk))) {
         if (const Candidate *c = find(force->tile, force->kind)) {
             pick = *c;

@@ -412,12 +412,16 @@ struct WaveTile {
     }
 
     // Unpack (Eq. 11): C <- alpha * acc + beta * C through C's offsets, RX
-    // blocks of rows at a time -- every C load of the group first, so they are
-    // in flight together, then the updates and non-temporal stores (C is
-    // written once and not reused).  C is not read when beta == 0.
+    // blocks of rows at a time (in PARTS parts of the rows, to bound the
+    // registers held) -- every C load of a part first, so they are in flight
+    // together, then the updates and non-temporal stores (C is written once
+    // and not reused).  C is not read when beta == 0.
+    template <int PARTS = 1>
     __device__ __forceinline__ void unpack(T *__restrict__ C, const int *offCx, const int *offCy,
                                            T alpha, T beta, bool cvec) const
     {
+        static_assert(NR % PARTS == 0, "row parts");
+        constexpr int NP = NR / PARTS;
         const bool readC = beta != T(0);
 #pragma unroll
         for (int grp = 0; grp < RB / RX; ++grp) {
@@ -426,51 +430,61 @@ struct WaveTile {
             if (kVecC && cvec) {
                 int oy[CGV];
                 cols_vec(offCy, oy);
-                vec cv[NR][CGV];
-                if (readC) {
 #pragma unroll
-                    for (int q = 0; q < NR; ++q)
+                for (int part = 0; part < PARTS; ++part) {
+                    vec cv[NP][CGV];
+                    if (readC) {
 #pragma unroll
-                        for (int cg = 0; cg < CGV; ++cg)
-                            if (ox[q] >= 0 && oy[cg] >= 0)
-                                cv[q][cg] = __builtin_nontemporal_load(
-                                    reinterpret_cast<const vec *>(C + ox[q] + oy[cg]));
-                }
+                        for (int p = 0; p < NP; ++p)
 #pragma unroll
-                for (int q = 0; q < NR; ++q)
-#pragma unroll
-                    for (int cg = 0; cg < CGV; ++cg) {
-                        if (ox[q] < 0 || oy[cg] < 0) continue;
-                        vec out;
-#pragma unroll
-                        for (int j = 0; j < VW; ++j) {
-                            const T a = alpha * acc[grp * RX + q / 4][kVecC ? cg * RY + j : 0][q % 4];
-                            out[j] = readC ? a + beta * cv[q][cg][j] : a;
-                        }
-                        __builtin_nontemporal_store(out, reinterpret_cast<vec *>(C + ox[q] + oy[cg]));
+                            for (int cg = 0; cg < CGV; ++cg)
+                                if (ox[part * NP + p] >= 0 && oy[cg] >= 0)
+                                    cv[p][cg] = __builtin_nontemporal_load(reinterpret_cast<const vec *>(
+                                        C + ox[part * NP + p] + oy[cg]));
                     }
+#pragma unroll
+                    for (int p = 0; p < NP; ++p)
+#pragma unroll
+                        for (int cg = 0; cg < CGV; ++cg) {
+                            const int q = part * NP + p;
+                            if (ox[q] < 0 || oy[cg] < 0) continue;
+                            vec out;
+#pragma unroll
+                            for (int j = 0; j < VW; ++j) {
+                                const T a =
+                                    alpha * acc[grp * RX + q / 4][kVecC ? cg * RY + j : 0][q % 4];
+                                out[j] = readC ? a + beta * cv[p][cg][j] : a;
+                            }
+                            __builtin_nontemporal_store(out,
+                                                        reinterpret_cast<vec *>(C + ox[q] + oy[cg]));
+                        }
+                }
             } else {
                 int oy[CB];
 #pragma unroll
                 for (int b = 0; b < CB; ++b) oy[b] = offCy[wn * WTN + block_row<RY>(b, l16)];
-                T cv[NR][CB];
-                if (readC) {
 #pragma unroll
-                    for (int q = 0; q < NR; ++q)
+                for (int part = 0; part < PARTS; ++part) {
+                    T cv[NP][CB];
+                    if (readC) {
 #pragma unroll
-                        for (int b = 0; b < CB; ++b)
-                            if (ox[q] >= 0 && oy[b] >= 0)
-                                cv[q][b] = __builtin_nontemporal_load(C + ox[q] + oy[b]);
-                }
+                        for (int p = 0; p < NP; ++p)
 #pragma unroll
-                for (int q = 0; q < NR; ++q)
-#pragma unroll
-                    for (int b = 0; b < CB; ++b) {
-                        if (ox[q] < 0 || oy[b] < 0) continue;
-                        const T a = alpha * acc[grp * RX + q / 4][b][q % 4];
-                        __builtin_nontemporal_store(readC ? a + beta * cv[q][b] : a,
-                                                    C + ox[q] + oy[b]);
+                            for (int b = 0; b < CB; ++b)
+                                if (ox[part * NP + p] >= 0 && oy[b] >= 0)
+                                    cv[p][b] = __builtin_nontemporal_load(C + ox[part * NP + p] + oy[b]);
                     }
+#pragma unroll
+                    for (int p = 0; p < NP; ++p)
+#pragma unroll
+                        for (int b = 0; b < CB; ++b) {
+                            const int q = part * NP + p;
+                            if (ox[q] < 0 || oy[b] < 0) continue;
+                            const T a = alpha * acc[grp * RX + q / 4][b][q % 4];
+                            __builtin_nontemporal_store(readC ? a + beta * cv[p][b] : a,
+                                                        C + ox[q] + oy[b]);
+                        }
+                }
             }
         }
     }
@@ -506,13 +520,14 @@ struct WaveTile {
 // s+2 are issued before the MFMAs of box s, so a gather has two boxes' worth
 // of MFMA time to arrive before its values are written to LDS.
 template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int WPE, int PF,
-          int NBUF, int XMODE, int YMODE>
+          int NBUF, int XMODE, int YMODE, int ONEBOX = 0>
 __global__ void __launch_bounds__(WM *WN * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
                   T *__restrict__ C, const T alpha, const T beta)
 {
     static_assert(PF == 1 || PF == 2, "prefetch depth");
     static_assert(NBUF == 2 || (NBUF == 1 && PF == 1), "one LDS buffer goes with one stage");
+    static_assert(!ONEBOX || (NBUF == 1 && PF == 1), "the one-box kernel has one stage");
     constexpr int NTH = WM * WN * 64;
     typedef Gather<T, MT, KT, XMODE, NTH, PF> GX;
     typedef Gather<T, NT, KT, YMODE, NTH, PF> GY;
@@ -561,7 +576,22 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     };
     typedef std::integral_constant<int, 0> S0;
     typedef std::integral_constant<int, 1> S1;
-    if constexpr (PF == 1) {
+    if constexpr (ONEBOX) {
+        // gather and pack X, then Y, then multiply, box after box: nothing in
+        // flight across the MFMAs and one operand's values staged at a time
+        // (a contracted set in one box needs no more)
+        for (uint32_t s = 0; s < nsteps; ++s) {
+            int ox, oy;
+            const int lim = box_origin(d, s0 + s, ox, oy);
+            gx.template load<0>(X + ox, lim);
+            if (s > 0) __syncthreads();   // the MFMAs of the previous box are done
+            gx.template store<0>(xs[0]);
+            gy.template load<0>(Y + oy, lim);
+            gy.template store<0>(ys[0]);
+            __syncthreads();
+            w.template macro<GX::PITCH, GY::PITCH>(xs[0], ys[0]);
+        }
+    } else if constexpr (PF == 1) {
         if (nsteps > 0) {
             fetch(S0(), 0);
             gx.template store<0>(xs[0]);
@@ -609,7 +639,7 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     if (slices > 1)
         w.unpack_atomic(C, offCx, offCy, alpha);
     else
-        w.unpack(C, offCx, offCy, alpha, beta, d.cvec != 0);
+        w.template unpack<ONEBOX ? 2 : 1>(C, offCx, offCy, alpha, beta, d.cvec != 0);
 }
 
 // ---------------------------------------------------------------------------

@@ -5,7 +5,7 @@ namespace gett {
 
 LaunchFn launch_fn_f64(int tile, int xm, int ym, int kind)
 {
-    static_assert(kNumTilesF64 == 14, "update the tile switch");
+    static_assert(kNumTilesF64 == 15, "update the tile switch");
     switch (tile) {
     case 0: return pick_modes<double, 0>(xm, ym, kind);
     case 1: return pick_modes<double, 1>(xm, ym, kind);
@@ -21,6 +21,7 @@ LaunchFn launch_fn_f64(int tile, int xm, int ym, int kind)
     case 11: return pick_modes<double, 11>(xm, ym, kind);
     case 12: return pick_modes<double, 12>(xm, ym, kind);
     case 13: return pick_modes<double, 13>(xm, ym, kind);
+    case 14: return pick_modes<double, 14>(xm, ym, kind);
     }
     return nullptr;
 }

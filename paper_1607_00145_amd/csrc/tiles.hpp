@@ -23,6 +23,8 @@ struct TileShape {
     float eff;   // fraction of the MFMA peak sustained when compute-bound
     float bw;    // fraction of the HBM peak sustained when streaming C (macro-kernel)
     float sbw;   // the same for the streaming kernel
+    int onebox;  // 1: no prefetch (each box gathered, packed and multiplied in turn),
+                 // for contracted sets that fit one K box; fewer registers live at once
 };
 
 constexpr TileShape kTilesF32[] = {
@@ -49,6 +51,7 @@ constexpr TileShape kTilesF64[] = {
     {64, 128, 24, 2, 2, 2, 2, 3, 1, 1, 0, 0.785f, 0.668f, 0.0f},
     {64, 32, 16, 2, 2, 2, 1, 2, 2, 2, 0, 0.70f, 0.485f, 0.0f},
     {32, 64, 16, 2, 2, 1, 2, 2, 2, 2, 0, 0.71f, 0.49f, 0.0f},
+    {64, 128, 24, 2, 2, 2, 2, 4, 1, 1, 0, 0.785f, 0.70f, 0.0f, 1},
 };
 constexpr int kNumTilesF32 = sizeof(kTilesF32) / sizeof(kTilesF32[0]);
 constexpr int kNumTilesF64 = sizeof(kTilesF64) / sizeof(kTilesF64[0]);

@@ -186,7 +186,7 @@ def test_plan_class_on_torch_views(gpu):
     assert p.describe()["dtype"] == "f64"
 
 
-TILES = {np.float32: 7, np.float64: 14}
+TILES = {np.float32: 7, np.float64: 15}
 
 
 @pytest.mark.parametrize("dtype,tile", [(dt, t) for dt in DTYPES for t in range(TILES[dt])])
