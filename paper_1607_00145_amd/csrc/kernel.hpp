@@ -222,6 +222,44 @@ struct Gather {
         }
     }
 
+    // load(p, limit) then store(tile), one item at a time (few registers)
+    __device__ __forceinline__ void copy(const T *__restrict__ p, int limit, T *tile)
+    {
+#pragma unroll
+        for (int it = 0; it < NI; ++it) {
+            const int slot = kConst ? lds[0] + it * lstep : lds[kConst ? 0 : it];
+            if (!kFull && slot < 0) continue;
+            T v[W];
+            if (kc[it] < limit) {
+                if (W == 1) {
+                    v[0] = p[goff[it]];
+                } else {
+                    const vec x = *reinterpret_cast<const vec *>(p + goff[it]);
+#pragma unroll
+                    for (int e = 0; e < W; ++e) v[e] = x[e];
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < W; ++e) v[e] = T(0);
+            }
+            T *dst = tile + slot;
+            if (MODE == kGatherRowVec) {
+                vec x;
+#pragma unroll
+                for (int e = 0; e < W; ++e) x[e] = v[e];
+                *reinterpret_cast<vec *>(dst) = x;
+            } else if (MODE == kGatherKVec) {
+#pragma unroll
+                for (int e = 0; e < W; ++e) dst[e * PITCH] = v[e];
+            } else if (kStrided) {
+#pragma unroll
+                for (int e = 0; e < W; ++e) dst[e * estep] = v[e];
+            } else {
+                *dst = v[0];
+            }
+        }
+    }
+
     template <int B = 0>
     __device__ __forceinline__ void store(T *tile) const
     {
@@ -370,13 +408,17 @@ struct WaveTile {
                 for (int r = 0; r < 4; ++r) acc[a][b][r] = T(0);
     }
 
-    // acc += X~ * Y~ over the KT positions of one packed box (LDS [k][row]).
-    template <int PX, int PY>
+    // acc += X~ * Y~ over the KT positions of one packed box (LDS [k][row]);
+    // FIRST: acc = X~ * Y~ (the accumulators need no zeroing beforehand).
+    // KU > 0 unrolls the MFMA steps KU at a time, which bounds how many LDS
+    // reads the compiler hoists ahead of the MFMAs (registers).
+    template <int PX, int PY, bool FIRST = false, int KU = 0>
     __device__ __forceinline__ void macro(const T *xs, const T *ys)
     {
         const T *xt = xs + wm * WTM + RX * l16;
         const T *yt = ys + wn * WTN + RY * l16;
-#pragma unroll
+        constexpr int UN = KU > 0 ? KU : KT / 4;
+#pragma unroll UN
         for (int ks = 0; ks < KT / 4; ++ks) {
             const int k = 4 * ks + g;
             typename XV::type av[RB / RX];
@@ -392,7 +434,7 @@ struct WaveTile {
 #pragma unroll
                 for (int b = 0; b < CB; ++b)
                     acc[a][b] = mfma16x16x4(XV::at(av[a / RX], a % RX), YV::at(bv[b / RY], b % RY),
-                                            acc[a][b]);
+                                            FIRST && ks == 0 ? accv{} : acc[a][b]);
         }
     }
 
@@ -562,7 +604,7 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     gy.setup(tid, rowY, kY, kco, d.yscalar_kfast, d.yes);
     WT w;
     w.init(tid);
-    w.zero();
+    if (!ONEBOX) w.zero();
 
     // boxes [s0, s0 + nsteps) of the contracted set: all of them, or this slice's share
     const uint32_t s0 = (uint32_t)((uint64_t)d.nsteps * slice / slices);
@@ -577,19 +619,31 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     typedef std::integral_constant<int, 0> S0;
     typedef std::integral_constant<int, 1> S1;
     if constexpr (ONEBOX) {
-        // gather and pack X, then Y, then multiply, box after box: nothing in
-        // flight across the MFMAs and one operand's values staged at a time
-        // (a contracted set in one box needs no more)
-        for (uint32_t s = 0; s < nsteps; ++s) {
+        // Gather and pack X, then Y, then multiply: nothing in flight across
+        // the MFMAs, one operand's values staged at a time, and the
+        // accumulators first written by the MFMAs (a contracted set in one
+        // box needs no more).  Plans with more boxes (a tile forced onto
+        // them) take the same steps box after box, copying item by item.
+        if (nsteps == 1) {
             int ox, oy;
-            const int lim = box_origin(d, s0 + s, ox, oy);
+            const int lim = box_origin(d, s0, ox, oy);
             gx.template load<0>(X + ox, lim);
-            if (s > 0) __syncthreads();   // the MFMAs of the previous box are done
             gx.template store<0>(xs[0]);
             gy.template load<0>(Y + oy, lim);
             gy.template store<0>(ys[0]);
             __syncthreads();
-            w.template macro<GX::PITCH, GY::PITCH>(xs[0], ys[0]);
+            w.template macro<GX::PITCH, GY::PITCH, true, 2>(xs[0], ys[0]);
+        } else {
+            w.zero();
+            for (uint32_t s = 0; s < nsteps; ++s) {
+                int ox, oy;
+                const int lim = box_origin(d, s0 + s, ox, oy);
+                if (s > 0) __syncthreads();   // the MFMAs of the previous box are done
+                gx.copy(X + ox, lim, xs[0]);
+                gy.copy(Y + oy, lim, ys[0]);
+                __syncthreads();
+                w.template macro<GX::PITCH, GY::PITCH, false, 2>(xs[0], ys[0]);
+            }
         }
     } else if constexpr (PF == 1) {
         if (nsteps > 0) {
