@@ -122,3 +122,42 @@ def test_workload_structures_sliced(gpu, monkeypatch, number):
     rng = np.random.default_rng(number)
     check_case(gpu, rng, (w.modes_C, w.modes_A, w.modes_B),
                (w.shape("C"), w.shape("A"), w.shape("B")), dtype, w.alpha, w.beta)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f64"])
+@pytest.mark.parametrize("number", [13, 14, 19])
+def test_appendix_sliced_full_size(gpu, number, dtype):
+    """The model's sliced plans at the paper's extents (Appendix A
+    contractions 13, 14, 19; Tables III / IV), alpha 1.5 and beta -0.5 on a
+    filled C (the beta pass runs), 1024 sampled elements against the oracle."""
+    import torch
+
+    import oracle
+    from gpu_util import TOL
+    from workloads.appendix_a import appendix_workloads
+    w = appendix_workloads(dtype)[number - 1]
+    npdt = np.float32 if dtype == "f32" else np.float64
+    A, B, _ = wl.make_inputs(w)
+    rng = np.random.default_rng(w.seed + 7)
+    C0 = rng.uniform(-1, 1, w.numel("C")).astype(npdt)
+    flat = lambda t: torch.from_numpy(np.asfortranarray(t).reshape(-1, order="F")).to(gpu)
+    tA, tB, tC = flat(A), flat(B), torch.from_numpy(C0.copy()).to(gpu)
+    code = g.GETT_FLOAT32 if dtype == "f32" else g.GETT_FLOAT64
+    st, h = g.gett_plan(code, w.modes_C, w.shape("C"), None, w.modes_A, w.shape("A"), None,
+                        w.modes_B, w.shape("B"), None, 0)
+    assert st == 0
+    try:
+        assert json.loads(g.gett_plan_describe(h))["kslices"] > 1
+        st = g.gett_contract(h, 1.5, tA.data_ptr(), tB.data_ptr(), -0.5, tC.data_ptr(),
+                             torch.cuda.current_stream().cuda_stream)
+        assert st == 0
+        torch.cuda.synchronize()
+    finally:
+        g.gett_destroy(h)
+    nC = w.numel("C")
+    pts = np.concatenate([rng.integers(0, nC, 1020), [0, 1, nC - 2, nC - 1]])
+    got = tC[torch.from_numpy(pts).to(gpu)].cpu().numpy()
+    Cin = C0.reshape(w.shape("C"), order="F")
+    ref = oracle.contract(w.modes_C, w.modes_A, w.modes_B, A, B, 1.5, -0.5, Cin,
+                          shape_C=w.shape("C"), points=pts)
+    assert oracle.rel_error(got, ref) <= TOL[npdt]
