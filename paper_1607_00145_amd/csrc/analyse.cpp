@@ -714,15 +714,27 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     // by C stride (the row operand's stride-one index stays first when it is
     // a free index, for its vector gathers) and tiles y-fastest.
     const bool streaming = bestMem > bestMfma;
+    // C's stride-one run along y, when shorter than a cache line and continued
+    // in memory by a row index: C is then stored in its memory order (below),
+    // which pays only if consecutive tile rows are consecutive in C, so that
+    // row index leads the x order -- taken when the row operand is small next
+    // to C (its gathers may lose their vectors).
+    const int64_t shortRun = Iy[0].strC == 1 && Iy[0].extent * (int64_t)itemB < 128 ? Iy[0].extent : 0;
+    int rowNext = -1;
+    for (size_t i = 0; i < Ix.size() && shortRun; ++i)
+        if (Ix[i].strC == shortRun) rowNext = (int)i;
+    const bool corderRows = rowNext >= 0 && bytesX * 8.0 < bytesC && !(flags & GETT_FLAG_SCALAR);
     if (streaming) {
         std::stable_sort(Ix.begin(), Ix.end(), [](const Index &a, const Index &b) {
             return a.strC < b.strC;
         });
-        for (size_t i = 0; i < Ix.size(); ++i)
+        for (size_t i = 0; i < Ix.size() && !corderRows; ++i)
             if (sX(Ix[i]) == 1) {
                 std::rotate(Ix.begin(), Ix.begin() + i, Ix.begin() + i + 1);
                 break;
             }
+    } else if (corderRows) {
+        std::rotate(Ix.begin(), Ix.begin() + rowNext, Ix.begin() + rowNext + 1);
     }
     const int kj = box.kj;
     const int64_t tj = box.tj, kbox = box.kbox, nblk = box.nblk, nsteps = box.nsteps;
@@ -755,6 +767,25 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     for (auto &x : Ix) if (x.strC % VW) cvec = false;
     for (size_t i = 1; i < Iy.size(); ++i) if (Iy[i].strC % VW) cvec = false;
     if (ts.ry != VW) cvec = false;   // the tile's lanes do not own VW consecutive columns
+    // C stored in its memory order through LDS (unpack_c_order): when C's
+    // stride-one run along y is shorter than a cache line and C continues in
+    // memory along a row index, the per-lane stores would cut every line.
+    // At least one run must fit a staging pass of the packing buffers.
+    int crun = 0;
+    if (cvec && kind == 0 && kslices == 1 && !ts.onebox && ysplit != kGatherRowVecStrided &&
+        Iy.size() > 1) {
+        const int64_t E = Iy[0].extent;
+        bool rowNext = false;
+        for (auto &x : Ix)
+            if (x.strC == E) rowNext = true;
+        const int64_t cap = (int64_t)ts.nbuf * ts.kt * ((ts.mt + VW) + (ts.nt + VW));
+        if (rowNext && E * (int64_t)itemB < 128 && E % VW == 0 && E < ts.nt &&
+            (cap / ts.mt - VW) / E >= 1)
+            crun = (int)E;
+    }
+    if (const char *co = getenv("GETT_C_ORDER")) {   // tuning hook: 0 turns it off
+        if (atoi(co) == 0) crun = 0;
+    }
 
     // ---- descriptor ----
     KDesc d;
@@ -800,6 +831,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     d.yscalar_kfast = sY(Ik[0]) < sY(Iy[0]) ? 1 : 0;
     d.yes = yes;
     d.kslices = kslices;
+    d.crun = crun;
     if (!an.emptyC && tilesX * tilesY * kslices * ts.wm * ts.wn * 64 >= (int64_t)UINT32_MAX)
         return GETT_ERROR_NOT_SUPPORTED;
 
@@ -861,7 +893,8 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     o << ",\"kbox\":{\"kj\":" << kj << ",\"tj\":" << tj << ",\"elements\":" << kbox << ",\"blocks\":" << nblk
       << ",\"steps\":" << nsteps << "}";
     o << ",\"gather_x\":\"" << mode_name(xmode) << "\",\"gather_y\":\"" << mode_name(ymode)
-      << "\",\"c_vector\":" << (cvec ? "true" : "false") << ",\"y_vector_stride\":" << yes;
+      << "\",\"c_vector\":" << (cvec ? "true" : "false") << ",\"y_vector_stride\":" << yes
+      << ",\"c_order_run\":" << crun;
     o << ",\"grid\":{\"tiles_x\":" << tilesX << ",\"tiles_y\":" << tilesY << ",\"workgroups\":"
       << tilesX * tilesY << ",\"threads\":" << ts.wm * ts.wn * 64 << "}";
     o << ",\"empty_c\":" << (an.emptyC ? "true" : "false") << ",\"empty_sum\":"

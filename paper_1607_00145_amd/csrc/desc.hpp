@@ -66,6 +66,8 @@ struct KDesc {
                                    // elements of one vector (extent of the first index)
     int32_t kslices;               // workgroups per tile, each summing an equal share of
                                    // the K boxes into C with atomics (1: one per tile)
+    int32_t crun;                  // > 0: C's stride-one run along y, stored in C order
+                                   // through LDS (E elements; 0: per-lane stores only)
 };
 
 }  // namespace gett

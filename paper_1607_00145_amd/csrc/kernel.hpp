@@ -452,15 +452,54 @@ struct WaveTile {
 #pragma unroll
         for (int cg = 0; cg < CGV; ++cg) oy[cg] = offCy[wn * WTN + cg * 16 * RY + RY * l16];
     }
+    // tile-local first column of this lane's column group cg (vector C accesses)
+    __device__ __forceinline__ int col_of(int cg) const { return wn * WTN + cg * 16 * RY + RY * l16; }
+    // tile-local row of element q of row group grp of this lane
+    __device__ __forceinline__ int row_of(int grp, int q) const
+    {
+        return wm * WTM + block_row<RX>(grp * RX + q / 4, Traits<T>::mrow(g, q % 4));
+    }
+    // column y lies in a run [kE, kE + E) wholly inside [y0, ylim)
+    static __device__ __forceinline__ bool in_whole_run(int y, int y0, int ylim, int E)
+    {
+        const int k = y / E;
+        return k * E >= y0 && (k + 1) * E <= ylim;
+    }
+    // alpha * acc of the column groups whose first column lies in [c0, c1)
+    // into stage[row][col - c0] (row pitch `pitch`; vector C accesses only)
+    __device__ __forceinline__ void stage(T *st, int pitch, int c0, int c1, T alpha) const
+    {
+        if constexpr (kVecC) {
+#pragma unroll
+            for (int grp = 0; grp < RB / RX; ++grp)
+#pragma unroll
+                for (int cg = 0; cg < CGV; ++cg) {
+                    const int col = col_of(cg);
+                    if (col < c0 || col >= c1) continue;
+#pragma unroll
+                    for (int q = 0; q < NR; ++q) {
+                        vec v;
+#pragma unroll
+                        for (int j = 0; j < VW; ++j) v[j] = alpha * acc[grp * RX + q / 4][cg * RY + j][q % 4];
+                        *reinterpret_cast<vec *>(st + row_of(grp, q) * pitch + (col - c0)) = v;
+                    }
+                }
+        }
+    }
 
     // Unpack (Eq. 11): C <- alpha * acc + beta * C through C's offsets, RX
     // blocks of rows at a time (in PARTS parts of the rows, to bound the
     // registers held) -- every C load of a part first, so they are in flight
     // together, then the updates and non-temporal stores (C is written once
     // and not reused).  C is not read when beta == 0.
+    //
+    // E > 0 (vector C accesses only): skip the column groups that lie in a run
+    // of E columns wholly inside the tile's columns [y0, ylim) -- those are
+    // stored in C's memory order by unpack_c_order.
     template <int PARTS = 1>
     __device__ __forceinline__ void unpack(T *__restrict__ C, const int *offCx, const int *offCy,
-                                           T alpha, T beta, bool cvec) const
+                                           T alpha, T beta, bool cvec, int y0 = 0, int ylim = 0,
+                                           int E = 0) const
     {
         static_assert(NR % PARTS == 0, "row parts");
         constexpr int NP = NR / PARTS;
@@ -472,6 +511,11 @@ struct WaveTile {
             if (kVecC && cvec) {
                 int oy[CGV];
                 cols_vec(offCy, oy);
+                if (E > 0) {
+#pragma unroll
+                    for (int cg = 0; cg < CGV; ++cg)
+                        if (in_whole_run(y0 + col_of(cg), y0, ylim, E)) oy[cg] = -1;
+                }
 #pragma unroll
                 for (int part = 0; part < PARTS; ++part) {
                     vec cv[NP][CGV];
@@ -556,6 +600,56 @@ struct WaveTile {
 };
 
 // ---------------------------------------------------------------------------
+// Unpack in C's memory order, for a C whose stride-one run (E elements of the
+// first column index) is shorter than a cache line while the next index in
+// memory is a row index: the per-lane stores of the MFMA layout would write
+// each 16-lane piece of a row into several runs, partial lines all.  The
+// columns of every run wholly inside the tile are staged in LDS (the packing
+// buffers, free after the K loop; as many runs per pass as fit in `cap`
+// elements) and the workgroup stores them as (run, row, 16-byte piece) in
+// order, so consecutive lanes write consecutive addresses through a run and
+// on across rows.  Columns of runs cut by the tile's edges are stored per lane.
+template <typename T, int MT, int NTH, typename WT>
+__device__ __forceinline__ void unpack_c_order(const WT &w, T *__restrict__ C, T *stage, int cap,
+                                               const int *offCx, const int *offCy, int y0,
+                                               int ylim, int E, T alpha, T beta, int tid)
+{
+    constexpr int VW = Traits<T>::VW;
+    typedef typename Traits<T>::vec vec;
+    w.unpack(C, offCx, offCy, alpha, beta, true, y0, ylim, E);   // runs cut by the edges
+    const int k0 = (y0 + E - 1) / E, k1 = ylim / E;            // whole runs [k0, k1)
+    if (k1 <= k0) return;
+    const int perPass = (cap / MT - VW) / E;                   // >= 1 (checked by the plan)
+    const int pitch = perPass * E + VW;
+    const int pieces = E / VW;                                 // 16-byte pieces per run row
+    const bool readC = beta != T(0);
+    for (int ka = k0; ka < k1; ka += perPass) {
+        const int kb = min(k1, ka + perPass);
+        const int c0 = ka * E - y0, c1 = kb * E - y0;         // tile-local columns of the pass
+        __syncthreads();   // the LDS is free: the last MFMAs or the previous pass are done
+        w.stage(stage, pitch, c0, c1, alpha);
+        __syncthreads();
+        const int n = (kb - ka) * MT * pieces;
+        for (int L = tid; L < n; L += NTH) {
+            const int run = L / (MT * pieces);
+            const int rest = L - run * (MT * pieces);
+            const int row = rest / pieces;
+            const int col = c0 + run * E + (rest - row * pieces) * VW;
+            const int ox = offCx[row];
+            if (ox < 0) continue;   // a row outside the tensor
+            vec v = *reinterpret_cast<const vec *>(stage + row * pitch + (col - c0));
+            T *dst = C + ox + offCy[col];
+            if (readC) {
+                const vec c = __builtin_nontemporal_load(reinterpret_cast<const vec *>(dst));
+#pragma unroll
+                for (int j = 0; j < VW; ++j) v[j] += beta * c[j];
+            }
+            __builtin_nontemporal_store(v, reinterpret_cast<vec *>(dst));
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // The macro-kernel: one tile per workgroup, any number of K boxes, NBUF LDS
 // buffers (one suits a contracted set that fits one box).  With PF = 1 the gathers of box s+1 are issued before the MFMAs
 // of box s; with PF = 2 there are two register stages and the gathers of box
@@ -575,8 +669,12 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     typedef Gather<T, NT, KT, YMODE, NTH, PF> GY;
     typedef WaveTile<T, MT, NT, KT, WM, WN, RX, RY> WT;
 
-    __shared__ __attribute__((aligned(16))) T xs[NBUF][KT * GX::PITCH];
-    __shared__ __attribute__((aligned(16))) T ys[NBUF][KT * GY::PITCH];
+    // the packed panels; after the K loop the same memory stages C for
+    // unpack_c_order
+    constexpr int kPanels = NBUF * KT * (GX::PITCH + GY::PITCH);
+    __shared__ __attribute__((aligned(16))) T panels[kPanels];
+    T(*xs)[KT * GX::PITCH] = reinterpret_cast<T(*)[KT * GX::PITCH]>(panels);
+    T(*ys)[KT * GY::PITCH] = reinterpret_cast<T(*)[KT * GY::PITCH]>(panels + NBUF * KT * GX::PITCH);
     // Element offsets fit in 31 bits (the plan refuses larger tensors); -1 marks
     // a row or column outside the tensor.
     __shared__ int rowX[MT], rowY[NT], offCx[MT], offCy[NT];
@@ -690,10 +788,16 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
             if (s + 1 < nsteps) step(S1(), s + 1);
         }
     }
-    if (slices > 1)
+    if (slices > 1) {
         w.unpack_atomic(C, offCx, offCy, alpha);
-    else
+    } else if (WT::kVecC && d.crun > 0 && d.cvec) {
+        const int y0 = ty * NT;
+        const int ylim = (int)min((int64_t)y0 + NT, d.sizeY);
+        unpack_c_order<T, MT, NTH>(w, C, panels, kPanels, offCx, offCy, y0, ylim, d.crun, alpha,
+                                   beta, tid);
+    } else {
         w.template unpack<ONEBOX ? 2 : 1>(C, offCx, offCy, alpha, beta, d.cvec != 0);
+    }
 }
 
 // ---------------------------------------------------------------------------
