@@ -829,6 +829,22 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     d.cvec = cvec ? 1 : 0;
     d.xscalar_kfast = sX(Ik[0]) < sX(Ix[0]) ? 1 : 0;
     d.yscalar_kfast = sY(Ik[0]) < sY(Iy[0]) ? 1 : 0;
+    // Element-wise gathers of an operand that is stride-one along the second
+    // index of its free set: the lanes walk that index (rows grouped by the
+    // first index's value) -- their loads then touch few cache lines.
+    auto lane_perm = [&](const std::vector<Index> &I, auto strOf, int mode, int rows,
+                         int32_t &kfast) -> int32_t {
+        if (mode != kGatherScalar || I.size() < 2 || strOf(I[1]) != 1 || I[0].extent >= rows ||
+            I[0].extent < 2)
+            return 0;
+        kfast = 0;
+        return (int32_t)I[0].extent;
+    };
+    d.xperm = lane_perm(Ix, sX, xmode, ts.mt, d.xscalar_kfast);
+    d.yperm = lane_perm(Iy, sY, ymode, ts.nt, d.yscalar_kfast);
+    if (const char *lp = getenv("GETT_LANE_PERM")) {   // tuning hook: 0 turns it off
+        if (atoi(lp) == 0) d.xperm = d.yperm = 0;
+    }
     d.yes = yes;
     d.kslices = kslices;
     d.crun = crun;
@@ -894,7 +910,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
       << ",\"steps\":" << nsteps << "}";
     o << ",\"gather_x\":\"" << mode_name(xmode) << "\",\"gather_y\":\"" << mode_name(ymode)
       << "\",\"c_vector\":" << (cvec ? "true" : "false") << ",\"y_vector_stride\":" << yes
-      << ",\"c_order_run\":" << crun;
+      << ",\"c_order_run\":" << crun << ",\"lane_perm\":[" << d.xperm << "," << d.yperm << "]";
     o << ",\"grid\":{\"tiles_x\":" << tilesX << ",\"tiles_y\":" << tilesY << ",\"workgroups\":"
       << tilesX * tilesY << ",\"threads\":" << ts.wm * ts.wn * 64 << "}";
     o << ",\"empty_c\":" << (an.emptyC ? "true" : "false") << ",\"empty_sum\":"

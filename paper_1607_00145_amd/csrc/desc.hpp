@@ -68,6 +68,8 @@ struct KDesc {
                                    // the K boxes into C with atomics (1: one per tile)
     int32_t crun;                  // > 0: C's stride-one run along y, stored in C order
                                    // through LDS (E elements; 0: per-lane stores only)
+    int32_t xperm, yperm;          // > 0: element-wise gathers of X (Y) walk the tile rows
+                                   // grouped by row mod this extent (0: in order)
 };
 
 }  // namespace gett

@@ -158,8 +158,11 @@ struct Gather {
     // rowoff: LDS table of operand offsets per tile row (-1 = outside the tensor)
     // koff/kco: LDS tables of offsets / kj-positions per box element
     // es: extent of the first row (K) index in the strided modes
+    // perm (scalar rows-fastest mode only, may be null): lane order over the
+    // tile rows -- item row r gathers tile row perm[r]
     __device__ __forceinline__ void setup(int tid, const int *rowoff, const int *koff,
-                                          const int *kco, int kfast, int es = 1)
+                                          const int *kco, int kfast, int es = 1,
+                                          const int *perm = nullptr)
     {
         lstep = 0;
         estep = MODE == kGatherKVecStrided ? es * PITCH : es;
@@ -187,6 +190,7 @@ struct Gather {
             } else {
                 r = i % ROWS;
                 kk = i / ROWS;
+                if (perm) r = perm[r];
             }
             const bool act = kFull || i < ITEMS;
             const int ro = act ? rowoff[r] : -1;
@@ -360,6 +364,33 @@ __device__ __forceinline__ void box_tables(const KDesc &d, int tid, int *kX, int
         kX[kk] = ox;
         kY[kk] = oy;
         kco[kk] = pos;
+    }
+}
+
+// Lane order for an element-wise gather whose operand is stride-one along
+// the second index of the tile's rows (the first, of extent E, has a large
+// stride there): rows are taken grouped by y mod E and then by y / E, so that
+// consecutive lanes step along the operand's stride-one index.  Row r of the
+// tile (global y = y0 + r) goes to position
+//   start(a) + (r - t(a)) / E,   a = y mod E, t(a) = (a - y0) mod E,
+// where start(a) counts the rows of the residues before a: each residue has
+// q = R / E rows plus one if t < R mod E.
+template <int R, int NTH>
+__device__ __forceinline__ void row_perm(int E, int y0, int tid, int *perm)
+{
+    const int q = R / E, rem = R % E, s = y0 % E;
+    const int u = (E - s) % E;   // t of residue 0
+    for (int r = tid; r < R; r += NTH) {
+        const int a = (y0 + r) % E;
+        const int t = (a - s + E) % E;
+        // residues 0..a-1 have t in the cyclic range [u, u + a) mod E; count those below rem
+        int below;
+        if (u + a <= E) {
+            below = max(0, min(u + a, rem) - u);
+        } else {
+            below = max(0, rem - u) + min(u + a - E, rem);
+        }
+        perm[a * q + below + (r - t) / E] = r;
     }
 }
 
@@ -680,6 +711,7 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     __shared__ int rowX[MT], rowY[NT], offCx[MT], offCy[NT];
     __shared__ int kX[KT], kY[KT];
     __shared__ int kco[KT];
+    __shared__ int permX[XMODE == kGatherScalar ? MT : 1], permY[YMODE == kGatherScalar ? NT : 1];
 
     const int tid = (int)threadIdx.x;
     // K slices: workgroup b computes slice b / tiles of tile b % tiles.
@@ -694,12 +726,16 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     tile_of_block(d, bid, nwg, tx, ty);
     tile_tables<MT, NT, NTH>(d, tx, ty, tid, rowX, offCx, rowY, offCy);
     box_tables<KT, NTH>(d, tid, kX, kY, kco);
+    if (XMODE == kGatherScalar && d.xperm > 0) row_perm<MT, NTH>(d.xperm, tx * MT, tid, permX);
+    if (YMODE == kGatherScalar && d.yperm > 0) row_perm<NT, NTH>(d.yperm, ty * NT, tid, permY);
     __syncthreads();
 
     GX gx;
     GY gy;
-    gx.setup(tid, rowX, kX, kco, d.xscalar_kfast);
-    gy.setup(tid, rowY, kY, kco, d.yscalar_kfast, d.yes);
+    gx.setup(tid, rowX, kX, kco, d.xscalar_kfast, 1,
+             XMODE == kGatherScalar && d.xperm > 0 ? permX : nullptr);
+    gy.setup(tid, rowY, kY, kco, d.yscalar_kfast, d.yes,
+             YMODE == kGatherScalar && d.yperm > 0 ? permY : nullptr);
     WT w;
     w.init(tid);
     if (!ONEBOX) w.zero();

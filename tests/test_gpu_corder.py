@@ -90,3 +90,23 @@ def test_c_order_every_tile(gpu, monkeypatch, dtype, tile):
     rng = np.random.default_rng(600 + tile)
     check_case(gpu, rng, modes, shapes(modes, ext), dtype, 1.5, 0.5)
     check_case(gpu, rng, modes, shapes(modes, ext), dtype, 1.0, 0.0)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float64])
+@pytest.mark.parametrize("name", list(PATTERNS))
+def test_lane_order_same_bits(gpu, monkeypatch, name, dtype):
+    """Element-wise gathers walking the operand's stride-one index (rows
+    grouped by the first index's value) pack the same tiles: identical bits
+    with and without the lane order."""
+    monkeypatch.setenv("GETT_FORCE_TILE", TILE[dtype])
+    monkeypatch.setenv("GETT_FORCE_KIND", "0")
+    modes, ext = PATTERNS[name], EXT[dtype]
+    outs = []
+    for lp in ("1", "0"):
+        monkeypatch.setenv("GETT_LANE_PERM", lp)
+        d = describe(modes, ext, dtype)
+        assert (max(d["lane_perm"]) > 0) == (lp == "1")
+        rng = np.random.default_rng(8)
+        got, _ = check_case(gpu, rng, modes, shapes(modes, ext), dtype, -1.0, 0.5)
+        outs.append(got.copy())
+    np.testing.assert_array_equal(outs[0], outs[1])
