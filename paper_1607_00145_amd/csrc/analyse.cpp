@@ -723,7 +723,8 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     int rowNext = -1;
     for (size_t i = 0; i < Ix.size() && shortRun; ++i)
         if (Ix[i].strC == shortRun) rowNext = (int)i;
-    const bool corderRows = rowNext >= 0 && bytesX * 8.0 < bytesC && !(flags & GETT_FLAG_SCALAR);
+    const bool corderRows = rowNext >= 0 && ts.corder && bytesX * 8.0 < bytesC &&
+                            !(flags & GETT_FLAG_SCALAR);
     if (streaming) {
         std::stable_sort(Ix.begin(), Ix.end(), [](const Index &a, const Index &b) {
             return a.strC < b.strC;
@@ -772,7 +773,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     // memory along a row index, the per-lane stores would cut every line.
     // At least one run must fit a staging pass of the packing buffers.
     int crun = 0;
-    if (cvec && kind == 0 && kslices == 1 && !ts.onebox && ysplit != kGatherRowVecStrided &&
+    if (cvec && ts.corder && kind == 0 && kslices == 1 && ysplit != kGatherRowVecStrided &&
         Iy.size() > 1) {
         const int64_t E = Iy[0].extent;
         bool rowNext = false;

@@ -687,7 +687,7 @@ __device__ __forceinline__ void unpack_c_order(const WT &w, T *__restrict__ C, T
 // s+2 are issued before the MFMAs of box s, so a gather has two boxes' worth
 // of MFMA time to arrive before its values are written to LDS.
 template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int WPE, int PF,
-          int NBUF, int XMODE, int YMODE, int ONEBOX = 0>
+          int NBUF, int XMODE, int YMODE, int ONEBOX = 0, int CORDER = 0>
 __global__ void __launch_bounds__(WM *WN * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
                   T *__restrict__ C, const T alpha, const T beta)
@@ -826,14 +826,18 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     }
     if (slices > 1) {
         w.unpack_atomic(C, offCx, offCy, alpha);
-    } else if (WT::kVecC && d.crun > 0 && d.cvec) {
-        const int y0 = ty * NT;
-        const int ylim = (int)min((int64_t)y0 + NT, d.sizeY);
-        unpack_c_order<T, MT, NTH>(w, C, panels, kPanels, offCx, offCy, y0, ylim, d.crun, alpha,
-                                   beta, tid);
-    } else {
-        w.template unpack<ONEBOX ? 2 : 1>(C, offCx, offCy, alpha, beta, d.cvec != 0);
+        return;
     }
+    if constexpr (CORDER && WT::kVecC) {   // compiled only into the tiles that carry it
+        if (d.crun > 0 && d.cvec) {
+            const int y0 = ty * NT;
+            const int ylim = (int)min((int64_t)y0 + NT, d.sizeY);
+            unpack_c_order<T, MT, NTH>(w, C, panels, kPanels, offCx, offCy, y0, ylim, d.crun,
+                                       alpha, beta, tid);
+            return;
+        }
+    }
+    w.template unpack<ONEBOX ? 2 : 1>(C, offCx, offCy, alpha, beta, d.cvec != 0);
 }
 
 // ---------------------------------------------------------------------------

@@ -43,7 +43,7 @@ hipError_t launch_one(const KDesc &d, const void *X, const void *Y, void *C, dou
     if constexpr (KIND == 0) {
         hipLaunchKernelGGL(
             (gett_macro_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.wpe, t.pf, t.nbuf, XM,
-                               YM, t.onebox>),
+                               YM, t.onebox, t.corder>),
             dim3(tiles * (unsigned)(d.kslices > 1 ? d.kslices : 1)), dim3(threads), 0, stream, d,
             static_cast<const T *>(X),
             static_cast<const T *>(Y), static_cast<T *>(C), static_cast<T>(alpha),

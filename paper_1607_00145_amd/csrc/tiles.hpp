@@ -25,14 +25,15 @@ struct TileShape {
     float sbw;   // the same for the streaming kernel
     int onebox;  // 1: no prefetch (each box gathered, packed and multiplied in turn),
                  // for contracted sets that fit one K box; fewer registers live at once
+    int corder;  // 1: the kernel carries the C-order epilogue (unpack_c_order)
 };
 
 constexpr TileShape kTilesF32[] = {
-    {128, 128, 16, 2, 2, 4, 4, 1, 1, 2, 0, 0.75f, 0.61f, 0.0f},
-    {64, 64, 16, 1, 1, 4, 4, 1, 1, 2, 0, 0.67f, 0.62f, 0.0f},
-    {128, 128, 16, 2, 2, 4, 4, 3, 1, 2, 2, 0.71f, 0.675f, 0.64f},
-    {64, 256, 16, 1, 4, 4, 4, 3, 1, 2, 2, 0.70f, 0.70f, 0.63f},
-    {128, 128, 32, 2, 2, 4, 4, 1, 1, 2, 0, 0.806f, 0.61f, 0.0f},
+    {128, 128, 16, 2, 2, 4, 4, 1, 1, 2, 0, 0.75f, 0.61f, 0.0f, 0, 1},
+    {64, 64, 16, 1, 1, 4, 4, 1, 1, 2, 0, 0.67f, 0.62f, 0.0f, 0, 1},
+    {128, 128, 16, 2, 2, 4, 4, 3, 1, 2, 2, 0.71f, 0.675f, 0.64f, 0, 1},
+    {64, 256, 16, 1, 4, 4, 4, 3, 1, 2, 2, 0.70f, 0.70f, 0.63f, 0, 1},
+    {128, 128, 32, 2, 2, 4, 4, 1, 1, 2, 0, 0.806f, 0.61f, 0.0f, 0, 1},
     {64, 32, 32, 2, 2, 2, 1, 2, 2, 2, 0, 0.64f, 0.35f, 0.0f},
     {32, 64, 32, 2, 2, 1, 2, 2, 2, 2, 0, 0.65f, 0.35f, 0.0f},
 };

@@ -48,11 +48,14 @@ def describe(modes, ext, dtype, flags=0):
 @pytest.mark.parametrize("dtype", [np.float32, np.float64])
 @pytest.mark.parametrize("name", list(PATTERNS))
 def test_c_order_against_oracle(gpu, monkeypatch, name, dtype):
+    """fp32 tiles carry the C-order epilogue; fp64 plans of the same
+    patterns keep the per-lane stores (and their element-wise gathers the
+    lane order)."""
     monkeypatch.setenv("GETT_FORCE_TILE", TILE[dtype])
     monkeypatch.setenv("GETT_FORCE_KIND", "0")
     modes, ext = PATTERNS[name], EXT[dtype]
     d = describe(modes, ext, dtype)
-    assert d["c_order_run"] == ext["a"]
+    assert d["c_order_run"] == (ext["a"] if dtype == np.float32 else 0)
     rng = np.random.default_rng(sum(map(ord, name)))
     for alpha, beta in [(1.0, 0.0), (-1.5, 0.5), (2.0, 1.0), (0.0, -1.0)]:
         check_case(gpu, rng, modes, shapes(modes, ext), dtype, alpha, beta)
@@ -63,7 +66,7 @@ def test_c_order_against_oracle(gpu, monkeypatch, name, dtype):
     np.testing.assert_array_equal(got.astype(np.float64), ref.out64)
 
 
-@pytest.mark.parametrize("dtype", [np.float32, np.float64])
+@pytest.mark.parametrize("dtype", [np.float32])
 @pytest.mark.parametrize("name", list(PATTERNS))
 def test_c_order_same_bits_as_per_lane(gpu, monkeypatch, name, dtype):
     """The staged stores compute alpha * acc + beta * C exactly as the
@@ -101,6 +104,8 @@ def test_lane_order_same_bits(gpu, monkeypatch, name, dtype):
     monkeypatch.setenv("GETT_FORCE_TILE", TILE[dtype])
     monkeypatch.setenv("GETT_FORCE_KIND", "0")
     modes, ext = PATTERNS[name], EXT[dtype]
+    if max(describe(modes, ext, dtype)["lane_perm"]) == 0:
+        pytest.skip("this plan gathers both operands in vectors")
     outs = []
     for lp in ("1", "0"):
         monkeypatch.setenv("GETT_LANE_PERM", lp)
