@@ -79,11 +79,15 @@ typedef struct gett_plan_s *gett_plan_t;
  * the other so that both are read (written) in runs; with this flag the
  * tiles follow the (merged) indices whole. */
 #define GETT_FLAG_NO_SPLIT 4u
-/* Results identical from call to call: no K slices.  By default, when the
- * tiles of C are too few to keep the GPU busy and the contracted set is long,
- * several workgroups share each tile's contracted range and add their
- * partial results into C with atomic additions (after C is set to beta * C),
- * so the order in which the partial sums meet varies between calls. */
+/* Results identical from call to call: no K slices and no stream-K tail.
+ * By default, when the tiles of C are too few to keep the GPU busy and the
+ * contracted set is long, several workgroups share each tile's contracted
+ * range (K slices); and when the tiles fill the workgroups the GPU holds at
+ * once an uneven number of times, the contracted ranges of the tiles left
+ * over from the last whole round are dealt in equal runs to one more round
+ * of workgroups (stream-K tail).  Both add partial results into C with
+ * atomic additions (after C, or those tiles of it, is set to beta * C), so
+ * the order in which the partial sums meet varies between calls. */
 #define GETT_FLAG_DETERMINISTIC 8u
 
 /*

@@ -189,7 +189,19 @@ void json_set(std::ostringstream &o, const char *key, const std::vector<Index> &
 
 }  // namespace
 
-const char *kind_name(int k) { return k == 1 ? "stream" : k == 2 ? "kslices" : "macro"; }
+const char *kind_name(int k)
+{
+    return k == 1 ? "stream" : k == 2 ? "kslices" : k == 3 ? "tail" : "macro";
+}
+
+// Workgroups of a tile resident on one CU at once: the wavefronts per SIMD its
+// register budget allows (a workgroup of four wavefronts puts one on each
+// SIMD), within the 160 KB of LDS its packed panels take.
+static double tail_occupancy(const TileShape &c, double itemB)
+{
+    const double lds = (double)c.nbuf * c.kt * (c.mt + c.nt + 8) * itemB;
+    return std::max(1.0, std::min((double)c.wpe, std::floor(160.0 * 1024.0 / lds)));
+}
 
 namespace {
 
@@ -583,6 +595,44 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
             }
             if (best.tile >= 0) ranked.push_back(best);
         }
+        // Stream-K tail: when the tiles do not fill a whole number of rounds
+        // of the workgroups resident at once (G = occupancy x 256 CUs), the
+        // SIMDs that get one wavefront more set the time, and those left
+        // with one wavefront run it slower than two together.  Instead, the
+        // whole rounds run as usual and the boxes of the remaining r tiles
+        // are dealt in equal runs to G more workgroups, which add their
+        // partial tiles into C with atomics (about r + G tile-sized
+        // read-modify-writes, which add about the time of a 6.8 TB/s stream
+        // of their reads and writes: measured on MI355X, where they overlap
+        // the MFMAs of other workgroups) after one pass that sets those
+        // tiles to beta * C.  Priced as the balanced load of every SIMD plus
+        // two boxes of set-up per piece, the atomics, and the scaling pass's
+        // launch.
+        const double occ = tail_occupancy(c, itemB);
+        const double G = occ * 256.0;
+        const double ntile = tx * ty;
+        const double rem = std::fmod(ntile, G);
+        if (c.tail && !(flags & GETT_FLAG_DETERMINISTIC) && !an.emptyC && wpt >= 4 &&
+            b.nsteps >= 16 && ntile > 256.0 && rem > 0.0) {
+            const double nb = (double)b.nsteps;
+            const double len = std::ceil(rem * nb / G);
+            const double pieces = std::ceil(len / nb) + 1.0;
+            const double boxes = occ * (((ntile - rem) / G) * nb + len + 2.0 * pieces);
+            const double boxFlops = (double)(c.mt / c.wm) * (c.nt / c.wn) * c.kt * 2.0;
+            const double tM = boxes * std::ceil(wpt / 4.0) * boxFlops / (peakSimd * c.eff) *
+                              (kSplitAhead && c.nbuf == 1 ? 1.4 : 1.0);
+            const double tMem = (bytesC + bytesX + bytesY +
+                                 0.05 * (bytesX * (ty - 1) + bytesY * (tx - 1))) /
+                                (8.0e12 * c.bw);
+            const double tAtomic = (rem + G) * c.mt * c.nt * itemB * 2.0 / 6.8e12;
+            Candidate cd;
+            cd.tile = t;
+            cd.kind = 3;
+            cd.tMfma = tM;
+            cd.tMem = tMem;
+            cd.cost = bound(std::max(tM, tMem), tChain) + tAtomic + 3.0e-6;
+            ranked.push_back(cd);
+        }
     }
     std::stable_sort(ranked.begin(), ranked.end(),
                      [](const Candidate &a, const Candidate &b) { return a.cost < b.cost; });
@@ -608,6 +658,11 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         if (c) {
             pick = *c;
             how = "forced";
+            // the stream-K tail on any plan of a tile that carries it (the
+            // model ranks it only where it may pay)
+            if (k == 3 && c->kind == 0 && tile_shape(dtype, t).tail && !an.emptyC &&
+                !(flags & GETT_FLAG_DETERMINISTIC))
+                pick.kind = 3;
         }
     }
     // tuning hook: this many K slices on the chosen tile
@@ -849,6 +904,24 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     d.yes = yes;
     d.kslices = kslices;
     d.crun = crun;
+    d.tile0 = 0;
+    d.tailFull = d.tailWgs = d.tailLen = 0;
+    if (kind == 3 && !an.emptyC) {
+        // whole tiles for the complete rounds of the workgroups resident at
+        // once, the boxes of the rest in equal runs over as many more (tuning
+        // hook: GETT_TAIL_WGS workgroups share the tail instead)
+        int64_t wgs = (int64_t)tail_occupancy(ts, dtype == GETT_FLOAT32 ? 4.0 : 8.0) * 256;
+        if (const char *tw = getenv("GETT_TAIL_WGS")) wgs = std::max<int64_t>(1, atoll(tw));
+        const int64_t T = (int64_t)tilesX * tilesY;
+        int64_t rem = T % wgs;
+        if (rem == 0) rem = std::min<int64_t>(wgs, T);
+        const int64_t nb = std::max<int64_t>(nsteps, 1);
+        const int64_t boxes = rem * nb;
+        const int64_t len = (boxes + std::min(wgs, boxes) - 1) / std::min(wgs, boxes);
+        d.tailFull = (int32_t)(T - rem);
+        d.tailLen = (int32_t)len;
+        d.tailWgs = (int32_t)((boxes + len - 1) / len);   // every one of them gets boxes
+    }
     if (!an.emptyC && tilesX * tilesY * kslices * ts.wm * ts.wn * 64 >= (int64_t)UINT32_MAX)
         return GETT_ERROR_NOT_SUPPORTED;
 
@@ -906,7 +979,10 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     }
     o << "]";
     o << ",\"streaming\":" << (streaming ? "true" : "false");
-    o << ",\"kernel\":\"" << (kind == 1 ? "stream" : "macro") << "\",\"kslices\":" << kslices;
+    o << ",\"kernel\":\"" << (kind == 1 ? "stream" : kind == 3 ? "tail" : "macro")
+      << "\",\"kslices\":" << kslices;
+    o << ",\"tail\":{\"full_tiles\":" << d.tailFull << ",\"workgroups\":" << d.tailWgs
+      << ",\"boxes\":" << d.tailLen << "}";
     o << ",\"kbox\":{\"kj\":" << kj << ",\"tj\":" << tj << ",\"elements\":" << kbox << ",\"blocks\":" << nblk
       << ",\"steps\":" << nsteps << "}";
     o << ",\"gather_x\":\"" << mode_name(xmode) << "\",\"gather_y\":\"" << mode_name(ymode)

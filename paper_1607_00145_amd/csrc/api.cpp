@@ -167,22 +167,27 @@ gett_status_t gett_contract(const gett_plan_t plan, double alpha, const void *A,
     // compute-bound and write-only walks; a read-modify-write C stream
     // (streaming walk, beta != 0) runs faster in hardware order (measured).
     if (d.xcdremap < 0) d.xcdremap = (d.order == 1 && beta != 0.0) ? 0 : 1;
+    int kind = P.kind == 1 || P.kind == 3 ? P.kind : 0;
     if (!readAB) {   // alpha == 0 or empty sum: C <- beta * C, A and B untouched
         d.nsteps = 0;
         d.kslices = 1;
+        if (kind == 3) kind = 0;
         X = nullptr;
         Y = nullptr;
     }
-    gett::LaunchFn fn = gett::launch_fn(P.dtype, P.tile, xmode, ymode, P.kind == 1 ? 1 : 0);
-    if (!fn) return GETT_ERROR_NOT_SUPPORTED;
+    gett::LaunchFn fn = gett::launch_fn(P.dtype, P.tile, xmode, ymode, kind);
+    gett::LaunchFn fn0 = kind == 3 ? gett::launch_fn(P.dtype, P.tile, xmode, ymode, 0) : fn;
+    if (!fn || !fn0) return GETT_ERROR_NOT_SUPPORTED;
     if (inject_launch_fault()) return GETT_ERROR_HIP;
-    if (d.kslices > 1 && beta != 1.0) {
-        // K slices add into C: first C <- beta * C (C <- 0, unread, when
-        // beta == 0) by the same kernel over no K boxes with alpha = 0
+    if ((d.kslices > 1 || kind == 3) && beta != 1.0) {
+        // K slices and the stream-K tail add into C: first C <- beta * C
+        // (C <- 0, unread, when beta == 0) over the tiles they add into, by
+        // the macro-kernel over no K boxes with alpha = 0
         KDesc d0 = d;
         d0.nsteps = 0;
         d0.kslices = 1;
-        const hipError_t e0 = fn(d0, nullptr, nullptr, C, 0.0, beta, (hipStream_t)stream);
+        d0.tile0 = kind == 3 ? d.tailFull : 0;
+        const hipError_t e0 = fn0(d0, nullptr, nullptr, C, 0.0, beta, (hipStream_t)stream);
         if (e0 != hipSuccess) return GETT_ERROR_HIP;
     }
     const hipError_t e = fn(d, X, Y, C, alpha, beta, (hipStream_t)stream);

@@ -70,6 +70,11 @@ struct KDesc {
                                    // through LDS (E elements; 0: per-lane stores only)
     int32_t xperm, yperm;          // > 0: element-wise gathers of X (Y) walk the tile rows
                                    // grouped by row mod this extent (0: in order)
+    int32_t tile0;                 // first tile of the grid (> 0: a pass over tiles tile0..)
+    // ---- stream-K tail (the tail kernel only) ----
+    int32_t tailFull;              // tiles computed whole, one workgroup each
+    int32_t tailWgs;               // workgroups that share the boxes of the other tiles
+    int32_t tailLen;               // boxes per such workgroup
 };
 
 }  // namespace gett

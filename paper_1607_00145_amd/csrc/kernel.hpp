@@ -687,7 +687,7 @@ __device__ __forceinline__ void unpack_c_order(const WT &w, T *__restrict__ C, T
 // s+2 are issued before the MFMAs of box s, so a gather has two boxes' worth
 // of MFMA time to arrive before its values are written to LDS.
 template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int WPE, int PF,
-          int NBUF, int XMODE, int YMODE, int ONEBOX = 0, int CORDER = 0>
+          int NBUF, int XMODE, int YMODE, int ONEBOX = 0, int CORDER = 0, int TAIL = 0>
 __global__ void __launch_bounds__(WM *WN * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
                   T *__restrict__ C, const T alpha, const T beta)
@@ -714,130 +714,162 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     __shared__ int permX[XMODE == kGatherScalar ? MT : 1], permY[YMODE == kGatherScalar ? NT : 1];
 
     const int tid = (int)threadIdx.x;
-    // K slices: workgroup b computes slice b / tiles of tile b % tiles.
-    const int slices = d.kslices > 1 ? d.kslices : 1;
-    int bid = (int)blockIdx.x, nwg = (int)gridDim.x, slice = 0;
-    if (slices > 1) {
-        nwg = d.tilesX * d.tilesY;
-        slice = bid / nwg;
-        bid -= slice * nwg;
-    }
-    int tx, ty;
-    tile_of_block(d, bid, nwg, tx, ty);
-    tile_tables<MT, NT, NTH>(d, tx, ty, tid, rowX, offCx, rowY, offCy);
+    const int ntiles = d.tilesX * d.tilesY;
     box_tables<KT, NTH>(d, tid, kX, kY, kco);
-    if (XMODE == kGatherScalar && d.xperm > 0) row_perm<MT, NTH>(d.xperm, tx * MT, tid, permX);
-    if (YMODE == kGatherScalar && d.yperm > 0) row_perm<NT, NTH>(d.yperm, ty * NT, tid, permY);
-    __syncthreads();
-
-    GX gx;
-    GY gy;
-    gx.setup(tid, rowX, kX, kco, d.xscalar_kfast, 1,
-             XMODE == kGatherScalar && d.xperm > 0 ? permX : nullptr);
-    gy.setup(tid, rowY, kY, kco, d.yscalar_kfast, d.yes,
-             YMODE == kGatherScalar && d.yperm > 0 ? permY : nullptr);
     WT w;
     w.init(tid);
-    if (!ONEBOX) w.zero();
 
-    // boxes [s0, s0 + nsteps) of the contracted set: all of them, or this slice's share
-    const uint32_t s0 = (uint32_t)((uint64_t)d.nsteps * slice / slices);
-    const uint32_t nsteps = (uint32_t)((uint64_t)d.nsteps * (slice + 1) / slices) - s0;
-    auto fetch = [&](auto stage, uint32_t s) {
-        constexpr int B = decltype(stage)::value;
-        int ox, oy;
-        const int lim = box_origin(d, s0 + s, ox, oy);
-        gx.template load<B>(X + ox, lim);
-        gy.template load<B>(Y + oy, lim);
-    };
-    typedef std::integral_constant<int, 0> S0;
-    typedef std::integral_constant<int, 1> S1;
-    if constexpr (ONEBOX) {
-        // Gather and pack X, then Y, then multiply: nothing in flight across
-        // the MFMAs, one operand's values staged at a time, and the
-        // accumulators first written by the MFMAs (a contracted set in one
-        // box needs no more).  Plans with more boxes (a tile forced onto
-        // them) take the same steps box after box, copying item by item.
-        if (nsteps == 1) {
-            int ox, oy;
-            const int lim = box_origin(d, s0, ox, oy);
-            gx.template load<0>(X + ox, lim);
-            gx.template store<0>(xs[0]);
-            gy.template load<0>(Y + oy, lim);
-            gy.template store<0>(ys[0]);
-            __syncthreads();
-            w.template macro<GX::PITCH, GY::PITCH, true, 2>(xs[0], ys[0]);
-        } else {
-            w.zero();
-            for (uint32_t s = 0; s < nsteps; ++s) {
-                int ox, oy;
-                const int lim = box_origin(d, s0 + s, ox, oy);
-                if (s > 0) __syncthreads();   // the MFMAs of the previous box are done
-                gx.copy(X + ox, lim, xs[0]);
-                gy.copy(Y + oy, lim, ys[0]);
-                __syncthreads();
-                w.template macro<GX::PITCH, GY::PITCH, false, 2>(xs[0], ys[0]);
-            }
-        }
-    } else if constexpr (PF == 1) {
-        if (nsteps > 0) {
-            fetch(S0(), 0);
-            gx.template store<0>(xs[0]);
-            gy.template store<0>(ys[0]);
-        }
+    // One piece of work: boxes [s0, s0 + nsteps) of the contracted set for
+    // tile `tile` (a tile id in the order tile_of_block deals them), stored
+    // with alpha / beta, or added into C with atomics when `atomic`.
+    auto piece = [&](int tile, uint32_t s0, uint32_t nsteps, bool atomic) {
+        int tx, ty;
+        tile_of_block(d, tile, ntiles, tx, ty);
+        tile_tables<MT, NT, NTH>(d, tx, ty, tid, rowX, offCx, rowY, offCy);
+        if (XMODE == kGatherScalar && d.xperm > 0) row_perm<MT, NTH>(d.xperm, tx * MT, tid, permX);
+        if (YMODE == kGatherScalar && d.yperm > 0) row_perm<NT, NTH>(d.yperm, ty * NT, tid, permY);
         __syncthreads();
-        for (uint32_t s = 0; s < nsteps; ++s) {
-            const int buf = NBUF == 2 ? (int)(s & 1) : 0;
-            const bool more = s + 1 < nsteps;
-            if (more) fetch(S0(), s + 1);
-            w.template macro<GX::PITCH, GY::PITCH>(xs[buf], ys[buf]);
-            if (NBUF == 1 && more) __syncthreads();   // the single buffer is free again
-            if (more) {
-                gx.template store<0>(xs[NBUF == 2 ? buf ^ 1 : 0]);
-                gy.template store<0>(ys[NBUF == 2 ? buf ^ 1 : 0]);
-            }
-            __syncthreads();
-        }
-    } else {
-        // One box: start the gathers of box s+2 into this stage's registers,
-        // run the MFMAs of box s from LDS buffer B, move box s+1's registers
-        // into the other buffer.
-        auto step = [&](auto stage, uint32_t s) {
+
+        GX gx;
+        GY gy;
+        gx.setup(tid, rowX, kX, kco, d.xscalar_kfast, 1,
+                 XMODE == kGatherScalar && d.xperm > 0 ? permX : nullptr);
+        gy.setup(tid, rowY, kY, kco, d.yscalar_kfast, d.yes,
+                 YMODE == kGatherScalar && d.yperm > 0 ? permY : nullptr);
+        if (!ONEBOX) w.zero();
+        auto fetch = [&](auto stage, uint32_t s) {
             constexpr int B = decltype(stage)::value;
-            if (s + 2 < nsteps) fetch(stage, s + 2);
-            w.template macro<GX::PITCH, GY::PITCH>(xs[B % NBUF], ys[B % NBUF]);
-            if (s + 1 < nsteps) {
-                gx.template store<B ^ 1>(xs[(B ^ 1) % NBUF]);
-                gy.template store<B ^ 1>(ys[(B ^ 1) % NBUF]);
+            int ox, oy;
+            const int lim = box_origin(d, s0 + s, ox, oy);
+            gx.template load<B>(X + ox, lim);
+            gy.template load<B>(Y + oy, lim);
+        };
+        typedef std::integral_constant<int, 0> S0;
+        typedef std::integral_constant<int, 1> S1;
+        if constexpr (ONEBOX) {
+            // Gather and pack X, then Y, then multiply: nothing in flight across
+            // the MFMAs, one operand's values staged at a time, and the
+            // accumulators first written by the MFMAs (a contracted set in one
+            // box needs no more).  Plans with more boxes (a tile forced onto
+            // them) take the same steps box after box, copying item by item.
+            if (nsteps == 1) {
+                int ox, oy;
+                const int lim = box_origin(d, s0, ox, oy);
+                gx.template load<0>(X + ox, lim);
+                gx.template store<0>(xs[0]);
+                gy.template load<0>(Y + oy, lim);
+                gy.template store<0>(ys[0]);
+                __syncthreads();
+                w.template macro<GX::PITCH, GY::PITCH, true, 2>(xs[0], ys[0]);
+            } else {
+                w.zero();
+                for (uint32_t s = 0; s < nsteps; ++s) {
+                    int ox, oy;
+                    const int lim = box_origin(d, s0 + s, ox, oy);
+                    if (s > 0) __syncthreads();   // the MFMAs of the previous box are done
+                    gx.copy(X + ox, lim, xs[0]);
+                    gy.copy(Y + oy, lim, ys[0]);
+                    __syncthreads();
+                    w.template macro<GX::PITCH, GY::PITCH, false, 2>(xs[0], ys[0]);
+                }
+            }
+        } else if constexpr (PF == 1) {
+            if (nsteps > 0) {
+                fetch(S0(), 0);
+                gx.template store<0>(xs[0]);
+                gy.template store<0>(ys[0]);
             }
             __syncthreads();
-        };
-        if (nsteps > 0) {
-            fetch(S0(), 0);
-            if (nsteps > 1) fetch(S1(), 1);
-            gx.template store<0>(xs[0]);
-            gy.template store<0>(ys[0]);
+            for (uint32_t s = 0; s < nsteps; ++s) {
+                const int buf = NBUF == 2 ? (int)(s & 1) : 0;
+                const bool more = s + 1 < nsteps;
+                if (more) fetch(S0(), s + 1);
+                w.template macro<GX::PITCH, GY::PITCH>(xs[buf], ys[buf]);
+                if (NBUF == 1 && more) __syncthreads();   // the single buffer is free again
+                if (more) {
+                    gx.template store<0>(xs[NBUF == 2 ? buf ^ 1 : 0]);
+                    gy.template store<0>(ys[NBUF == 2 ? buf ^ 1 : 0]);
+                }
+                __syncthreads();
+            }
+        } else {
+            // One box: start the gathers of box s+2 into this stage's registers,
+            // run the MFMAs of box s from LDS buffer B, move box s+1's registers
+            // into the other buffer.
+            auto step = [&](auto stage, uint32_t s) {
+                constexpr int B = decltype(stage)::value;
+                if (s + 2 < nsteps) fetch(stage, s + 2);
+                w.template macro<GX::PITCH, GY::PITCH>(xs[B % NBUF], ys[B % NBUF]);
+                if (s + 1 < nsteps) {
+                    gx.template store<B ^ 1>(xs[(B ^ 1) % NBUF]);
+                    gy.template store<B ^ 1>(ys[(B ^ 1) % NBUF]);
+                }
+                __syncthreads();
+            };
+            if (nsteps > 0) {
+                fetch(S0(), 0);
+                if (nsteps > 1) fetch(S1(), 1);
+                gx.template store<0>(xs[0]);
+                gy.template store<0>(ys[0]);
+            }
+            __syncthreads();
+            for (uint32_t s = 0; s < nsteps; s += 2) {
+                step(S0(), s);
+                if (s + 1 < nsteps) step(S1(), s + 1);
+            }
         }
-        __syncthreads();
-        for (uint32_t s = 0; s < nsteps; s += 2) {
-            step(S0(), s);
-            if (s + 1 < nsteps) step(S1(), s + 1);
-        }
-    }
-    if (slices > 1) {
-        w.unpack_atomic(C, offCx, offCy, alpha);
-        return;
-    }
-    if constexpr (CORDER && WT::kVecC) {   // compiled only into the tiles that carry it
-        if (d.crun > 0 && d.cvec) {
-            const int y0 = ty * NT;
-            const int ylim = (int)min((int64_t)y0 + NT, d.sizeY);
-            unpack_c_order<T, MT, NTH>(w, C, panels, kPanels, offCx, offCy, y0, ylim, d.crun,
-                                       alpha, beta, tid);
+        if (atomic) {
+            w.unpack_atomic(C, offCx, offCy, alpha);
             return;
         }
+        if constexpr (CORDER && WT::kVecC) {   // compiled only into the tiles that carry it
+            if (d.crun > 0 && d.cvec) {
+                const int y0 = ty * NT;
+                const int ylim = (int)min((int64_t)y0 + NT, d.sizeY);
+                unpack_c_order<T, MT, NTH>(w, C, panels, kPanels, offCx, offCy, y0, ylim, d.crun,
+                                           alpha, beta, tid);
+                return;
+            }
+        }
+        w.template unpack<ONEBOX ? 2 : 1>(C, offCx, offCy, alpha, beta, d.cvec != 0);
+    };
+
+    if constexpr (TAIL) {
+        // Stream-K tail: workgroups below tailFull compute one whole tile
+        // each; every later one sums a run of tailLen consecutive boxes of the
+        // concatenated box sequences of the remaining tiles (the end of one
+        // tile and the start of the next, possibly) and adds its partial
+        // tiles into C with atomics (C of those tiles was set to beta * C
+        // beforehand).
+        const int bid = (int)blockIdx.x;
+        if (bid < d.tailFull) {
+            piece(bid, 0, (uint32_t)d.nsteps, false);
+            return;
+        }
+        const uint64_t nb = (uint64_t)d.nsteps;
+        const uint64_t total = (uint64_t)(ntiles - d.tailFull) * nb;
+        uint64_t pos = (uint64_t)(bid - d.tailFull) * (uint64_t)d.tailLen;
+        const uint64_t end = min(pos + (uint64_t)d.tailLen, total);
+        while (pos < end) {
+            const uint64_t t = pos / nb;
+            const uint32_t s0 = (uint32_t)(pos - t * nb);
+            const uint32_t n = (uint32_t)min(nb - s0, end - pos);
+            piece(d.tailFull + (int)t, s0, n, true);
+            pos += n;
+            __syncthreads();   // the next piece rewrites the tables and panels
+        }
+    } else {
+        // K slices: workgroup b computes slice b / tiles of tile tile0 + b % tiles
+        // (tiles = the tiles from tile0 on; tile0 > 0 for a pass that scales
+        // the tail tiles of a stream-K plan).
+        const int slices = d.kslices > 1 ? d.kslices : 1;
+        const int span = ntiles - d.tile0;
+        const int bid = (int)blockIdx.x;
+        const int slice = slices > 1 ? bid / span : 0;
+        const uint32_t s0 = (uint32_t)((uint64_t)d.nsteps * slice / slices);
+        const uint32_t n = (uint32_t)((uint64_t)d.nsteps * (slice + 1) / slices) - s0;
+        piece(d.tile0 + bid - slice * span, s0, n, slices > 1);
     }
-    w.template unpack<ONEBOX ? 2 : 1>(C, offCx, offCy, alpha, beta, d.cvec != 0);
 }
 
 // ---------------------------------------------------------------------------

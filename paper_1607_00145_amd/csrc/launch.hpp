@@ -41,13 +41,24 @@ hipError_t launch_one(const KDesc &d, const void *X, const void *Y, void *C, dou
     if (tiles == 0) return hipSuccess;
     const int threads = t.wm * t.wn * 64;
     if constexpr (KIND == 0) {
+        if ((unsigned)d.tile0 >= tiles) return hipSuccess;
         hipLaunchKernelGGL(
             (gett_macro_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.wpe, t.pf, t.nbuf, XM,
                                YM, t.onebox, t.corder>),
-            dim3(tiles * (unsigned)(d.kslices > 1 ? d.kslices : 1)), dim3(threads), 0, stream, d,
-            static_cast<const T *>(X),
-            static_cast<const T *>(Y), static_cast<T *>(C), static_cast<T>(alpha),
-            static_cast<T>(beta));
+            dim3((tiles - (unsigned)d.tile0) * (unsigned)(d.kslices > 1 ? d.kslices : 1)),
+            dim3(threads), 0, stream, d, static_cast<const T *>(X), static_cast<const T *>(Y),
+            static_cast<T *>(C), static_cast<T>(alpha), static_cast<T>(beta));
+    } else if constexpr (KIND == 3) {
+        if (d.tailFull < 0 || d.tailWgs < 1 || d.tailLen < 1 || (unsigned)d.tailFull >= tiles ||
+            (uint64_t)d.tailWgs * (uint64_t)d.tailLen <
+                (uint64_t)(tiles - (unsigned)d.tailFull) * (uint64_t)d.nsteps)
+            return hipErrorInvalidValue;   // the tail workgroups must cover every box
+        hipLaunchKernelGGL(
+            (gett_macro_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.wpe, t.pf, t.nbuf, XM,
+                               YM, t.onebox, t.corder, 1>),
+            dim3((unsigned)d.tailFull + (unsigned)d.tailWgs), dim3(threads), 0, stream, d,
+            static_cast<const T *>(X), static_cast<const T *>(Y), static_cast<T *>(C),
+            static_cast<T>(alpha), static_cast<T>(beta));
     } else {
         auto k = gett_stream_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.stream, XM, YM>;
         const unsigned grid = persistent_grid(k, threads, tiles);
@@ -63,10 +74,12 @@ template <typename T, int TI>
 LaunchFn pick_modes(int xm, int ym, int kind)
 {
     constexpr bool kStream = TileTable<T>::tiles[TI].stream != 0;
+    constexpr bool kTail = TileTable<T>::tiles[TI].tail != 0;
 #define GETT_CASE(a, b)                                                                       \
     if (xm == a && ym == b) {                                                                 \
         if (kind == 0) return &launch_one<T, TI, a, b, 0>;                                   \
-        if (kStream) return &launch_one<T, TI, a, b, kStream ? 1 : 0>;                       \
+        if (kind == 1 && kStream) return &launch_one<T, TI, a, b, kStream ? 1 : 0>;          \
+        if (kind == 3 && kTail) return &launch_one<T, TI, a, b, kTail ? 3 : 0>;              \
         return nullptr;                                                                       \
     }
     GETT_CASE(0, 0) GETT_CASE(0, 1) GETT_CASE(0, 2) GETT_CASE(0, 3) GETT_CASE(0, 4)

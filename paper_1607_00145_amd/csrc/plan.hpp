@@ -31,7 +31,8 @@ struct Analysis {
 // A kernel candidate: tile shape and kind, with the model's estimate.
 struct Candidate {
     int tile = 0, kind = 0;                 // kind 0: macro-kernel, 1: streaming kernel,
-                                            // 2: macro-kernel over K slices
+                                            // 2: macro-kernel over K slices,
+                                            // 3: stream-K tail kernel
     int slices = 1;                         // workgroups per tile (kind 2)
     double tMfma = 0, tMem = 0, cost = 0;   // seconds
 };
@@ -57,7 +58,8 @@ struct gett_plan_s {
     int tile;                // index into the tile table of the dtype
     int xmode, ymode;        // gather modes of the preferred kernel
     int kind;                // 0: macro-kernel, 1: persistent streaming kernel,
-                             // 2: macro-kernel over K slices (desc.kslices > 1)
+                             // 2: macro-kernel over K slices (desc.kslices > 1),
+                             // 3: stream-K tail kernel (desc.tailFull ...)
     std::vector<gett::Candidate> ranked;   // every candidate, best model estimate first
     // the arguments of gett_plan, kept to re-plan with another candidate
     std::string modes[3];
@@ -93,7 +95,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
                       const char *mB, const int64_t *eB, const int64_t *sB, uint32_t flags,
                       const Choice *force);
 
-// "macro", "stream" or "kslices" (Candidate::kind).
+// "macro", "stream", "kslices" or "tail" (Candidate::kind).
 const char *kind_name(int kind);
 // Launch table lookup (defined with the kernel instantiations).  kind 0: the
 // macro-kernel, 1: the persistent streaming kernel.

@@ -26,12 +26,13 @@ struct TileShape {
     int onebox;  // 1: no prefetch (each box gathered, packed and multiplied in turn),
                  // for contracted sets that fit one K box; fewer registers live at once
     int corder;  // 1: the kernel carries the C-order epilogue (unpack_c_order)
+    int tail;    // 1: also compiled as the stream-K tail kernel
 };
 
 constexpr TileShape kTilesF32[] = {
     {128, 128, 16, 2, 2, 4, 4, 1, 1, 2, 0, 0.75f, 0.61f, 0.0f, 0, 1},
     {64, 64, 16, 1, 1, 4, 4, 1, 1, 2, 0, 0.67f, 0.62f, 0.0f, 0, 1},
-    {128, 128, 16, 2, 2, 4, 4, 3, 1, 2, 2, 0.71f, 0.675f, 0.64f, 0, 1},
+    {128, 128, 16, 2, 2, 4, 4, 3, 1, 2, 2, 0.71f, 0.675f, 0.64f, 0, 1, 1},
     {64, 256, 16, 1, 4, 4, 4, 3, 1, 2, 2, 0.70f, 0.70f, 0.63f, 0, 1},
     {128, 128, 32, 2, 2, 4, 4, 1, 1, 2, 0, 0.806f, 0.61f, 0.0f, 0, 1},
     {64, 32, 32, 2, 2, 2, 1, 2, 2, 2, 0, 0.64f, 0.35f, 0.0f},
@@ -46,7 +47,7 @@ constexpr TileShape kTilesF64[] = {
     {64, 64, 16, 2, 2, 2, 2, 2, 2, 2, 0, 0.75f, 0.34f, 0.0f},
     {64, 128, 16, 2, 2, 2, 2, 2, 2, 2, 0, 0.785f, 0.34f, 0.0f},
     {128, 64, 16, 2, 2, 2, 2, 2, 2, 2, 0, 0.785f, 0.34f, 0.0f},
-    {96, 128, 16, 2, 2, 1, 2, 2, 2, 2, 0, 0.79f, 0.34f, 0.0f},
+    {96, 128, 16, 2, 2, 1, 2, 2, 2, 2, 0, 0.79f, 0.34f, 0.0f, 0, 0, 1},
     {128, 64, 24, 2, 2, 2, 2, 3, 1, 1, 0, 0.785f, 0.615f, 0.0f},
     {64, 128, 24, 1, 4, 2, 2, 3, 1, 1, 0, 0.775f, 0.59f, 0.0f},
     {64, 128, 24, 2, 2, 2, 2, 3, 1, 1, 0, 0.785f, 0.668f, 0.0f},
