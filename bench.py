@@ -289,6 +289,9 @@ def report_workload(w, dev, stream, runs, flush):
     rec["plan"]["tile"] = [p.plan["tile"]["mt"], p.plan["tile"]["nt"], p.plan["tile"]["kt"]]
     rec["plan"]["workgroups"] = p.plan["grid"]["workgroups"]
     rec["plan"]["kslices"] = p.plan["kslices"]
+    rec["plan"]["kernel"] = p.plan["kernel"]
+    if p.plan["kernel"] == "tail":
+        rec["plan"]["tail"] = p.plan["tail"]
     t = TtgtProblem(p)
     for _ in range(3):
         t.launch(stream)

@@ -203,6 +203,53 @@ static double tail_occupancy(const TileShape &c, double itemB)
     return std::max(1.0, std::min((double)c.wpe, std::floor(160.0 * 1024.0 / lds)));
 }
 
+// Time one CU takes, in units of one K box on a SIMD shared by two or more
+// wavefronts, to run `full` workgroups of `nb` boxes and then `tail`
+// workgroups of `len` boxes, `occ` of them resident at once (in that order:
+// the dispatcher deals workgroups in order of their index).  The resident
+// workgroups share the SIMDs evenly; a wavefront left alone on its SIMD runs
+// at 0.64 of the rate of two (measured on MI355X: it waits for its own
+// gathers and LDS reads).
+static double cu_time(int occ, int full, double nb, int tail, double len)
+{
+    std::vector<double> left;
+    int next = 0;
+    const int n = full + tail;
+    auto work = [&](int i) { return i < full ? nb : len; };
+    while (next < n && (int)left.size() < occ) left.push_back(work(next++));
+    double t = 0.0;
+    while (!left.empty()) {
+        const double w = (double)left.size();
+        const double rate = (left.size() >= 2 ? 1.0 : 0.64) / w;   // boxes per unit, each
+        const double step = *std::min_element(left.begin(), left.end());
+        t += step / rate;
+        std::vector<double> still;
+        for (double r : left)
+            if (r - step > 1e-9) still.push_back(r - step);
+        left.swap(still);
+        while (next < n && (int)left.size() < occ) left.push_back(work(next++));
+    }
+    return t;
+}
+
+// Stream-K tail shape for T tiles of nb boxes over G tail workgroups:
+// whole tiles for the complete rounds of G, the boxes of the rest in equal
+// runs; every tail workgroup gets boxes.
+struct TailShape {
+    int64_t full = 0, wgs = 0, len = 0;
+};
+static TailShape tail_shape(int64_t T, int64_t nb, int64_t G)
+{
+    TailShape s;
+    int64_t rem = T % G;
+    if (rem == 0) rem = std::min<int64_t>(G, T);
+    const int64_t boxes = rem * nb;
+    s.len = (boxes + std::min(G, boxes) - 1) / std::min(G, boxes);
+    s.full = T - rem;
+    s.wgs = (boxes + s.len - 1) / s.len;
+    return s;
+}
+
 namespace {
 
 const char *mode_name(int m)
@@ -595,43 +642,51 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
             }
             if (best.tile >= 0) ranked.push_back(best);
         }
-        // Stream-K tail: when the tiles do not fill a whole number of rounds
-        // of the workgroups resident at once (G = occupancy x 256 CUs), the
-        // SIMDs that get one wavefront more set the time, and those left
-        // with one wavefront run it slower than two together.  Instead, the
-        // whole rounds run as usual and the boxes of the remaining r tiles
-        // are dealt in equal runs to G more workgroups, which add their
-        // partial tiles into C with atomics (about r + G tile-sized
-        // read-modify-writes, which add about the time of a 6.8 TB/s stream
-        // of their reads and writes: measured on MI355X, where they overlap
-        // the MFMAs of other workgroups) after one pass that sets those
-        // tiles to beta * C.  Priced as the balanced load of every SIMD plus
-        // two boxes of set-up per piece, the atomics, and the scaling pass's
-        // launch.
-        const double occ = tail_occupancy(c, itemB);
-        const double G = occ * 256.0;
+        // Stream-K tail: when the tiles do not fill the CUs a whole number of
+        // times, the CUs that get one tile more set the time, and a wavefront
+        // left alone on its SIMD runs slower than two together.  Instead, the
+        // tiles of the complete rounds of G = 256 g workgroups run whole and
+        // the boxes of the remaining ones are dealt in equal runs to G more
+        // workgroups (g = 1 .. the tile's occupancy; the best is kept), which
+        // add their partial tiles into C with atomics after one pass that
+        // sets those tiles to beta * C.  Priced by cu_time for the busiest CU
+        // (two boxes of set-up per piece), the atomics (about r + G
+        // tile-sized read-modify-writes, which add about the time of a
+        // 6.8 TB/s stream of their reads and writes: measured on MI355X,
+        // where they overlap the MFMAs of other workgroups) and the scaling
+        // pass's launch.
         const double ntile = tx * ty;
-        const double rem = std::fmod(ntile, G);
         if (c.tail && !(flags & GETT_FLAG_DETERMINISTIC) && !an.emptyC && wpt >= 4 &&
-            b.nsteps >= 16 && ntile > 256.0 && rem > 0.0) {
-            const double nb = (double)b.nsteps;
-            const double len = std::ceil(rem * nb / G);
-            const double pieces = std::ceil(len / nb) + 1.0;
-            const double boxes = occ * (((ntile - rem) / G) * nb + len + 2.0 * pieces);
+            b.nsteps >= 16 && ntile > 256.0 && std::fmod(ntile, 256.0) > 0.0) {
+            const int occ = (int)tail_occupancy(c, itemB);
             const double boxFlops = (double)(c.mt / c.wm) * (c.nt / c.wn) * c.kt * 2.0;
-            const double tM = boxes * std::ceil(wpt / 4.0) * boxFlops / (peakSimd * c.eff) *
-                              (kSplitAhead && c.nbuf == 1 ? 1.4 : 1.0);
+            const double boxTime = std::ceil(wpt / 4.0) * boxFlops / (peakSimd * c.eff) *
+                                   (kSplitAhead && c.nbuf == 1 ? 1.4 : 1.0);
             const double tMem = (bytesC + bytesX + bytesY +
                                  0.05 * (bytesX * (ty - 1) + bytesY * (tx - 1))) /
                                 (8.0e12 * c.bw);
-            const double tAtomic = (rem + G) * c.mt * c.nt * itemB * 2.0 / 6.8e12;
-            Candidate cd;
-            cd.tile = t;
-            cd.kind = 3;
-            cd.tMfma = tM;
-            cd.tMem = tMem;
-            cd.cost = bound(std::max(tM, tMem), tChain) + tAtomic + 3.0e-6;
-            ranked.push_back(cd);
+            Candidate best;
+            best.tile = -1;
+            for (int g = 1; g <= occ; ++g) {
+                const TailShape ts = tail_shape((int64_t)ntile, b.nsteps, 256 * (int64_t)g);
+                const double pieces = std::ceil((double)ts.len / b.nsteps) + 1.0;
+                const double units = cu_time(occ, (int)std::ceil(ts.full / 256.0), (double)b.nsteps,
+                                             (int)std::ceil(ts.wgs / 256.0),
+                                             (double)ts.len + 2.0 * pieces);
+                const double tM = units * boxTime;
+                const double tAtomic =
+                    (double)(ntile - ts.full + ts.wgs) * c.mt * c.nt * itemB * 2.0 / 6.8e12;
+                const double cost = bound(std::max(tM, tMem), tChain) + tAtomic + 3.0e-6;
+                if (best.tile < 0 || cost < best.cost) {
+                    best.tile = t;
+                    best.kind = 3;
+                    best.slices = 256 * g;
+                    best.tMfma = tM;
+                    best.tMem = tMem;
+                    best.cost = cost;
+                }
+            }
+            if (best.tile >= 0) ranked.push_back(best);
         }
     }
     std::stable_sort(ranked.begin(), ranked.end(),
@@ -907,20 +962,14 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     d.tile0 = 0;
     d.tailFull = d.tailWgs = d.tailLen = 0;
     if (kind == 3 && !an.emptyC) {
-        // whole tiles for the complete rounds of the workgroups resident at
-        // once, the boxes of the rest in equal runs over as many more (tuning
-        // hook: GETT_TAIL_WGS workgroups share the tail instead)
-        int64_t wgs = (int64_t)tail_occupancy(ts, dtype == GETT_FLOAT32 ? 4.0 : 8.0) * 256;
+        // the model's number of tail workgroups (256 when the tail was forced
+        // on a plan the model did not rank it for; tuning hook: GETT_TAIL_WGS)
+        int64_t wgs = pick.kind == 3 && pick.slices > 1 ? pick.slices : 256;
         if (const char *tw = getenv("GETT_TAIL_WGS")) wgs = std::max<int64_t>(1, atoll(tw));
-        const int64_t T = (int64_t)tilesX * tilesY;
-        int64_t rem = T % wgs;
-        if (rem == 0) rem = std::min<int64_t>(wgs, T);
-        const int64_t nb = std::max<int64_t>(nsteps, 1);
-        const int64_t boxes = rem * nb;
-        const int64_t len = (boxes + std::min(wgs, boxes) - 1) / std::min(wgs, boxes);
-        d.tailFull = (int32_t)(T - rem);
-        d.tailLen = (int32_t)len;
-        d.tailWgs = (int32_t)((boxes + len - 1) / len);   // every one of them gets boxes
+        const TailShape tsh = tail_shape((int64_t)tilesX * tilesY, std::max<int64_t>(nsteps, 1), wgs);
+        d.tailFull = (int32_t)tsh.full;
+        d.tailWgs = (int32_t)tsh.wgs;
+        d.tailLen = (int32_t)tsh.len;
     }
     if (!an.emptyC && tilesX * tilesY * kslices * ts.wm * ts.wn * 64 >= (int64_t)UINT32_MAX)
         return GETT_ERROR_NOT_SUPPORTED;
@@ -975,6 +1024,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         o << (i ? "," : "") << "{\"tile\":" << ranked[i].tile << ",\"kind\":\""
           << kind_name(ranked[i].kind) << "\"";
         if (ranked[i].kind == 2) o << ",\"kslices\":" << ranked[i].slices;
+        if (ranked[i].kind == 3) o << ",\"tail_workgroups\":" << ranked[i].slices;
         o << ",\"model_us\":" << ranked[i].cost * 1e6 << "}";
     }
     o << "]";

@@ -33,7 +33,8 @@ struct Candidate {
     int tile = 0, kind = 0;                 // kind 0: macro-kernel, 1: streaming kernel,
                                             // 2: macro-kernel over K slices,
                                             // 3: stream-K tail kernel
-    int slices = 1;                         // workgroups per tile (kind 2)
+    int slices = 1;                         // workgroups per tile (kind 2), tail
+                                            // workgroups (kind 3)
     double tMfma = 0, tMem = 0, cost = 0;   // seconds
 };
 

@@ -48,9 +48,9 @@ constexpr TileShape kTilesF64[] = {
     {64, 128, 16, 2, 2, 2, 2, 2, 2, 2, 0, 0.785f, 0.34f, 0.0f},
     {128, 64, 16, 2, 2, 2, 2, 2, 2, 2, 0, 0.785f, 0.34f, 0.0f},
     {96, 128, 16, 2, 2, 1, 2, 2, 2, 2, 0, 0.79f, 0.34f, 0.0f, 0, 0, 1},
-    {128, 64, 24, 2, 2, 2, 2, 3, 1, 1, 0, 0.785f, 0.615f, 0.0f},
+    {128, 64, 24, 2, 2, 2, 2, 3, 1, 1, 0, 0.785f, 0.615f, 0.0f, 0, 0, 1},
     {64, 128, 24, 1, 4, 2, 2, 3, 1, 1, 0, 0.775f, 0.59f, 0.0f},
-    {64, 128, 24, 2, 2, 2, 2, 3, 1, 1, 0, 0.785f, 0.668f, 0.0f},
+    {64, 128, 24, 2, 2, 2, 2, 3, 1, 1, 0, 0.785f, 0.668f, 0.0f, 0, 0, 1},
     {64, 32, 16, 2, 2, 2, 1, 2, 2, 2, 0, 0.70f, 0.485f, 0.0f},
     {32, 64, 16, 2, 2, 1, 2, 2, 2, 2, 0, 0.71f, 0.49f, 0.0f},
     {64, 128, 24, 2, 2, 2, 2, 4, 1, 1, 0, 0.785f, 0.70f, 0.0f, 1},
