@@ -180,6 +180,43 @@ class LogProblem:
             self.g.gett_log_destroy(self.h)
 
 
+class SelectProblem:
+    """The same workload run through method selection (Sec. 6): the library
+    times GETT, TTGT and LoG on the problem's buffers and keeps the fastest."""
+
+    def __init__(self, p: Problem, stream, max_candidates):
+        import torch
+        g, w = p.g, p.w
+        self.p, self.g = p, g
+        dt = g.GETT_FLOAT32 if w.dtype == "f32" else g.GETT_FLOAT64
+        st, self.h = g.gett_select_plan(dt, w.modes_C, w.shape("C"), None, w.modes_A,
+                                        w.shape("A"), None, w.modes_B, w.shape("B"), None, 0, -1)
+        if st != 0:
+            raise RuntimeError(f"gett_select_plan: {g.gett_status_string(st)}")
+        _, self.nws = g.gett_select_workspace_size(self.h)
+        self.ws = torch.empty(max(self.nws, 1), dtype=torch.uint8, device=p.dev)
+        scratch = torch.empty_like(p.C)
+        st = g.gett_select_tune(self.h, max_candidates, p.A.data_ptr(), p.B.data_ptr(),
+                                scratch.data_ptr(), self.ws.data_ptr(), self.nws,
+                                stream.cuda_stream)
+        del scratch
+        if st != 0:
+            raise RuntimeError(f"gett_select_tune: {g.gett_status_string(st)}")
+        self.plan = json.loads(g.gett_select_describe(self.h))
+
+    def launch(self, stream):
+        p = self.p
+        st = self.g.gett_select_contract(self.h, p.w.alpha, p.A.data_ptr(), p.B.data_ptr(),
+                                         p.w.beta, p.C.data_ptr(), self.ws.data_ptr(), self.nws,
+                                         stream.cuda_stream)
+        if st != 0:
+            raise RuntimeError(f"gett_select_contract: {self.g.gett_status_string(st)}")
+
+    def close(self):
+        self.g.gett_select_destroy(self.h)
+        del self.ws
+
+
 def time_log(p: Problem, stream, runs, flush):
     """Cold minimum (ms) of the LoG run of a problem, or None when LoG does not apply."""
     lp = LogProblem(p)
@@ -425,6 +462,13 @@ def sweep_run(sweep, dev, stream, runs, flush, max_candidates):
         tx = min(time_launches(lambda: t.launch(stream), runs, stream, flush))
         t.close()
         tl, _ = time_log(p, stream, runs, flush)
+        # method selection: its GETT plan starts from the tuned choice above
+        sp = SelectProblem(p, stream, 0)
+        for _ in range(2):
+            sp.launch(stream)
+        ts = min(time_launches(lambda: sp.launch(stream), runs, stream, flush))
+        smethod = sp.plan["method"]
+        sp.close()
         p.close()
         del p
         tg = time_gemm(M, N, K, w, dev, stream, runs, flush)
@@ -444,7 +488,9 @@ def sweep_run(sweep, dev, stream, runs, flush, max_candidates):
                "log_gflops": round(flops / (tl * 1e-3) / 1e9, 1) if tl else None,
                "gemm_ms": round(tg, 5),
                "gemm_gflops": round(flops / (tg * 1e-3) / 1e9, 1),
-               "vs_equal_size_gemm": round(tg / best, 4)}
+               "vs_equal_size_gemm": round(tg / best, 4),
+               "select_method": smethod, "select_ms": round(ts, 5),
+               "select_vs_equal_size_gemm": round(tg / ts, 4)}
         log(f"[sweep] {w.name}: model {tm*1e3:.1f} us, tuned {tt*1e3:.1f} us, "
             f"ttgt {tx*1e3:.1f} us, log {tl*1e3 if tl else float('nan'):.1f} us, "
             f"gemm {tg*1e3:.1f} us")

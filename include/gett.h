@@ -321,6 +321,88 @@ gett_status_t gett_log_destroy(gett_log_plan_t plan);
  * gett_log_destroy.  "" for NULL. */
 const char *gett_log_describe(const gett_log_plan_t plan);
 
+/* ------------------------------------------------------------------------
+ * Method selection (Sec. 6): the fastest of GETT, TTGT and LoG
+ *
+ * The paper's code generator times GETT, TTGT and LoG candidates for a
+ * contraction and keeps the fastest (Sec. 6, stages 2-6; the best-of-three
+ * results of Sec. 7).  A selection plan holds this library's three plans
+ * for one contraction and runs the one chosen.
+ * ------------------------------------------------------------------------ */
+
+typedef enum { GETT_METHOD_GETT = 0, GETT_METHOD_TTGT = 1, GETT_METHOD_LOG = 2 } gett_method_t;
+
+typedef struct gett_select_plan_s *gett_select_plan_t;
+
+/*
+ * gett_select_plan -- plan all three methods (host only).
+ *
+ * Arguments as for gett_plan (flags apply to the GETT plan), plus
+ *   max_workspace_bytes  the largest workspace TTGT may use (Table II,
+ *                        --maxWorkspace); negative: no limit.
+ *
+ * The GETT plan must succeed (its errors are returned).  TTGT is a candidate
+ * when gett_ttgt_plan succeeds within the cap, LoG when gett_log_plan does;
+ * their refusals are not errors.  The method starts as GETT (no workspace)
+ * until gett_select_tune or gett_select_force changes it.
+ */
+gett_status_t gett_select_plan(gett_select_plan_t *plan, gett_dtype_t dtype,
+                               const char *modes_C, const int64_t *extent_C,
+                               const int64_t *stride_C, const char *modes_A,
+                               const int64_t *extent_A, const int64_t *stride_A,
+                               const char *modes_B, const int64_t *extent_B,
+                               const int64_t *stride_B, uint32_t flags,
+                               int64_t max_workspace_bytes);
+
+/* gett_select_workspace_size -- bytes of device workspace the TTGT candidate
+ * needs (0 without one, or when it transposes nothing). */
+gett_status_t gett_select_workspace_size(const gett_select_plan_t plan, uint64_t *bytes);
+
+/*
+ * gett_select_tune -- time the candidates and keep the fastest.
+ *
+ * Runs gett_plan_tune(max_candidates) on the GETT plan (max_candidates 0:
+ * the GETT plan as gett_plan made it, a remembered tuned choice included),
+ * then times each available method (one untimed and three timed launches
+ * with alpha 1, beta 0, so C is overwritten) on A, B, C and `stream`, and
+ * sets the plan's method to the fastest.  TTGT is timed only when
+ * `workspace` holds at least gett_select_workspace_size() bytes.
+ * Synchronises with `stream`.  Errors as for the methods' contract calls;
+ * GETT_ERROR_INVALID_VALUE for max_candidates < 0.  Not safe to call
+ * concurrently on one plan.
+ */
+gett_status_t gett_select_tune(gett_select_plan_t plan, int max_candidates, const void *A,
+                               const void *B, void *C, void *workspace,
+                               uint64_t workspace_bytes, void *stream);
+
+/* gett_select_force -- use `method` (GETT_ERROR_NOT_SUPPORTED when that
+ * method is not a candidate for this contraction). */
+gett_status_t gett_select_force(gett_select_plan_t plan, gett_method_t method);
+
+/* gett_select_method -- the method gett_select_contract runs. */
+gett_status_t gett_select_method(const gett_select_plan_t plan, gett_method_t *method);
+
+/*
+ * gett_select_contract -- C <- alpha * A * B + beta * C by the plan's method.
+ *
+ * Arguments and pointer rules as for gett_contract; `workspace` /
+ * `workspace_bytes` as for gett_ttgt_contract and used only when the method
+ * is TTGT.  Asynchronous on `stream`.
+ */
+gett_status_t gett_select_contract(const gett_select_plan_t plan, double alpha, const void *A,
+                                   const void *B, double beta, void *C, void *workspace,
+                                   uint64_t workspace_bytes, void *stream);
+
+/* gett_select_destroy -- free a selection plan and its three plans.  NULL is
+ * accepted and ignored. */
+gett_status_t gett_select_destroy(gett_select_plan_t plan);
+
+/* gett_select_describe -- the chosen method, the available candidates, the
+ * workspace and the measured milliseconds per launch (null where not timed)
+ * as a JSON object; valid until the next call that changes the plan.  ""
+ * for NULL. */
+const char *gett_select_describe(const gett_select_plan_t plan);
+
 #ifdef __cplusplus
 }
 #endif

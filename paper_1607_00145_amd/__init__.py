@@ -28,6 +28,9 @@ GETT_FLAG_SCALAR = 2
 GETT_FLAG_NO_SPLIT = 4
 GETT_FLAG_DETERMINISTIC = 8
 GETT_MAX_RANK = 12
+GETT_METHOD_GETT = 0
+GETT_METHOD_TTGT = 1
+GETT_METHOD_LOG = 2
 GETT_SUCCESS = 0
 GETT_ERROR_INVALID_VALUE = 1
 GETT_ERROR_INVALID_INDICES = 2
@@ -104,6 +107,29 @@ def load_library() -> ctypes.CDLL:
     lib.gett_log_destroy.argtypes = [ctypes.c_void_p]
     lib.gett_log_describe.restype = ctypes.c_char_p
     lib.gett_log_describe.argtypes = [ctypes.c_void_p]
+    lib.gett_select_plan.restype = ctypes.c_int
+    lib.gett_select_plan.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int,
+                                     ctypes.c_char_p, i64p, i64p, ctypes.c_char_p, i64p, i64p,
+                                     ctypes.c_char_p, i64p, i64p, ctypes.c_uint32,
+                                     ctypes.c_int64]
+    lib.gett_select_workspace_size.restype = ctypes.c_int
+    lib.gett_select_workspace_size.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_uint64)]
+    lib.gett_select_tune.restype = ctypes.c_int
+    lib.gett_select_tune.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
+                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                     ctypes.c_uint64, ctypes.c_void_p]
+    lib.gett_select_force.restype = ctypes.c_int
+    lib.gett_select_force.argtypes = [ctypes.c_void_p, ctypes.c_int]
+    lib.gett_select_method.restype = ctypes.c_int
+    lib.gett_select_method.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int)]
+    lib.gett_select_contract.restype = ctypes.c_int
+    lib.gett_select_contract.argtypes = [ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p,
+                                         ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p,
+                                         ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p]
+    lib.gett_select_destroy.restype = ctypes.c_int
+    lib.gett_select_destroy.argtypes = [ctypes.c_void_p]
+    lib.gett_select_describe.restype = ctypes.c_char_p
+    lib.gett_select_describe.argtypes = [ctypes.c_void_p]
     lib.gett_status_string.restype = ctypes.c_char_p
     lib.gett_status_string.argtypes = [ctypes.c_int]
     lib.gett_plan_describe.restype = ctypes.c_char_p
@@ -218,6 +244,60 @@ def gett_log_destroy(plan) -> int:
 
 def gett_log_describe(plan) -> str:
     return load_library().gett_log_describe(plan).decode()
+
+
+def gett_select_plan(dtype: int, modes_C: str, extent_C, stride_C, modes_A: str, extent_A,
+                     stride_A, modes_B: str, extent_B, stride_B, flags: int = 0,
+                     max_workspace_bytes: int = -1):
+    """Returns (status, selection plan handle or None)."""
+    lib = load_library()
+    h = ctypes.c_void_p()
+    st = lib.gett_select_plan(ctypes.byref(h), int(dtype),
+                              modes_C.encode(), _arr(extent_C), _arr(stride_C),
+                              modes_A.encode(), _arr(extent_A), _arr(stride_A),
+                              modes_B.encode(), _arr(extent_B), _arr(stride_B),
+                              int(flags), int(max_workspace_bytes))
+    return st, (h.value if st == 0 else None)
+
+
+def gett_select_workspace_size(plan):
+    """Returns (status, bytes)."""
+    n = ctypes.c_uint64()
+    st = load_library().gett_select_workspace_size(plan, ctypes.byref(n))
+    return st, int(n.value)
+
+
+def gett_select_tune(plan, max_candidates: int, A: int, B: int, C: int, workspace: int,
+                     workspace_bytes: int, stream: int = 0) -> int:
+    return load_library().gett_select_tune(plan, int(max_candidates), A or None, B or None,
+                                           C or None, workspace or None, int(workspace_bytes),
+                                           stream or None)
+
+
+def gett_select_force(plan, method: int) -> int:
+    return load_library().gett_select_force(plan, int(method))
+
+
+def gett_select_method(plan):
+    """Returns (status, method)."""
+    m = ctypes.c_int()
+    st = load_library().gett_select_method(plan, ctypes.byref(m))
+    return st, int(m.value)
+
+
+def gett_select_contract(plan, alpha: float, A: int, B: int, beta: float, C: int, workspace: int,
+                         workspace_bytes: int, stream: int = 0) -> int:
+    return load_library().gett_select_contract(plan, float(alpha), A or None, B or None,
+                                               float(beta), C or None, workspace or None,
+                                               int(workspace_bytes), stream or None)
+
+
+def gett_select_destroy(plan) -> int:
+    return load_library().gett_select_destroy(plan)
+
+
+def gett_select_describe(plan) -> str:
+    return load_library().gett_select_describe(plan).decode()
 
 
 def gett_status_string(status: int) -> str:

@@ -30,7 +30,10 @@ def test_library_exports_every_declared_symbol():
                             "gett_status_string", "gett_plan_describe", "gett_transpose",
                             "gett_ttgt_plan", "gett_ttgt_workspace_size", "gett_ttgt_contract",
                             "gett_ttgt_destroy", "gett_ttgt_describe", "gett_log_plan",
-                            "gett_log_contract", "gett_log_destroy", "gett_log_describe"])
+                            "gett_log_contract", "gett_log_destroy", "gett_log_describe",
+                            "gett_select_plan", "gett_select_workspace_size", "gett_select_tune",
+                            "gett_select_force", "gett_select_method", "gett_select_contract",
+                            "gett_select_destroy", "gett_select_describe"])
     for n in names:
         assert hasattr(lib, n), n
     out = subprocess.run(["nm", "-D", "--defined-only", g.LIB_PATH], capture_output=True,
