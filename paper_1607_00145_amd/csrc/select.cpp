@@ -32,7 +32,10 @@ struct gett_select_plan_s {
 
 namespace {
 
-const char *method_name(int m) { return m == GETT_METHOD_TTGT ? "ttgt" : m == GETT_METHOD_LOG ? "log" : "gett"; }
+const char *method_name(int m)
+{
+    return m == GETT_METHOD_TTGT ? "ttgt" : m == GETT_METHOD_LOG ? "log" : "gett";
+}
 
 bool available(const gett_select_plan_s &p, gett_method_t m)
 {
@@ -65,7 +68,8 @@ gett_status_t launch(const gett_select_plan_s &p, gett_method_t m, double alpha,
 {
     switch (m) {
     case GETT_METHOD_GETT: return gett_contract(p.gett, alpha, A, B, beta, C, stream);
-    case GETT_METHOD_TTGT: return gett_ttgt_contract(p.ttgt, alpha, A, B, beta, C, ws, wsBytes, stream);
+    case GETT_METHOD_TTGT:
+        return gett_ttgt_contract(p.ttgt, alpha, A, B, beta, C, ws, wsBytes, stream);
     case GETT_METHOD_LOG: return gett_log_contract(p.log, alpha, A, B, beta, C, stream);
     }
     return GETT_ERROR_INVALID_VALUE;
@@ -143,7 +147,8 @@ gett_status_t gett_select_tune(gett_select_plan_t plan, int max_candidates, cons
         const gett_method_t mm = (gett_method_t)m;
         if (!available(p, mm)) continue;
         // TTGT only with a workspace of its size
-        if (mm == GETT_METHOD_TTGT && p.workspace > 0 && (!workspace || workspace_bytes < p.workspace))
+        if (mm == GETT_METHOD_TTGT && p.workspace > 0 &&
+            (!workspace || workspace_bytes < p.workspace))
             continue;
         // one untimed launch, then three timed (alpha 1, beta 0: C is overwritten)
         st = launch(p, mm, 1.0, A, B, 0.0, C, workspace, workspace_bytes, stream);

@@ -1,8 +1,9 @@
 """gett_contract under HIP graph capture (serving loops replay one captured
-contraction): a plain plan, a plan over K slices (two kernels, the beta pass
-first) and an alpha = 0 call, each captured once and replayed several times
+contraction): a plain plan, a plan over K slices and one with a stream-K
+tail (two kernels each, the beta pass first) and an alpha = 0 call, each
+captured once and replayed several times
 with eager work between the replays; every replay must equal the eager
-result bit for bit (integer-valued inputs make the sliced sums exact)."""
+result bit for bit (integer-valued inputs make the atomic sums exact)."""
 import json
 
 import numpy as np
@@ -13,11 +14,15 @@ import paper_1607_00145_amd as g
 pytestmark = pytest.mark.gpu
 
 CASES = {
-    # (modes C, A, B), extents, forced K slices (None: the model's plan)
-    "plain": (("a,b,c,d", "a,e,b", "e,d,c"), {"a": 40, "b": 36, "c": 50, "d": 44, "e": 16}, None),
-    "kslices": (("a,b", "a,c,d", "d,b,c"), {"a": 96, "b": 94, "c": 94, "d": 96}, None),
-    "kslices_forced": (("a,b,c", "a,k,c", "k,b"), {"a": 33, "b": 47, "c": 5, "k": 600}, "8"),
+    # (modes C, A, B), extents, environment of the plan (forced choices)
+    "plain": (("a,b,c,d", "a,e,b", "e,d,c"), {"a": 40, "b": 36, "c": 50, "d": 44, "e": 16}, {}),
+    "kslices": (("a,b", "a,c,d", "d,b,c"), {"a": 96, "b": 94, "c": 94, "d": 96}, {}),
+    "kslices_forced": (("a,b,c", "a,k,c", "k,b"), {"a": 33, "b": 47, "c": 5, "k": 600},
+                       {"GETT_FORCE_KSLICES": "8"}),
+    "tail_forced": (("a,b", "a,k", "k,b"), {"a": 300, "b": 290, "k": 333},
+                    {"GETT_FORCE_KIND": "3", "GETT_TAIL_WGS": "5"}),
 }
+TAIL_TILE = {np.float32: "2", np.float64: "8"}
 
 
 @pytest.mark.parametrize("dtype", [np.float32, np.float64])
@@ -25,9 +30,11 @@ CASES = {
 @pytest.mark.parametrize("name", list(CASES))
 def test_graph_replay_matches_eager(gpu, monkeypatch, name, alpha, beta, dtype):
     import torch
-    modes, ext, slices = CASES[name]
-    if slices:
-        monkeypatch.setenv("GETT_FORCE_KSLICES", slices)
+    modes, ext, env = CASES[name]
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
+    if name.startswith("tail"):
+        monkeypatch.setenv("GETT_FORCE_TILE", TAIL_TILE[dtype])
     sp = lambda m: m.split(",")
     shp = lambda m: [ext[x] for x in sp(m)]
     tdt = torch.float32 if dtype == np.float32 else torch.float64
@@ -45,6 +52,8 @@ def test_graph_replay_matches_eager(gpu, monkeypatch, name, alpha, beta, dtype):
         d = json.loads(g.gett_plan_describe(h))
         if name.startswith("kslices"):
             assert d["kslices"] > 1
+        if name.startswith("tail"):
+            assert d["kernel"] == "tail" and d["tail"]["full_tiles"] > 0
         # eager reference
         C = C0.clone()
         assert g.gett_contract(h, alpha, A.data_ptr(), B.data_ptr(), beta, C.data_ptr(),
