@@ -115,6 +115,66 @@ __device__ __forceinline__ int box_origin(const KDesc &d, uint32_t s, int &ox, i
     return d.extK[d.kj] - blk * d.tj;
 }
 
+// Origins of consecutive K boxes without a division per box: the block
+// along index kj advances by one; when it wraps, the first later contracted
+// index advances (extent and strides held in registers), and only when that
+// one wraps too is the origin decomposed afresh by box_origin.  Any box may
+// be asked for; consecutive ones cost a few scalar additions.
+struct BoxWalker {
+    uint32_t cur;        // box whose origin is held
+    int ox, oy, lim;     // its origins in X and Y and valid positions along kj
+    int blk, c1;         // its block along kj and value of index kj + 1
+    int nblk, e1;        // blocks along kj; extent of index kj + 1 (0: none)
+    int bx, by;          // origin step of one block along kj in X and Y
+    int sx1, sy1;        // strides of index kj + 1 in X and Y
+    int ek, tj;          // extent of index kj and its block length
+
+    __device__ __forceinline__ void reset(const KDesc &d, uint32_t s)
+    {
+        cur = s;
+        lim = box_origin(d, s, ox, oy);
+        blk = (int)(s % (uint32_t)nblk);
+        c1 = e1 > 0 ? (int)((s / (uint32_t)nblk) % (uint32_t)e1) : 0;
+    }
+    __device__ __forceinline__ void init(const KDesc &d, uint32_t s)
+    {
+        nblk = d.nblk > 0 ? d.nblk : 1;
+        tj = d.tj;
+        ek = d.extK[d.kj];
+        bx = d.tj * (int)d.strXk[d.kj];
+        by = d.tj * (int)d.strYk[d.kj];
+        const bool later = d.kj + 1 < d.nk;
+        e1 = later ? d.extK[d.kj + 1] : 0;
+        sx1 = later ? (int)d.strXk[d.kj + 1] : 0;
+        sy1 = later ? (int)d.strYk[d.kj + 1] : 0;
+        reset(d, s);
+    }
+    // origin of box s (returns the valid positions along kj)
+    __device__ __forceinline__ int at(const KDesc &d, uint32_t s, int &x, int &y)
+    {
+        if (s == cur + 1) {
+            cur = s;
+            if (++blk < nblk) {
+                ox += bx;
+                oy += by;
+                lim -= tj;
+            } else if (++c1 < e1) {
+                blk = 0;
+                ox += sx1 - (nblk - 1) * bx;
+                oy += sy1 - (nblk - 1) * by;
+                lim = ek;
+            } else {
+                reset(d, s);
+            }
+        } else if (s != cur) {
+            reset(d, s);
+        }
+        x = ox;
+        y = oy;
+        return lim;
+    }
+};
+
 // Per-thread description of the part of one operand tile it gathers.  Item
 // `it` of thread `tid` is element (or 16-byte vector) tid + it * NTH of the
 // tile in the mode's order; items past the tile's end are idle.
@@ -443,11 +503,54 @@ struct WaveTile {
     // FIRST: acc = X~ * Y~ (the accumulators need no zeroing beforehand).
     // KU > 0 unrolls the MFMA steps KU at a time, which bounds how many LDS
     // reads the compiler hoists ahead of the MFMAs (registers).
-    template <int PX, int PY, bool FIRST = false, int KU = 0>
+    // PIPE: the fragments of step ks + 1 are read into a second register set
+    // while the MFMAs of step ks are issued (scheduling groups interleave
+    // them), so one wavefront alone on its SIMD does not wait for LDS between
+    // steps.
+    template <int PX, int PY, bool FIRST = false, int KU = 0, bool PIPE = false>
     __device__ __forceinline__ void macro(const T *xs, const T *ys)
     {
         const T *xt = xs + wm * WTM + RX * l16;
         const T *yt = ys + wn * WTN + RY * l16;
+        if constexpr (PIPE) {
+            typename XV::type av[2][RB / RX];
+            typename YV::type bv[2][CB / RY];
+            auto read = [&](int ks, int buf) {
+                const int k = 4 * ks + g;
+#pragma unroll
+                for (int gi = 0; gi < RB / RX; ++gi)
+                    av[buf][gi] =
+                        *reinterpret_cast<const typename XV::type *>(xt + k * PX + gi * 16 * RX);
+#pragma unroll
+                for (int gj = 0; gj < CB / RY; ++gj)
+                    bv[buf][gj] =
+                        *reinterpret_cast<const typename YV::type *>(yt + k * PY + gj * 16 * RY);
+            };
+            constexpr int NREAD = RB / RX + CB / RY;   // LDS reads per step
+            constexpr int NMFMA = RB * CB;             // MFMAs per step
+            read(0, 0);
+#pragma unroll
+            for (int ks = 0; ks < KT / 4; ++ks) {
+                if (ks + 1 < KT / 4) read(ks + 1, (ks + 1) & 1);
+#pragma unroll
+                for (int a = 0; a < RB; ++a)
+#pragma unroll
+                    for (int b = 0; b < CB; ++b)
+                        acc[a][b] = mfma16x16x4(XV::at(av[ks & 1][a / RX], a % RX),
+                                                YV::at(bv[ks & 1][b / RY], b % RY),
+                                                FIRST && ks == 0 ? accv{} : acc[a][b]);
+                // interleave: each of the next step's LDS reads after a
+                // share of this step's MFMAs
+                if (ks + 1 < KT / 4) {
+#pragma unroll
+                    for (int r = 0; r < NREAD; ++r) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, NMFMA / NREAD, 0);
+                        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                    }
+                }
+            }
+            return;
+        }
         constexpr int UN = KU > 0 ? KU : KT / 4;
 #pragma unroll UN
         for (int ks = 0; ks < KT / 4; ++ks) {
@@ -737,10 +840,14 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
         gy.setup(tid, rowY, kY, kco, d.yscalar_kfast, d.yes,
                  YMODE == kGatherScalar && d.yperm > 0 ? permY : nullptr);
         if (!ONEBOX) w.zero();
+        BoxWalker walk;
+        if constexpr (!ONEBOX) {
+            if (nsteps > 0) walk.init(d, s0);   // fetch runs only when there are boxes
+        }
         auto fetch = [&](auto stage, uint32_t s) {
             constexpr int B = decltype(stage)::value;
             int ox, oy;
-            const int lim = box_origin(d, s0 + s, ox, oy);
+            const int lim = walk.at(d, s0 + s, ox, oy);
             gx.template load<B>(X + ox, lim);
             gy.template load<B>(Y + oy, lim);
         };
@@ -784,7 +891,10 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
                 const int buf = NBUF == 2 ? (int)(s & 1) : 0;
                 const bool more = s + 1 < nsteps;
                 if (more) fetch(S0(), s + 1);
-                w.template macro<GX::PITCH, GY::PITCH>(xs[buf], ys[buf]);
+                // one wavefront per SIMD over 4-step boxes: reads interleaved
+                // with the MFMAs (measured faster there, not for 8-step boxes)
+                w.template macro<GX::PITCH, GY::PITCH, false, 0, WPE == 1 && KT == 16>(xs[buf],
+                                                                                  ys[buf]);
                 if (NBUF == 1 && more) __syncthreads();   // the single buffer is free again
                 if (more) {
                     gx.template store<0>(xs[NBUF == 2 ? buf ^ 1 : 0]);
