@@ -220,7 +220,9 @@ static double cu_time(int occ, int full, double nb, int tail, double len)
     double t = 0.0;
     while (!left.empty()) {
         const double w = (double)left.size();
-        const double rate = (left.size() >= 2 ? 1.0 : 0.64) / w;   // boxes per unit, each
+        // (a tile that holds one wavefront per SIMD anyway has that rate in
+        // its measured efficiency)
+        const double rate = (left.size() >= 2 || occ < 2 ? 1.0 : 0.64) / w;   // per unit, each
         const double step = *std::min_element(left.begin(), left.end());
         t += step / rate;
         std::vector<double> still;
@@ -558,9 +560,17 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         const double waves = tx * ty * wpt;
         const double perSimd = wpt >= 4 ? std::ceil(tx * ty / 256.0) * std::ceil(wpt / 4.0)
                                         : std::ceil(waves / 1024.0);
+        // The busiest CU's tiles pass through its resident slots (cu_time):
+        // a last round with fewer tiles than slots leaves wavefronts alone.
+        const double perSimdRun =
+            wpt >= 4
+                ? cu_time((int)tail_occupancy(c, itemB), (int)std::ceil(tx * ty / 256.0), 1.0, 0,
+                          0.0) *
+                      std::ceil(wpt / 4.0)
+                : perSimd;
         const double kpad = (double)std::max<int64_t>(b.nsteps, 1) * c.kt;
         const double waveFlops = (double)(c.mt / c.wm) * (c.nt / c.wn) * kpad * 2.0;
-        const double tMfma = perSimd * waveFlops / (peakSimd * c.eff) *
+        const double tMfma = perSimdRun * waveFlops / (peakSimd * c.eff) *
                              (kSplitAhead && c.nbuf == 1 && b.nsteps > 1 ? 1.4 : 1.0);
         // The persistent streaming kernel needs the contracted set in one box.
         const bool canStream = c.stream && b.nsteps <= 1;
@@ -618,8 +628,11 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
             best.tile = -1;
             for (int P = 2; P <= 256 && b.nsteps / P >= 8; P *= 2) {
                 const double wgs = tx * ty * P;
-                const double perSimdP = wpt >= 4 ? std::ceil(wgs / 256.0) * std::ceil(wpt / 4.0)
-                                                 : std::ceil(wgs * wpt / 1024.0);
+                const double perSimdP =
+                    wpt >= 4 ? cu_time((int)tail_occupancy(c, itemB), (int)std::ceil(wgs / 256.0),
+                                       1.0, 0, 0.0) *
+                                   std::ceil(wpt / 4.0)
+                             : std::ceil(wgs * wpt / 1024.0);
                 const double kpadP = (std::ceil((double)b.nsteps / P) + 2.0) * c.kt;
                 const double tM = perSimdP * (double)(c.mt / c.wm) * (c.nt / c.wn) * kpadP * 2.0 /
                                   (peakSimd * c.eff) *
