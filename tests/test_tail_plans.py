@@ -18,6 +18,8 @@ SHAPES = {
                        {"a": 23, "b": 17, "i": 19, "j": 21, "e": 13, "f": 11}),
     "ab-ak-kb": (("a,b", "a,k", "k,b"), {"a": 300, "b": 290, "k": 333}),
     "abc-adc-db": (("a,b,c", "a,d,c", "d,b"), {"a": 45, "b": 200, "c": 7, "d": 150}),
+    # one K box: every tail run is whole tiles, added with atomics
+    "abcd-aeb-edc": (("a,b,c,d", "a,e,b", "e,d,c"), {"a": 30, "b": 17, "c": 29, "d": 31, "e": 16}),
     "cc4x4": (("a,b,i,j", "i,e,j,f", "f,a,e,b"), {x: 48 for x in "abijef"}),
 }
 
