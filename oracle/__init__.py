@@ -42,29 +42,54 @@ def build(force: bool = True) -> str:
     return _LIB
 
 
+def _open(path: str):
+    """ctypes handle of a built oracle library with its signatures set."""
+    lib = ctypes.CDLL(path)
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    lib.oracle_contract.restype = ctypes.c_int
+    lib.oracle_contract.argtypes = [
+        ctypes.c_int,
+        ctypes.c_char_p, i64p, i64p,
+        ctypes.c_char_p, i64p, i64p,
+        ctypes.c_char_p, i64p, i64p,
+        ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_double,
+        ctypes.c_void_p, ctypes.c_int64, i64p,
+        ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), ctypes.c_int]
+    lib.oracle_max_threads.restype = ctypes.c_int
+    lib.oracle_transpose.restype = ctypes.c_int
+    lib.oracle_transpose.argtypes = [
+        ctypes.c_int, ctypes.c_int, i64p, i64p, i64p, ctypes.c_double, ctypes.c_void_p,
+        ctypes.c_double, ctypes.c_void_p, i64p,
+        ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    return lib
+
+
 def _load():
     global _lib
     if _lib is None:
         build(force=False)
-        lib = ctypes.CDLL(_LIB)
-        i64p = ctypes.POINTER(ctypes.c_int64)
-        lib.oracle_contract.restype = ctypes.c_int
-        lib.oracle_contract.argtypes = [
-            ctypes.c_int,
-            ctypes.c_char_p, i64p, i64p,
-            ctypes.c_char_p, i64p, i64p,
-            ctypes.c_char_p, i64p, i64p,
-            ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_double,
-            ctypes.c_void_p, ctypes.c_int64, i64p,
-            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), ctypes.c_int]
-        lib.oracle_max_threads.restype = ctypes.c_int
-        lib.oracle_transpose.restype = ctypes.c_int
-        lib.oracle_transpose.argtypes = [
-            ctypes.c_int, ctypes.c_int, i64p, i64p, i64p, ctypes.c_double, ctypes.c_void_p,
-            ctypes.c_double, ctypes.c_void_p, i64p,
-            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
-        _lib = lib
+        _lib = _open(_LIB)
     return _lib
+
+
+class using_library:
+    """Context manager: route every call to another build of the oracle's
+    source (the mutation tests build copies with a planted mistake and check
+    that the pins catch it)."""
+
+    def __init__(self, path: str):
+        self.path = path
+
+    def __enter__(self):
+        global _lib
+        self.saved = _load()
+        _lib = _open(self.path)
+        return self
+
+    def __exit__(self, *exc):
+        global _lib
+        _lib = self.saved
+        return False
 
 
 def max_threads() -> int:
@@ -190,6 +215,12 @@ def rel_error(got, ref: Result) -> float:
     got = np.asarray(got, dtype=np.float64).reshape(-1)
     out = np.asarray(ref.out64, dtype=np.float64).reshape(-1)
     den = np.asarray(ref.den64, dtype=np.float64).reshape(-1)
+    if got.size != out.size or den.size != out.size:
+        raise ValueError(f"sizes differ: got {got.size}, out64 {out.size}, den64 {den.size}")
+    # den64 is a sum of magnitudes: a negative or NaN value means a broken
+    # reference, and dividing by it would let any result pass
+    if np.any(~(den >= 0)):
+        raise ValueError("den64 must be >= 0 everywhere")
     if got.size == 0:
         return 0.0
     diff = np.abs(got - out)

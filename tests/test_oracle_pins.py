@@ -394,6 +394,94 @@ def test_error_metric_catches_a_dropped_term():
     assert oracle.rel_error(A @ B, ref) < 1e-14
 
 
+# ------------------------------- the parity metric's denominator (den64) ---
+#
+# The parity bar divides |GPU - out64| by den64 = |alpha| sum_k |a||b| +
+# |beta| |c|: the benchmark spec's metric max|diff| / sum_k |A||B| (Sec. 2.2, Eq. 3
+# with its alpha and beta).  These checks fix den64 independently of the
+# oracle's own loop: closed forms, a hand computation and invariants that a
+# dropped term, a signed instead of absolute factor, or a missing |alpha| /
+# |beta| would break.
+
+def signs(rng, shape):
+    """Entries +1 or -1 with random sign: |a| = 1 everywhere."""
+    return np.asfortranarray(rng.choice([-1.0, 1.0], size=shape))
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_den_of_unit_magnitudes_is_contracted_size(seed):
+    """|a| = |b| = 1 makes sum_k |a||b| = S_Ik exactly, whatever the signs:
+    den64 = |alpha| * S_Ik + |beta| * |c|, for either sign of alpha and beta
+    and any mode pattern (strided and permuted views included)."""
+    rng = np.random.default_rng(4000 + seed)
+    mc, ma, mb, ext = wl.random_problem(rng, max_rank=6, max_ext=4,
+                                        allow_empty_sets=(seed % 4 == 3))
+    sk = int(np.prod([ext[m] for m in split(ma) if m not in split(mc)]))
+    A = signs(rng, [ext[m] for m in split(ma)])
+    B = signs(rng, [ext[m] for m in split(mb)])
+    if seed % 2:   # a strided view of B
+        big = signs(rng, [2 * ext[m] for m in split(mb)])
+        B = big[tuple(slice(0, None, 2) for _ in split(mb))]
+    alpha = [1.5, -0.75, -2.0, 0.5][seed % 4]
+    beta = [0.0, -1.25, 2.0][seed % 3]
+    C = rand(rng, [ext[m] for m in split(mc)]) if beta != 0 else None
+    got = run(mc, ma, mb, ext, A, B, alpha, beta, C)
+    expect = abs(alpha) * sk + (abs(beta) * np.abs(C) if beta != 0 else 0.0)
+    np.testing.assert_array_equal(got.den64, np.broadcast_to(expect, got.den64.shape))
+
+
+def test_den_hand_computed_2x2x2():
+    """C[m,n] = alpha * A[m,k] B[k,n] + beta * C[m,n] with m, n, k of extent 2,
+    worked by hand:
+        A = [[1, -2], [3, -4]] (rows m, columns k), B = [[-1, 0.5], [2, -3]]
+        (rows k, columns n), C = [[1, -1], [2, -2]], alpha = -2, beta = -0.5.
+        sum_k |a||b|: (0,0) 1+4 = 5, (0,1) 0.5+6 = 6.5, (1,0) 3+8 = 11,
+                      (1,1) 1.5+12 = 13.5
+        den = 2 * that + 0.5 * |c| = 10.5, 13.5, 23, 28
+        sum_k ab:     -5, 6.5, -11, 13.5
+        out = -2 * that - 0.5 * c = 9.5, -12.5, 21, -26."""
+    A = np.array([[1.0, -2.0], [3.0, -4.0]], order="F")
+    B = np.array([[-1.0, 0.5], [2.0, -3.0]], order="F")
+    C = np.array([[1.0, -1.0], [2.0, -2.0]], order="F")
+    got = oracle.contract("m,n", "m,k", "k,n", A, B, -2.0, -0.5, C)
+    np.testing.assert_array_equal(got.den64, [[10.5, 13.5], [23.0, 28.0]])
+    np.testing.assert_array_equal(got.out64, [[9.5, -12.5], [21.0, -26.0]])
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_den_bounds_the_result_and_ignores_signs(seed):
+    """Triangle inequality: |out64| <= den64 element by element, and den64 >= 0.
+    Flipping the sign of any entries of A, B or C leaves den64 bit-identical
+    (|-x| = |x| exactly, the same summation order), while out64 changes."""
+    rng = np.random.default_rng(4100 + seed)
+    mc, ma, mb, ext = wl.random_problem(rng, max_rank=6, max_ext=5)
+    shp = lambda m: [ext[x] for x in split(m)]
+    A, B, C = rand(rng, shp(ma)), rand(rng, shp(mb)), rand(rng, shp(mc))
+    alpha, beta = (-1.5, -0.5) if seed % 2 else (0.75, 2.0)
+    r = run(mc, ma, mb, ext, A, B, alpha, beta, C)
+    assert np.all(r.den64 >= 0)
+    assert np.all(np.abs(r.out64) <= r.den64 * (1 + 1e-15))
+    flip = lambda X: np.asfortranarray(X * rng.choice([-1.0, 1.0], size=X.shape))
+    r2 = run(mc, ma, mb, ext, flip(A), flip(B), alpha, beta, flip(C))
+    np.testing.assert_array_equal(r2.den64, r.den64)
+    # powers of two scale exactly: den(2 alpha, 2 beta) = 2 den(alpha, beta)
+    r3 = run(mc, ma, mb, ext, A, B, 2 * alpha, 2 * beta, C)
+    np.testing.assert_array_equal(r3.den64, 2 * r.den64)
+
+
+def test_rel_error_refuses_a_negative_or_nan_denominator():
+    """A negative (or NaN) den64 would make every check pass vacuously."""
+    ref = oracle.Result(np.array([1.0, 2.0]), np.array([1.0, -1.0]))
+    with pytest.raises(ValueError):
+        oracle.rel_error(np.array([1.0, 2.0]), ref)
+    ref = oracle.Result(np.array([1.0, 2.0]), np.array([1.0, np.nan]))
+    with pytest.raises(ValueError):
+        oracle.rel_error(np.array([1.0, 2.0]), ref)
+    ref = oracle.Result(np.array([1.0, 2.0]), np.array([1.0, 1.0]))
+    with pytest.raises(ValueError):
+        oracle.rel_error(np.array([1.0, 2.0, 3.0]), ref)   # sizes differ
+
+
 # ------------------------------------------- Eq. 4: tensor transposition ---
 
 def test_transpose_worked_example():
