@@ -31,7 +31,7 @@ extern "C" {
 #endif
 
 /* Maximum number of modes of one tensor. */
-#define GETT_MAX_RANK 12
+#define GETT_MAX_RANK 16
 
 /* Element type of A, B and C (Table II: --floatType=[s,d]).  Products and
  * sums are formed in the same type (fp32 or fp64 matrix-core arithmetic). */
@@ -50,7 +50,11 @@ typedef enum {
      * between tensors */
     GETT_ERROR_INVALID_INDICES = 2,
     /* rank above GETT_MAX_RANK; C strides that may map two elements of C to
-     * one address; a tensor whose largest element offset reaches 2^31 - 1 */
+     * one address; a tensor whose largest element offset reaches 2^62; for
+     * gett_plan, a tile whose rows (with one K box) span 2^31 - 1 elements or
+     * more of one tensor (tensors themselves may hold 2^31 elements or more:
+     * each tile is reached through 64-bit base offsets); for the TTGT and
+     * LoG planners and gett_transpose, any offset reaching 2^31 - 1 */
     GETT_ERROR_NOT_SUPPORTED = 3,
     /* a HIP runtime call (kernel launch) or a rocBLAS call failed */
     GETT_ERROR_HIP = 4,

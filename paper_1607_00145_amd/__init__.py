@@ -27,7 +27,7 @@ GETT_FLAG_NO_SWAP = 1
 GETT_FLAG_SCALAR = 2
 GETT_FLAG_NO_SPLIT = 4
 GETT_FLAG_DETERMINISTIC = 8
-GETT_MAX_RANK = 12
+GETT_MAX_RANK = 16
 GETT_METHOD_GETT = 0
 GETT_METHOD_TTGT = 1
 GETT_METHOD_LOG = 2

@@ -37,16 +37,48 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
+# Translation units built once per tile shape (GETT_TILE = 0 .. n-1) and once
+# without it, so the kernel instantiations compile in parallel.
+PER_TILE = {"launch_f32.hip": "kTilesF32", "launch_f64.hip": "kTilesF64"}
+
+
+def tile_count(array: str) -> int:
+    """Entries of a tile table in tiles.hpp."""
+    text = open(os.path.join(CSRC, "tiles.hpp")).read()
+    body = text[text.index(array + "[] = {"):]
+    body = body[:body.index("};")]
+    return sum(1 for line in body.splitlines() if line.strip().startswith("{"))
+
+
+def jobs_of(src: str):
+    """(source, tile or None) compile jobs of one source file."""
+    if src in PER_TILE:
+        return [(src, None)] + [(src, t) for t in range(tile_count(PER_TILE[src]))]
+    return [(src, None)]
+
+
 def sources():
     return sorted(f for f in os.listdir(CSRC) if f.endswith((".cpp", ".hip")))
 
 
-def compile_one(src: str) -> str:
+def newest_input() -> float:
+    """Modification time of the newest source or header the objects depend on."""
+    files = [os.path.join(CSRC, f) for f in os.listdir(CSRC)]
+    files += [os.path.join(ROOT, "include", f) for f in os.listdir(os.path.join(ROOT, "include"))]
+    return max(os.path.getmtime(f) for f in files)
+
+
+def compile_one(job, incremental: bool = False) -> str:
+    src, tile = job
     os.makedirs(BUILD, exist_ok=True)
-    obj = os.path.join(BUILD, src + ".o")
+    obj = os.path.join(BUILD, src + ("" if tile is None else f".t{tile}") + ".o")
+    if incremental and os.path.exists(obj) and os.path.getmtime(obj) >= newest_input():
+        return obj
     cmd = [hipcc()] + COMMON
     if src.endswith(".hip"):
         cmd += DEVICE + ["-x", "hip"]
+    if tile is not None:
+        cmd += [f"-DGETT_TILE={tile}"]
     cmd += ["-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
@@ -59,11 +91,15 @@ def compile_one(src: str) -> str:
     return obj
 
 
-def build(jobs: int = 0) -> str:
-    srcs = sources()
-    jobs = jobs or min(len(srcs), os.cpu_count() or 4)
+def build(jobs: int = 0, incremental: bool = False) -> str:
+    """Compile every source (or, incremental, only those whose object is older
+    than the newest source or header) and link libgett.so."""
+    work = [j for src in sources() for j in jobs_of(src)]
+    # the largest units first, so they do not end up last on one worker
+    work.sort(key=lambda j: (j[0] not in PER_TILE, j[1] is None))
+    jobs = jobs or min(len(work), os.cpu_count() or 4)
     with cf.ThreadPoolExecutor(jobs) as ex:
-        objs = list(ex.map(compile_one, srcs))
+        objs = list(ex.map(lambda j: compile_one(j, incremental), work))
     os.makedirs(LIBDIR, exist_ok=True)
     tmp = LIB + f".tmp{os.getpid()}"
     cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + objs + \
@@ -78,5 +114,7 @@ def build(jobs: int = 0) -> str:
 if __name__ == "__main__":
     ap = argparse.ArgumentParser()
     ap.add_argument("-j", type=int, default=0)
+    ap.add_argument("--incremental", action="store_true",
+                    help="recompile only objects older than the newest source or header")
     a = ap.parse_args()
-    print(build(a.j))
+    print(build(a.j, a.incremental))

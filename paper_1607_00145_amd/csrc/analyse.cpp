@@ -102,14 +102,16 @@ gett_status_t load_tensor(const char *m, const int64_t *e, const int64_t *s, Ten
     return GETT_SUCCESS;
 }
 
+// Largest element offset of a tensor (INT64_MAX beyond 2^62).
 int64_t max_offset(const Tensor &t)
 {
+    const int64_t cap = (int64_t)1 << 62;
     int64_t m = 0;
     for (size_t i = 0; i < t.modes.size(); ++i) {
         if (t.ext[i] <= 1) continue;
-        if (t.str[i] >= INT32_MAX) return INT64_MAX;
+        if (t.str[i] >= cap || (t.ext[i] - 1) > cap / t.str[i]) return INT64_MAX;
         m += (t.ext[i] - 1) * t.str[i];
-        if (m >= INT32_MAX) return INT64_MAX;
+        if (m >= cap) return INT64_MAX;
     }
     return m;
 }
@@ -189,6 +191,23 @@ void json_set(std::ostringstream &o, const char *key, const std::vector<Index> &
 
 }  // namespace
 
+Hooks read_hooks()
+{
+    Hooks h;
+    const struct {
+        const char *name;
+        const char **slot;
+    } vars[] = {{"GETT_FORCE_TILE", &h.forceTile},     {"GETT_FORCE_KIND", &h.forceKind},
+                {"GETT_FORCE_KSLICES", &h.forceKslices}, {"GETT_SPLIT_F", &h.splitF},
+                {"GETT_C_ORDER", &h.cOrder},           {"GETT_XCD_REMAP", &h.xcdRemap},
+                {"GETT_LANE_PERM", &h.lanePerm},       {"GETT_TAIL_WGS", &h.tailWgs}};
+    for (const auto &v : vars) {
+        *v.slot = getenv(v.name);
+        if (*v.slot) h.text += std::string(v.name) + "=" + *v.slot + ";";
+    }
+    return h;
+}
+
 const char *kind_name(int k)
 {
     return k == 1 ? "stream" : k == 2 ? "kslices" : k == 3 ? "tail" : "macro";
@@ -267,7 +286,8 @@ const char *mode_name(int m)
 
 gett_status_t front_end(Analysis &an, gett_dtype_t dtype, const char *mC, const int64_t *eC,
                         const int64_t *sC, const char *mA, const int64_t *eA, const int64_t *sA,
-                        const char *mB, const int64_t *eB, const int64_t *sB, int rank[3])
+                        const char *mB, const int64_t *eB, const int64_t *sB, int rank[3],
+                        bool offsets31)
 {
     if (dtype != GETT_FLOAT32 && dtype != GETT_FLOAT64) return GETT_ERROR_INVALID_VALUE;
     Tensor A, B, C;
@@ -315,8 +335,8 @@ gett_status_t front_end(Analysis &an, gett_dtype_t dtype, const char *mC, const 
     an.maxOffA = max_offset(A);
     an.maxOffB = max_offset(B);
     an.maxOffC = max_offset(C);
-    if (an.maxOffA >= INT32_MAX || an.maxOffB >= INT32_MAX || an.maxOffC >= INT32_MAX)
-        return GETT_ERROR_NOT_SUPPORTED;
+    const int64_t lim = offsets31 ? (int64_t)INT32_MAX : INT64_MAX;
+    if (an.maxOffA >= lim || an.maxOffB >= lim || an.maxOffC >= lim) return GETT_ERROR_NOT_SUPPORTED;
     if (!c_is_injective(C)) return GETT_ERROR_NOT_SUPPORTED;
 
     for (auto &x : an.Im) { an.sizeM *= x.extent; }
@@ -350,7 +370,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     Analysis an;
     int rank[3];
     const gett_status_t st =
-        front_end(an, dtype, mC, eC, sC, mA, eA, sA, mB, eB, sB, rank);
+        front_end(an, dtype, mC, eC, sC, mA, eA, sA, mB, eB, sB, rank, false);
     if (st != GETT_SUCCESS) return st;
 
     // ---- operand roles: C's stride-one index on the column (y) side ----
@@ -529,8 +549,9 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     // box is exposed (measured on MI355X: 1.4-1.8x slower than the
     // double-buffered tiles of the same depth).
     // Each tile's K box is priced on the contracted order that tile gets.
-    const char *ft = getenv("GETT_FORCE_TILE");
-    const char *fk = getenv("GETT_FORCE_KIND");
+    const Hooks hk = read_hooks();
+    const char *ft = hk.forceTile;
+    const char *fk = hk.forceKind;
     // An operand gathers in vectors when its stride-one index leads its free
     // order or the contracted order (before any index split).
     auto vecable = [&](const std::vector<Index> &I, auto strOf) {
@@ -735,7 +756,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     }
     // tuning hook: this many K slices on the chosen tile
     // (1: none), unless the plan must be deterministic
-    if (const char *fs = getenv("GETT_FORCE_KSLICES")) {
+    if (const char *fs = hk.forceKslices) {
         const int P = atoi(fs);
         if (P == 1 && pick.kind == 2) {
             if (const Candidate *c = find(pick.tile, 0)) pick = *c;
@@ -803,7 +824,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
                                  Cbytes * writePrice(itemB * t);
                 if (c < best) { best = c; f = t; }
             }
-            if (const char *fs = getenv("GETT_SPLIT_F")) f = atoi(fs);   // tuning hook
+            if (const char *fs = hk.splitF) f = atoi(fs);   // tuning hook
             std::vector<Index> trial = Iy;
             if (f >= VW && (f & (f - 1)) == 0 && Iy[0].extent % f == 0 && ts.nt % (f * VW) == 0) {
                 split_front(trial, 0, (size_t)yRow, f);
@@ -907,8 +928,44 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
             (cap / ts.mt - VW) / E >= 1)
             crun = (int)E;
     }
-    if (const char *co = getenv("GETT_C_ORDER")) {   // tuning hook: 0 turns it off
+    if (const char *co = hk.cOrder) {   // tuning hook: 0 turns it off
         if (atoi(co) == 0) crun = 0;
+    }
+
+    // ---- addressing: the kernels reach each tile through 64-bit base
+    //      offsets and address inside it with 32-bit offsets (rows and
+    //      columns relative to the tile's base, K-box positions relative to
+    //      the box origin), so tensors may hold 2^31 elements or more as long
+    //      as one tile's rows plus one box span less than 2^31 - 1 elements.
+    //      Over R consecutive positions of a set, digit i moves at most
+    //      min(e_i - 1, floor((R - 1) / P_i) + 1) above its lowest value
+    //      (P_i: product of the earlier extents). ----
+    {
+        constexpr int64_t cap = (int64_t)1 << 62;
+        auto sat = [](int64_t a, int64_t b) {   // a * b, saturating at cap
+            return (a != 0 && b > cap / a) ? cap : a * b;
+        };
+        auto span = [&](const std::vector<Index> &I, auto strOf, int64_t R) {
+            int64_t tot = 0, P = 1;
+            for (const Index &x : I) {
+                const int64_t moves = std::min<int64_t>(x.extent - 1, (R - 1) / P + 1);
+                tot = std::min(cap, tot + sat(std::max<int64_t>(moves, 0), strOf(x)));
+                P = sat(P, std::max<int64_t>(x.extent, 1));
+            }
+            return tot;
+        };
+        auto kspan = [&](auto strOf) {
+            int64_t tot = sat(box.tj - 1, strOf(Ik[box.kj]));
+            for (int i = 0; i < box.kj; ++i)
+                tot = std::min(cap, tot + sat(Ik[i].extent - 1, strOf(Ik[i])));
+            return tot;
+        };
+        auto sC = [](const Index &x) { return x.strC; };
+        const int64_t lim = INT32_MAX;
+        if (!an.emptyC && (span(Ix, sX, ts.mt) + kspan(sX) >= lim ||
+                           span(Iy, sY, ts.nt) + kspan(sY) >= lim ||
+                           span(Ix, sC, ts.mt) + span(Iy, sC, ts.nt) >= lim))
+            return GETT_ERROR_NOT_SUPPORTED;
     }
 
     // ---- descriptor ----
@@ -949,7 +1006,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     d.group = (int32_t)std::max<int64_t>(1, std::min<int64_t>(8, tilesX));
     d.order = streaming ? 1 : 0;
     d.xcdremap = -1;   // decided per call (see gett_contract)
-    if (const char *xr = getenv("GETT_XCD_REMAP")) d.xcdremap = atoi(xr) != 0;   // tuning hook
+    if (const char *xr = hk.xcdRemap) d.xcdremap = atoi(xr) != 0;   // tuning hook
     d.cvec = cvec ? 1 : 0;
     d.xscalar_kfast = sX(Ik[0]) < sX(Ix[0]) ? 1 : 0;
     d.yscalar_kfast = sY(Ik[0]) < sY(Iy[0]) ? 1 : 0;
@@ -966,7 +1023,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     };
     d.xperm = lane_perm(Ix, sX, xmode, ts.mt, d.xscalar_kfast);
     d.yperm = lane_perm(Iy, sY, ymode, ts.nt, d.yscalar_kfast);
-    if (const char *lp = getenv("GETT_LANE_PERM")) {   // tuning hook: 0 turns it off
+    if (const char *lp = hk.lanePerm) {   // tuning hook: 0 turns it off
         if (atoi(lp) == 0) d.xperm = d.yperm = 0;
     }
     d.yes = yes;
@@ -978,7 +1035,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         // the model's number of tail workgroups (256 when the tail was forced
         // on a plan the model did not rank it for; tuning hook: GETT_TAIL_WGS)
         int64_t wgs = pick.kind == 3 && pick.slices > 1 ? pick.slices : 256;
-        if (const char *tw = getenv("GETT_TAIL_WGS")) wgs = std::max<int64_t>(1, atoll(tw));
+        if (const char *tw = hk.tailWgs) wgs = std::max<int64_t>(1, atoll(tw));
         const TailShape tsh = tail_shape((int64_t)tilesX * tilesY, std::max<int64_t>(nsteps, 1), wgs);
         d.tailFull = (int32_t)tsh.full;
         d.tailWgs = (int32_t)tsh.wgs;
@@ -989,6 +1046,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
 
     plan.dtype = dtype;
     plan.flags = flags;
+    plan.hooks = hk.text;
     plan.rank[0] = rank[0];
     plan.rank[1] = rank[1];
     plan.rank[2] = rank[2];

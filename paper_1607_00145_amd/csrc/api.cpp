@@ -65,7 +65,7 @@ std::unordered_map<std::string, std::pair<int, int>> g_tuned;
 std::string key_of(const gett_plan_s &p)
 {
     std::ostringstream k;
-    k << (int)p.dtype << "|" << p.flags;
+    k << (int)p.dtype << "|" << p.flags << "|" << p.hooks;
     for (int i = 0; i < 3; ++i) {
         k << "|" << p.modes[i] << "|";
         for (auto v : p.ext[i]) k << v << ",";

@@ -16,7 +16,7 @@
 
 namespace gett {
 
-constexpr int kMaxDims = 12;   // per index set (== GETT_MAX_RANK)
+constexpr int kMaxDims = 16;   // per index set (== GETT_MAX_RANK)
 
 // Gather modes of an operand tile (see kernel.hpp).
 enum GatherMode : int {

@@ -95,22 +95,23 @@ __device__ __forceinline__ void tile_of_block(const KDesc &d, int bid, int nwg, 
 
 // Origin of K box `s`: block `s % nblk` of index kj, then one point of each
 // later contracted index (first one fastest).  Returns the origin offsets in
-// X and Y and the number of valid positions left along index kj.
-__device__ __forceinline__ int box_origin(const KDesc &d, uint32_t s, int &ox, int &oy)
+// X and Y (64-bit: a tensor may hold 2^31 elements or more) and the number of
+// valid positions left along index kj.
+__device__ __forceinline__ int box_origin(const KDesc &d, uint32_t s, int64_t &ox, int64_t &oy)
 {
     const uint32_t nb = (uint32_t)d.nblk;
     const uint32_t rest0 = s / nb;
     const int blk = (int)(s - rest0 * nb);
     uint32_t rest = rest0;
-    ox = blk * d.tj * (int)d.strXk[d.kj];
-    oy = blk * d.tj * (int)d.strYk[d.kj];
+    ox = (int64_t)(blk * d.tj) * d.strXk[d.kj];
+    oy = (int64_t)(blk * d.tj) * d.strYk[d.kj];
     for (int i = d.kj + 1; i < d.nk; ++i) {
         const uint32_t e = (uint32_t)d.extK[i];
         const uint32_t q = rest / e;
         const uint32_t c = rest - q * e;
         rest = q;
-        ox += (int)c * (int)d.strXk[i];
-        oy += (int)c * (int)d.strYk[i];
+        ox += (int64_t)c * d.strXk[i];
+        oy += (int64_t)c * d.strYk[i];
     }
     return d.extK[d.kj] - blk * d.tj;
 }
@@ -122,11 +123,12 @@ __device__ __forceinline__ int box_origin(const KDesc &d, uint32_t s, int &ox, i
 // be asked for; consecutive ones cost a few scalar additions.
 struct BoxWalker {
     uint32_t cur;        // box whose origin is held
-    int ox, oy, lim;     // its origins in X and Y and valid positions along kj
+    int64_t ox, oy;      // its origins in X and Y
+    int lim;             // valid positions along kj
     int blk, c1;         // its block along kj and value of index kj + 1
     int nblk, e1;        // blocks along kj; extent of index kj + 1 (0: none)
-    int bx, by;          // origin step of one block along kj in X and Y
-    int sx1, sy1;        // strides of index kj + 1 in X and Y
+    int64_t bx, by;      // origin step of one block along kj in X and Y
+    int64_t sx1, sy1;    // strides of index kj + 1 in X and Y
     int ek, tj;          // extent of index kj and its block length
 
     __device__ __forceinline__ void reset(const KDesc &d, uint32_t s)
@@ -141,16 +143,16 @@ struct BoxWalker {
         nblk = d.nblk > 0 ? d.nblk : 1;
         tj = d.tj;
         ek = d.extK[d.kj];
-        bx = d.tj * (int)d.strXk[d.kj];
-        by = d.tj * (int)d.strYk[d.kj];
+        bx = (int64_t)d.tj * d.strXk[d.kj];
+        by = (int64_t)d.tj * d.strYk[d.kj];
         const bool later = d.kj + 1 < d.nk;
         e1 = later ? d.extK[d.kj + 1] : 0;
-        sx1 = later ? (int)d.strXk[d.kj + 1] : 0;
-        sy1 = later ? (int)d.strYk[d.kj + 1] : 0;
+        sx1 = later ? d.strXk[d.kj + 1] : 0;
+        sy1 = later ? d.strYk[d.kj + 1] : 0;
         reset(d, s);
     }
     // origin of box s (returns the valid positions along kj)
-    __device__ __forceinline__ int at(const KDesc &d, uint32_t s, int &x, int &y)
+    __device__ __forceinline__ int at(const KDesc &d, uint32_t s, int64_t &x, int64_t &y)
     {
         if (s == cur + 1) {
             cur = s;
@@ -160,8 +162,8 @@ struct BoxWalker {
                 lim -= tj;
             } else if (++c1 < e1) {
                 blk = 0;
-                ox += sx1 - (nblk - 1) * bx;
-                oy += sy1 - (nblk - 1) * by;
+                ox += sx1 - (int64_t)(nblk - 1) * bx;
+                oy += sy1 - (int64_t)(nblk - 1) * by;
                 lim = ek;
             } else {
                 reset(d, s);
@@ -366,11 +368,68 @@ template <int R> __device__ __forceinline__ int block_row(int b, int rho)
     return (b / R) * 16 * R + R * rho + (b % R);
 }
 
+// Lowest offset any of the positions [x0, x1] of a linearised set can have
+// (in the operand and in C), taken digit by digit: a digit that wraps inside
+// the range can be 0, one that does not keeps its value at x0.  Offsets of the
+// range relative to it are then >= 0, and the analyser bounds them by 2^31 - 1
+// (the tile's own span), so the per-tile tables hold 32-bit offsets while the
+// tensors may be larger.
+__device__ __forceinline__ void range_base(int n, const int32_t *ext, const int64_t *sop,
+                                           const int64_t *sc, uint32_t x0, uint32_t x1,
+                                           int64_t &bop, int64_t &bc)
+{
+    bop = 0;
+    bc = 0;
+    for (int i = 0; i < n; ++i) {
+        const uint32_t e = (uint32_t)ext[i];
+        const uint32_t q0 = x0 / e, q1 = x1 / e;
+        const int64_t dmin = q0 == q1 ? (int64_t)(x0 - q0 * e) : 0;
+        bop += dmin * sop[i];
+        bc += dmin * sc[i];
+        x0 = q0;
+        x1 = q1;
+    }
+}
+
+// A value the whole wavefront shares, said so to the compiler (it then stays
+// in scalar registers: a C base it takes for a per-lane value costs the
+// epilogue its batched loads -- each load of C followed by its own wait).
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ int64_t uniform(int64_t v)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Base offsets of one tile: rows [tx MT, ...) of the x set, columns
+// [ty NT, ...) of the y set, in the operands and in C.
+struct TileBase {
+    int64_t x, cx, y, cy;
+};
+
+template <int MT, int NT>
+__device__ __forceinline__ TileBase tile_base(const KDesc &d, int tx, int ty)
+{
+    TileBase b;
+    const uint32_t x0 = (uint32_t)(uniform(tx) * MT), y0 = (uint32_t)(uniform(ty) * NT);
+    const uint32_t x1 = (uint32_t)min((int64_t)x0 + MT, d.sizeX) - 1;
+    const uint32_t y1 = (uint32_t)min((int64_t)y0 + NT, d.sizeY) - 1;
+    range_base(d.nx, d.extX, d.strXop, d.strCx, x0, x1, b.x, b.cx);
+    range_base(d.ny, d.extY, d.strYop, d.strCy, y0, y1, b.y, b.cy);
+    b.x = uniform(b.x);
+    b.cx = uniform(b.cx);
+    b.y = uniform(b.y);
+    b.cy = uniform(b.cy);
+    return b;
+}
+
 // identify_subtensor for one tile: operand and C offsets of every tile row
-// (x side) and column (y side), one mixed-radix decomposition each.
+// (x side) and column (y side), relative to the tile's base offsets, one
+// mixed-radix decomposition each.
 template <int MT, int NT, int NTH>
-__device__ __forceinline__ void tile_tables(const KDesc &d, int tx, int ty, int tid, int *rowX,
-                                            int *offCx, int *rowY, int *offCy)
+__device__ __forceinline__ void tile_tables(const KDesc &d, int tx, int ty, const TileBase &b,
+                                            int tid, int *rowX, int *offCx, int *rowY, int *offCy)
 {
     for (int r = tid; r < MT + NT; r += NTH) {
         const bool isx = r < MT;
@@ -378,17 +437,18 @@ __device__ __forceinline__ void tile_tables(const KDesc &d, int tx, int ty, int 
         uint32_t v = (uint32_t)(isx ? tx * MT : ty * NT) + rr;
         int oo = -1, oc = -1;
         if ((int64_t)v < (isx ? d.sizeX : d.sizeY)) {
-            oo = 0;
-            oc = 0;
+            int64_t o64 = 0, c64 = 0;
             const int n = isx ? d.nx : d.ny;
             for (int i = 0; i < n; ++i) {
                 const uint32_t e = (uint32_t)(isx ? d.extX[i] : d.extY[i]);
                 const uint32_t q = v / e;
                 const uint32_t id = v - q * e;
                 v = q;
-                oo += (int)id * (int)(isx ? d.strXop[i] : d.strYop[i]);
-                oc += (int)id * (int)(isx ? d.strCx[i] : d.strCy[i]);
+                o64 += (int64_t)id * (isx ? d.strXop[i] : d.strYop[i]);
+                c64 += (int64_t)id * (isx ? d.strCx[i] : d.strCy[i]);
             }
+            oo = (int)(o64 - (isx ? b.x : b.y));
+            oc = (int)(c64 - (isx ? b.cx : b.cy));
         }
         if (isx) {
             rowX[rr] = oo;
@@ -409,17 +469,21 @@ __device__ __forceinline__ void box_tables(const KDesc &d, int tid, int *kX, int
         int pos = kInvalidK;
         if (kk < d.kbox) {
             uint32_t k = (uint32_t)kk;
+            int64_t x64 = 0, y64 = 0;
             for (int i = 0; i < d.kj; ++i) {
                 const uint32_t e = (uint32_t)d.extK[i];
                 const uint32_t q = k / e;
                 const uint32_t id = k - q * e;
                 k = q;
-                ox += (int)id * (int)d.strXk[i];
-                oy += (int)id * (int)d.strYk[i];
+                x64 += (int64_t)id * d.strXk[i];
+                y64 += (int64_t)id * d.strYk[i];
             }
             pos = (int)k;   // position along index kj, < tj
-            ox += (int)k * (int)d.strXk[d.kj];
-            oy += (int)k * (int)d.strYk[d.kj];
+            x64 += (int64_t)k * d.strXk[d.kj];
+            y64 += (int64_t)k * d.strYk[d.kj];
+            // within the box's span, which the analyser bounds by 2^31 - 1
+            ox = (int)x64;
+            oy = (int)y64;
         }
         kX[kk] = ox;
         kY[kk] = oy;
@@ -809,8 +873,9 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     __shared__ __attribute__((aligned(16))) T panels[kPanels];
     T(*xs)[KT * GX::PITCH] = reinterpret_cast<T(*)[KT * GX::PITCH]>(panels);
     T(*ys)[KT * GY::PITCH] = reinterpret_cast<T(*)[KT * GY::PITCH]>(panels + NBUF * KT * GX::PITCH);
-    // Element offsets fit in 31 bits (the plan refuses larger tensors); -1 marks
-    // a row or column outside the tensor.
+    // Offsets relative to the tile's base offsets (TileBase) and to the box
+    // origin fit in 31 bits (the plan checks the spans); -1 marks a row or
+    // column outside the tensor.
     __shared__ int rowX[MT], rowY[NT], offCx[MT], offCy[NT];
     __shared__ int kX[KT], kY[KT];
     __shared__ int kco[KT];
@@ -828,7 +893,11 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     auto piece = [&](int tile, uint32_t s0, uint32_t nsteps, bool atomic) {
         int tx, ty;
         tile_of_block(d, tile, ntiles, tx, ty);
-        tile_tables<MT, NT, NTH>(d, tx, ty, tid, rowX, offCx, rowY, offCy);
+        const TileBase tb = tile_base<MT, NT>(d, tx, ty);
+        tile_tables<MT, NT, NTH>(d, tx, ty, tb, tid, rowX, offCx, rowY, offCy);
+        const T *Xt = X + tb.x;
+        const T *Yt = Y + tb.y;
+        T *Ct = C + (tb.cx + tb.cy);
         if (XMODE == kGatherScalar && d.xperm > 0) row_perm<MT, NTH>(d.xperm, tx * MT, tid, permX);
         if (YMODE == kGatherScalar && d.yperm > 0) row_perm<NT, NTH>(d.yperm, ty * NT, tid, permY);
         __syncthreads();
@@ -846,10 +915,10 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
         }
         auto fetch = [&](auto stage, uint32_t s) {
             constexpr int B = decltype(stage)::value;
-            int ox, oy;
+            int64_t ox, oy;
             const int lim = walk.at(d, s0 + s, ox, oy);
-            gx.template load<B>(X + ox, lim);
-            gy.template load<B>(Y + oy, lim);
+            gx.template load<B>(Xt + ox, lim);
+            gy.template load<B>(Yt + oy, lim);
         };
         typedef std::integral_constant<int, 0> S0;
         typedef std::integral_constant<int, 1> S1;
@@ -860,22 +929,22 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
             // box needs no more).  Plans with more boxes (a tile forced onto
             // them) take the same steps box after box, copying item by item.
             if (nsteps == 1) {
-                int ox, oy;
+                int64_t ox, oy;
                 const int lim = box_origin(d, s0, ox, oy);
-                gx.template load<0>(X + ox, lim);
+                gx.template load<0>(Xt + ox, lim);
                 gx.template store<0>(xs[0]);
-                gy.template load<0>(Y + oy, lim);
+                gy.template load<0>(Yt + oy, lim);
                 gy.template store<0>(ys[0]);
                 __syncthreads();
                 w.template macro<GX::PITCH, GY::PITCH, true, 2>(xs[0], ys[0]);
             } else {
                 w.zero();
                 for (uint32_t s = 0; s < nsteps; ++s) {
-                    int ox, oy;
+                    int64_t ox, oy;
                     const int lim = box_origin(d, s0 + s, ox, oy);
                     if (s > 0) __syncthreads();   // the MFMAs of the previous box are done
-                    gx.copy(X + ox, lim, xs[0]);
-                    gy.copy(Y + oy, lim, ys[0]);
+                    gx.copy(Xt + ox, lim, xs[0]);
+                    gy.copy(Yt + oy, lim, ys[0]);
                     __syncthreads();
                     w.template macro<GX::PITCH, GY::PITCH, false, 2>(xs[0], ys[0]);
                 }
@@ -929,19 +998,19 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
             }
         }
         if (atomic) {
-            w.unpack_atomic(C, offCx, offCy, alpha);
+            w.unpack_atomic(Ct, offCx, offCy, alpha);
             return;
         }
         if constexpr (CORDER && WT::kVecC) {   // compiled only into the tiles that carry it
             if (d.crun > 0 && d.cvec) {
                 const int y0 = ty * NT;
                 const int ylim = (int)min((int64_t)y0 + NT, d.sizeY);
-                unpack_c_order<T, MT, NTH>(w, C, panels, kPanels, offCx, offCy, y0, ylim, d.crun,
+                unpack_c_order<T, MT, NTH>(w, Ct, panels, kPanels, offCx, offCy, y0, ylim, d.crun,
                                            alpha, beta, tid);
                 return;
             }
         }
-        w.template unpack<ONEBOX ? 2 : 1>(C, offCx, offCy, alpha, beta, d.cvec != 0);
+        w.template unpack<ONEBOX ? 2 : 1>(Ct, offCx, offCy, alpha, beta, d.cvec != 0);
     };
 
     if constexpr (TAIL) {
@@ -1016,13 +1085,13 @@ gett_stream_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
     if (t >= ntiles) return;   // uniform per workgroup; the host never launches more
 
     const bool withK = d.nsteps > 0;   // 0: alpha == 0 or an empty sum, A and B unread
-    int ox0 = 0, oy0 = 0, lim = 0;
+    int64_t ox0 = 0, oy0 = 0;
+    int lim = 0;
     if (withK) lim = box_origin(d, 0, ox0, oy0);
-    const T *Xb = X + ox0;
-    const T *Yb = Y + oy0;
 
     box_tables<KT, NTH>(d, tid, kX, kY, kco);
-    tile_tables<MT, NT, NTH>(d, t / d.tilesY, t % d.tilesY, tid, rowX[0], offCx[0], rowY[0],
+    TileBase cb = tile_base<MT, NT>(d, t / d.tilesY, t % d.tilesY);
+    tile_tables<MT, NT, NTH>(d, t / d.tilesY, t % d.tilesY, cb, tid, rowX[0], offCx[0], rowY[0],
                              offCy[0]);
     __syncthreads();
 
@@ -1033,8 +1102,8 @@ gett_stream_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
     if (withK) {
         gx.setup(tid, rowX[0], kX, kco, d.xscalar_kfast);
         gy.setup(tid, rowY[0], kY, kco, d.yscalar_kfast, d.yes);
-        gx.load(Xb, lim);
-        gy.load(Yb, lim);
+        gx.load(X + (cb.x + ox0), lim);
+        gy.load(Y + (cb.y + oy0), lim);
         gx.store(xs);
         gy.store(ys);
     }
@@ -1044,16 +1113,18 @@ gett_stream_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
         const int cur = j & 1;
         const int tn = t + G;
         const bool more = tn < ntiles;
+        TileBase nb = cb;
         if (more) {
-            tile_tables<MT, NT, NTH>(d, tn / d.tilesY, tn % d.tilesY, tid, rowX[cur ^ 1],
+            nb = tile_base<MT, NT>(d, tn / d.tilesY, tn % d.tilesY);
+            tile_tables<MT, NT, NTH>(d, tn / d.tilesY, tn % d.tilesY, nb, tid, rowX[cur ^ 1],
                                      offCx[cur ^ 1], rowY[cur ^ 1], offCy[cur ^ 1]);
         }
         __syncthreads();
         if (more && withK) {
             gx.setup(tid, rowX[cur ^ 1], kX, kco, d.xscalar_kfast);
             gy.setup(tid, rowY[cur ^ 1], kY, kco, d.yscalar_kfast, d.yes);
-            gx.load(Xb, lim);
-            gy.load(Yb, lim);
+            gx.load(X + (nb.x + ox0), lim);
+            gy.load(Y + (nb.y + oy0), lim);
         }
         w.zero();
         if (withK) w.template macro<GX::PITCH, GY::PITCH>(xs, ys);
@@ -1062,7 +1133,8 @@ gett_stream_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
             gx.store(xs);
             gy.store(ys);
         }
-        w.unpack(C, offCx[cur], offCy[cur], alpha, beta, d.cvec != 0);
+        w.unpack(C + (cb.cx + cb.cy), offCx[cur], offCy[cur], alpha, beta, d.cvec != 0);
+        cb = nb;
         __syncthreads();
     }
 }

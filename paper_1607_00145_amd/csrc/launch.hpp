@@ -89,4 +89,9 @@ LaunchFn pick_modes(int xm, int ym, int kind)
     return nullptr;
 }
 
+// The launchers of one tile shape.  Each (dtype, tile) pair is compiled in a
+// translation unit of its own (launch_f32.hip / launch_f64.hip built once per
+// tile with GETT_TILE defined), so the instantiations build in parallel.
+template <typename T, int TI> LaunchFn pick_tile(int xm, int ym, int kind);
+
 }  // namespace gett

@@ -238,7 +238,7 @@ gett_status_t gett_log_plan(gett_log_plan_t *plan, gett_dtype_t dtype, const cha
         int rank[3];
         p->dtype = dtype;
         st = gett::front_end(p->an, dtype, modes_C, extent_C, stride_C, modes_A, extent_A, stride_A,
-                             modes_B, extent_B, stride_B, rank);
+                             modes_B, extent_B, stride_B, rank, true);
         if (st == GETT_SUCCESS) {
             for (auto *s : {&p->an.Im, &p->an.In})
                 for (auto &x : *s) {

@@ -45,6 +45,20 @@ struct Choice {
     bool timing;          // a candidate being timed: overrides the test hooks
 };
 
+// Test and tuning hooks: environment variables that override the model's
+// choices (GETT_FORCE_TILE, GETT_FORCE_KIND, GETT_FORCE_KSLICES,
+// GETT_SPLIT_F, GETT_C_ORDER, GETT_XCD_REMAP, GETT_LANE_PERM,
+// GETT_TAIL_WGS), read once per plan.  `text` names the ones set: it is part
+// of the key under which a tuned choice is remembered, so a choice timed under
+// one setting is not reused under another.
+struct Hooks {
+    const char *forceTile = nullptr, *forceKind = nullptr, *forceKslices = nullptr,
+               *splitF = nullptr, *cOrder = nullptr, *xcdRemap = nullptr, *lanePerm = nullptr,
+               *tailWgs = nullptr;
+    std::string text;
+};
+Hooks read_hooks();
+
 typedef hipError_t (*LaunchFn)(const KDesc &, const void *, const void *, void *, double, double,
                                hipStream_t);
 
@@ -70,16 +84,20 @@ struct gett_plan_s {
     double flops;            // 2 * S_Im * S_In * S_Ik (Eq. 14)
     double bytesAlgo;        // |A| + |B| + |C| (+|C| when beta may be read)
     std::string text;        // JSON description
+    std::string hooks;       // the test / tuning hooks in force when planned (Hooks::text)
 };
 
 namespace gett {
 
 // Parse and validate the three mode lists, classify the indices into I_m,
-// I_n, I_k, drop extent-1 indices and merge super-indices (shared by GETT and
-// TTGT).  rank receives the number of modes of C, A, B as given.
+// I_n, I_k, drop extent-1 indices and merge super-indices (shared by GETT,
+// TTGT and LoG).  rank receives the number of modes of C, A, B as given.
+// offsets31: refuse tensors whose largest element offset reaches 2^31 - 1
+// (the methods that address with 32-bit offsets throughout).
 gett_status_t front_end(Analysis &an, gett_dtype_t dtype, const char *mC, const int64_t *eC,
                         const int64_t *sC, const char *mA, const int64_t *eA, const int64_t *sA,
-                        const char *mB, const int64_t *eB, const int64_t *sB, int rank[3]);
+                        const char *mB, const int64_t *eB, const int64_t *sB, int rank[3],
+                        bool offsets31);
 
 // Null, misaligned or overlapping operand pointers are refused (A and B only
 // matter when they are read).

@@ -114,3 +114,19 @@ def touched_mask(C: Operand):
         idx = idx + (np.arange(C.shape[ax]) * s).reshape(sh)
     m[C.offset + idx.reshape(-1)] = True
     return m
+
+
+def compare_whole(tC, w, A, B, Cin, chunk: int = 1 << 24) -> float:
+    """Every element of a dense column-major C on the device against the
+    oracle (all host threads), in chunks of `chunk` elements so the host
+    holds at most a chunk of out64 / den64 at a time.  Returns the largest
+    relative error; raises on a non-finite or mismatched element."""
+    nC = w.numel("C")
+    worst = 0.0
+    for lo in range(0, nC, chunk):
+        hi = min(nC, lo + chunk)
+        got = tC[lo:hi].cpu().numpy()
+        ref = oracle.contract(w.modes_C, w.modes_A, w.modes_B, A, B, w.alpha, w.beta, Cin,
+                              shape_C=w.shape("C"), points=np.arange(lo, hi, dtype=np.int64))
+        worst = max(worst, oracle.rel_error(got, ref))
+    return worst

@@ -190,10 +190,14 @@ def test_invalid_values_and_unsupported():
     st, _ = g.gett_plan(0, "m,n", [4, 4], [0, 4], "m,k", [4, 2], None, "k,n", [2, 4], None)
     assert st == 1                                                  # zero stride
     big = 1 << 16
-    st, _ = g.gett_plan(0, "m,n", [big, big], None, "m,k", [big, 2], None, "k,n", [2, big], None)
-    assert st == 3                                                  # C offsets beyond 2^31
-    modes = ",".join(f"i{i}" for i in range(13))
-    st, _ = g.gett_plan(0, modes, [1] * 13, None, "k,", [1], None, "k,", [1], None)
+    st, h = g.gett_plan(0, "m,n", [big, big], None, "m,k", [big, 2], None, "k,n", [2, big], None)
+    assert st == 0                                                  # C of 2^32 elements
+    g.gett_destroy(h)
+    st, _ = g.gett_plan(0, "m,n", [1 << 20, 4], [1, 1 << 30], "m,k", [1 << 20, 2], None, "k,n",
+                        [2, 4], None)
+    assert st == 3                                                  # one tile spans > 2^31
+    modes = ",".join(f"i{i}" for i in range(17))
+    st, _ = g.gett_plan(0, modes, [1] * 17, None, "k,", [1], None, "k,", [1], None)
     assert st == 3                                                  # rank > GETT_MAX_RANK
 
 
@@ -424,7 +428,7 @@ def test_transpose_host_side_errors():
     assert g.gett_transpose(f32, [2, 3], None, [3, 1], 1, 0, 0, Q) == E
     assert g.gett_transpose(f32, [2, 3], None, [3, 1], 1, P + 2, 0, Q) == E
     assert g.gett_transpose(f32, [2, 3], None, [3, 1], 1, P, 0, P + 8) == E        # overlap
-    assert g.gett_transpose(f32, [2] * 13, None, None, 1, P, 0, Q) == g.GETT_ERROR_NOT_SUPPORTED
+    assert g.gett_transpose(f32, [2] * 17, None, None, 1, P, 0, Q) == g.GETT_ERROR_NOT_SUPPORTED
     assert g.gett_transpose(f32, [2, 2], None, [1, 1], 1, P, 0, Q) == \
         g.GETT_ERROR_NOT_SUPPORTED                                                 # not injective
     assert g.gett_transpose(f32, [1 << 16, 1 << 16], None, None, 1, P, 0, Q) == \
@@ -525,3 +529,17 @@ def test_log_contract_host_side_errors():
     finally:
         g.gett_log_destroy(h)
     assert g.gett_log_describe(None) == "" and g.gett_log_destroy(None) == 0
+
+
+@pytest.mark.parametrize("variant", ["8x8x8", "15x1x1"])
+@pytest.mark.parametrize("dtype", [g.GETT_FLOAT32, g.GETT_FLOAT64])
+def test_rank16_plans_keep_every_index(variant, dtype):
+    """Tensors of 16 modes (GETT_MAX_RANK; Sec. 2.2 allows any order) plan
+    with every index kept: no two indices of a set are memory neighbours in
+    all the tensors that hold them."""
+    mc, ma, mb, ext = wl.rank16_problem(variant)
+    d = describe(mc, ma, mb, ext, dtype=dtype)
+    sizes = {"8x8x8": (8, 8, 8), "15x1x1": (15, 1, 1)}[variant]
+    assert (len(d["I_m"]), len(d["I_n"]), len(d["I_k"])) == sizes
+    assert d["merges"] == []
+    assert max(len(d["x_order"]), len(d["y_order"])) == max(sizes[0], sizes[1])

@@ -11,8 +11,8 @@ import pytest
 import oracle
 import paper_1607_00145_amd as g
 import workloads as wl
-from gpu_util import TOL, Operand, make_operand, reference, result_view, run_gpu, split, \
-    touched_mask
+from gpu_util import TOL, Operand, compare_whole, make_operand, reference, result_view, \
+    run_gpu, split, touched_mask
 
 pytestmark = pytest.mark.gpu
 DTYPES = [np.float32, np.float64]
@@ -84,10 +84,11 @@ def test_workload_structure_scaled(gpu, number):
 
 
 @pytest.mark.parametrize("number", [1, 2, 3, 4, 5])
-def test_workload_full_size_sampled(gpu, number):
-    """Full-size workloads in the benchmark's launch configuration; the
-    oracle checks 4096 sampled elements; for beta == 0 (C pre-filled with NaN)
-    every element must have been written."""
+def test_workload_full_size_whole(gpu, number):
+    """Full-size workloads in the benchmark's launch configuration, every
+    element of C against the oracle (Sec. 7: the naive loop nest as the
+    correctness reference).  For beta == 0 C starts as NaN, so an element
+    never written would also fail."""
     import torch
     w = wl.WORKLOADS[number - 1]
     A, B, Cin = wl.make_inputs(w)
@@ -108,14 +109,11 @@ def test_workload_full_size_sampled(gpu, number):
     assert st == 0
     torch.cuda.synchronize()
     g.gett_destroy(h)
+    del tA, tB
     if Cin is None:
         assert bool(torch.isfinite(tC).all()), "some element of C was not written"
-    rng = np.random.default_rng(w.seed + 99)
-    pts = np.concatenate([rng.integers(0, nC, 4090), [0, nC - 1, 1, nC - 2, nC // 2, 12345]])
-    got = tC[torch.from_numpy(pts).to(dev)].cpu().numpy()
-    ref = oracle.contract(w.modes_C, w.modes_A, w.modes_B, A, B, w.alpha, w.beta, Cin,
-                          shape_C=w.shape("C"), points=pts)
-    err = oracle.rel_error(got, ref)
+    err = compare_whole(tC, w, A, B, Cin)
+    print(f"{w.name}: {nC} elements, max rel err {err:.3e}", flush=True)
     assert err <= TOL[w.np_dtype], f"{w.name}: rel err {err:.3e}"
 
 
@@ -227,25 +225,26 @@ def test_streaming_kernel_many_tiles_per_workgroup(gpu, monkeypatch, number):
                (w.shape("C"), w.shape("A"), w.shape("B")), w.np_dtype, w.alpha, w.beta)
 
 
-@pytest.mark.parametrize("dtype", DTYPES)
-def test_largest_supported_offsets(gpu, dtype):
-    """C with 2^31 - 2^16 elements (element offsets up to just below 2^31, the
-    largest the plan accepts): every element written, sampled values against
-    the oracle, the far corner included.  One more row of C is refused."""
+@pytest.mark.parametrize("dtype,c_layout", [(np.float32, "col"), (np.float32, "row"),
+                                            (np.float64, "col")])
+def test_beyond_2_31_elements(gpu, dtype, c_layout):
+    """C with 2^31 + 2^24 elements (8 GiB in fp32, 16 GiB in fp64): the tiles
+    are reached through 64-bit base offsets (Sec. 2.2 allows tensors of any
+    size).  C starts as NaN; every element is compared with the oracle.  With
+    the row layout (n stride-one) the row offsets of C exceed 2^31 too."""
     import torch
-    m, n, k = 65536, 32767, 8
-    tdt = torch.float32 if dtype == np.float32 else torch.float64
+    m, n, k = 65536, 32768 + 256, 8
+    w = wl.Workload(900, "mn_2p31", "f32" if dtype == np.float32 else "f64", "m,n", "m,k",
+                    "k,n", {"m": m, "n": n, "k": k})
+    A, B, _ = wl.make_inputs(w)
     code = g.GETT_FLOAT32 if dtype == np.float32 else g.GETT_FLOAT64
-    st, h = g.gett_plan(code, "mn", [m, n + 1], None, "mk", [m, k], None, "kn", [k, n + 1], None, 0)
-    assert st == g.GETT_ERROR_NOT_SUPPORTED      # its last offset m * (n + 1) - 1 = 2^31 - 1
-    rng = np.random.default_rng(70_000)
-    A = rng.uniform(-1, 1, (m, k)).astype(dtype)
-    B = rng.uniform(-1, 1, (k, n)).astype(dtype)
+    strides = None if c_layout == "col" else [n, 1]
+    st, h = g.gett_plan(code, "m,n", [m, n], strides, "m,k", [m, k], None, "k,n", [k, n], None, 0)
+    assert st == 0, g.gett_status_string(st)
     tA = torch.from_numpy(np.asfortranarray(A).reshape(-1, order="F")).to(gpu)
     tB = torch.from_numpy(np.asfortranarray(B).reshape(-1, order="F")).to(gpu)
+    tdt = torch.float32 if dtype == np.float32 else torch.float64
     tC = torch.full((m * n,), float("nan"), dtype=tdt, device=gpu)
-    st, h = g.gett_plan(code, "mn", [m, n], None, "mk", [m, k], None, "kn", [k, n], None, 0)
-    assert st == 0
     try:
         st = g.gett_contract(h, 1.0, tA.data_ptr(), tB.data_ptr(), 0.0, tC.data_ptr(),
                              torch.cuda.current_stream().cuda_stream)
@@ -254,11 +253,23 @@ def test_largest_supported_offsets(gpu, dtype):
     finally:
         g.gett_destroy(h)
     assert bool(torch.isfinite(tC).all()), "some element of C was not written"
-    nC = m * n
-    pts = np.concatenate([rng.integers(0, nC, 2040),
-                          [0, 1, m - 1, m, nC // 2, nC - m, nC - 2, nC - 1]])
-    got = tC[torch.from_numpy(pts).to(gpu)].cpu().numpy()
+    if c_layout == "row":   # bring C to column-major order for the comparison
+        tC = tC.view(m, n).t().contiguous().view(-1)
+        torch.cuda.synchronize()
+    err = compare_whole(tC, w, A, B, None, chunk=1 << 26)
     del tC
     torch.cuda.empty_cache()
-    ref = oracle.contract("mn", "mk", "kn", A, B, 1.0, 0.0, None, shape_C=[m, n], points=pts)
-    assert oracle.rel_error(got, ref) <= TOL[dtype]
+    assert err <= TOL[dtype], f"rel err {err:.3e}"
+
+
+@pytest.mark.parametrize("variant", ["8x8x8", "15x1x1"])
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("kinds", [("dense",) * 3, ("permuted", "gapped", "permuted")])
+def test_rank16(gpu, variant, dtype, kinds):
+    """Tensors of 16 modes, every index kept by the plan, against the oracle
+    (dense and permuted / gapped layouts; with permuted layouts some indices
+    may merge)."""
+    mc, ma, mb, ext = wl.rank16_problem(variant)
+    rng = np.random.default_rng(90_000 + len(mc))
+    shp = lambda m: [ext[x] for x in split(m)]
+    check_case(gpu, rng, (mc, ma, mb), (shp(mc), shp(ma), shp(mb)), dtype, -0.75, 1.5, kinds)

@@ -1,14 +1,13 @@
 """GPU parity over the Fig. 11 sweep (Sec. 7.3): both contractions, both
 precisions, every S_Ik from 8 to 1024 at full size (S_Im = S_In = 1152),
-in the plan the benchmark times.  The oracle checks 2048 sampled elements of
-C; C starts as NaN, so every element must have been written."""
+in the plan the benchmark times.  The oracle checks every element of C;
+C starts as NaN, so every element must also have been written."""
 import numpy as np
 import pytest
 
-import oracle
 import paper_1607_00145_amd as g
 import workloads as wl
-from gpu_util import TOL
+from gpu_util import TOL, compare_whole
 
 pytestmark = pytest.mark.gpu
 
@@ -36,10 +35,5 @@ def test_fig11_point(gpu, variant, dtype, k):
     finally:
         g.gett_destroy(h)
     assert bool(torch.isfinite(tC).all()), "some element of C was not written"
-    rng = np.random.default_rng(w.seed + 7)
-    pts = np.concatenate([rng.integers(0, nC, 2043), [0, 1, nC // 2, nC - 2, nC - 1]])
-    got = tC[torch.from_numpy(pts).to(gpu)].cpu().numpy()
-    ref = oracle.contract(w.modes_C, w.modes_A, w.modes_B, A, B, w.alpha, w.beta, None,
-                          shape_C=w.shape("C"), points=pts)
-    err = oracle.rel_error(got, ref)
+    err = compare_whole(tC, w, A, B, None)
     assert err <= TOL[w.np_dtype], f"{w.name}: rel err {err:.3e}"

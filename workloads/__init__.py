@@ -182,3 +182,33 @@ def random_problem(rng: np.random.Generator, max_rank: int = 6, max_ext: int = 5
     ma = list(Im + Ik); rng.shuffle(ma)
     mb = list(In + Ik); rng.shuffle(mb)
     return ",".join(mc), ",".join(ma), ",".join(mb), ext
+
+
+def rank16_problem(variant: str = "8x8x8"):
+    """Contractions whose tensors have 16 modes and whose index sets cannot
+    merge (no two indices of a set are neighbours in memory in every tensor
+    holding them), so the plan keeps every index:
+      "8x8x8"  I_m, I_n, I_k of 8 indices each; C interleaves m and n, A
+               interleaves m and k, B holds k in reverse order between the n;
+      "15x1x1" C of 16 modes, 15 of them in I_m (A then has 16 modes).
+    Returns (modes_C, modes_A, modes_B, extents); a few extents are 3, the
+    rest 2."""
+    if variant == "8x8x8":
+        m = [f"m{i}" for i in range(8)]
+        n = [f"n{i}" for i in range(8)]
+        k = [f"k{i}" for i in range(8)]
+        mc = [x for pair in zip(m, n) for x in pair]
+        ma = [x for pair in zip(m, k) for x in pair]
+        mb = [x for pair in zip(list(reversed(k)), n) for x in pair]
+        ext = {x: 2 for x in m + n + k}
+        ext.update({"m0": 3, "n3": 3, "k2": 3})
+    elif variant == "15x1x1":
+        m = [f"m{i}" for i in range(15)]
+        mc = m[:7] + ["n"] + m[7:]
+        ma = ["k"] + list(reversed(m))
+        mb = ["n", "k"]
+        ext = {x: 2 for x in m}
+        ext.update({"n": 5, "k": 7, "m4": 3})
+    else:
+        raise ValueError(variant)
+    return ",".join(mc), ",".join(ma), ",".join(mb), ext
