@@ -83,16 +83,18 @@ typedef struct gett_plan_s *gett_plan_t;
  * the other so that both are read (written) in runs; with this flag the
  * tiles follow the (merged) indices whole. */
 #define GETT_FLAG_NO_SPLIT 4u
-/* Results identical from call to call: no K slices and no stream-K tail.
- * By default, when the tiles of C are too few to keep the GPU busy and the
- * contracted set is long, several workgroups share each tile's contracted
- * range (K slices); and when the tiles fill the workgroups the GPU holds at
- * once an uneven number of times, the contracted ranges of the tiles left
- * over from the last whole round are dealt in equal runs to one more round
- * of workgroups (stream-K tail).  Both add partial results into C with
- * atomic additions (after C, or those tiles of it, is set to beta * C), so
- * the order in which the partial sums meet varies between calls. */
-#define GETT_FLAG_DETERMINISTIC 8u
+/* Whole tiles only: no K slices and no stream-K tail, so a launch needs no
+ * workspace.  By default, when the tiles of C are too few to keep the GPU
+ * busy and the contracted set is long, several workgroups share each tile's
+ * contracted range (K slices); and when the tiles fill the workgroups the GPU
+ * holds at once an uneven number of times, the contracted ranges of the tiles
+ * left over from the last whole round are dealt in equal runs to one more
+ * round of workgroups (stream-K tail).  The partial tiles these produce are
+ * summed in a fixed order (see gett_contract), so results are identical from
+ * call to call with or without this flag. */
+#define GETT_FLAG_WHOLE_TILES 8u
+/* Former name of GETT_FLAG_WHOLE_TILES. */
+#define GETT_FLAG_DETERMINISTIC GETT_FLAG_WHOLE_TILES
 
 /*
  * gett_plan -- analyse a contraction and choose its kernel (Sec. 3.2-3.3).
@@ -140,6 +142,19 @@ gett_status_t gett_plan(gett_plan_t *plan, gett_dtype_t dtype,
  * returns.  A plan may be used from several host threads and streams at
  * once.  Pointers must be aligned to the element size; 16-byte aligned
  * pointers enable vector accesses.
+ *
+ * Workspace.  A plan with K slices or a stream-K tail (gett_plan_describe:
+ * "partials": "workspace") saves the partial tiles of a tile's pieces in
+ * device memory; the last piece of each tile to finish sums them in piece
+ * order and stores the tile (Listing 4 sums the contracted loop in order;
+ * this keeps the result independent of timing).  The library owns that
+ * memory: one set of buffers per device and stream, allocated (hipMalloc)
+ * by the first call that needs it or more of it, kept until the process
+ * ends.  Such a call synchronises `stream` and must not be inside a HIP graph
+ * capture -- capture a plan's calls after an eager call on the same stream.
+ * Calls on one stream share its buffers (they run in order); calls on
+ * different streams use different ones.  Errors: GETT_ERROR_HIP also when
+ * that allocation fails.
  */
 gett_status_t gett_contract(const gett_plan_t plan, double alpha, const void *A, const void *B,
                             double beta, void *C, void *stream);

@@ -26,7 +26,8 @@ GETT_FLAG_NONE = 0
 GETT_FLAG_NO_SWAP = 1
 GETT_FLAG_SCALAR = 2
 GETT_FLAG_NO_SPLIT = 4
-GETT_FLAG_DETERMINISTIC = 8
+GETT_FLAG_WHOLE_TILES = 8
+GETT_FLAG_DETERMINISTIC = GETT_FLAG_WHOLE_TILES   # former name
 GETT_MAX_RANK = 16
 GETT_METHOD_GETT = 0
 GETT_METHOD_TTGT = 1

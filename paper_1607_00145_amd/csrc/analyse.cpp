@@ -558,10 +558,15 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         return strOf(I[0]) == 1 || strOf(Ik[0]) == 1;
     };
     const bool slowGather = (flags & GETT_FLAG_SCALAR) || !vecable(Ix, sX) || !vecable(Iy, sY);
+    // Partial tiles (K slices, stream-K tail) are summed through the
+    // workspace: the stream of partial tiles and one workgroup's reads of a
+    // tile's pieces are priced at these rates (MI355X).
+    constexpr double kPartialBw = 5.0e12, kSumBw = 1.0e11;
     // Every (tile, kernel kind) pair is a candidate; the model ranks them.
     std::vector<Candidate> ranked;
     for (int t = 0; t < num_tiles(dtype); ++t) {
         const TileShape &c = tile_shape(dtype, t);
+        const double tileBytes = (double)c.mt * c.nt * itemB;
         // a one-box tile is ranked only for a contracted set in one box whose
         // operands are both gathered in vectors: it waits for each operand's
         // gathers in turn, which element-wise gathers make long (it still
@@ -635,15 +640,15 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         }
         // K slices: when a contracted set of many boxes meets too few tiles to
         // give every SIMD two wavefronts, P workgroups share each tile's
-        // boxes and add their partial tiles into C with atomics, after one
-        // pass that sets C to beta * C.  Priced like the macro-kernel on
-        // tiles * P workgroups with ceil(boxes / P) boxes each plus two
-        // boxes' worth of set-up and epilogue per workgroup, plus P atomic
-        // read-modify-writes of C, which add to the time (measured on
-        // MI355X: float atomics on distinct addresses sustain about
-        // 1.7 TB/s counting the read and the write), the scaling pass and
-        // its launch.  Each slice keeps at least eight boxes.
-        if (!(flags & GETT_FLAG_DETERMINISTIC) && !an.emptyC && waves < 2048.0 &&
+        // boxes.  Their partial tiles go to the workspace and the last of a
+        // tile's slices to finish sums the P of them in slice order.  Priced
+        // like the macro-kernel on tiles * P workgroups with ceil(boxes / P)
+        // boxes each plus two boxes' worth of set-up and epilogue per
+        // workgroup, plus the partial tiles' traffic, which adds to the time:
+        // P tile writes and reads per tile as a stream, and the last slice's
+        // P reads of one tile in turn.  Each slice keeps at least eight
+        // boxes.
+        if (!(flags & GETT_FLAG_WHOLE_TILES) && !an.emptyC && waves < 2048.0 &&
             b.nsteps >= 16) {
             Candidate best;
             best.tile = -1;
@@ -662,9 +667,10 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
                 const double tMemP = (bytesC + bytesX + bytesY +
                                       0.05 * (bytesX * (ty - 1) + bytesY * (tx - 1))) /
                                      (8.0e12 * c.bw * shareP);
-                const double tAtomic = bytesC * 2.0 * P / 1.7e12;
+                const double tPart =
+                    tx * ty * tileBytes * 2.0 * P / kPartialBw + P * tileBytes / kSumBw + 1.0e-6;
                 const double tChainP = chain(wgs, std::ceil((double)b.nsteps / P));
-                const double cost = bound(std::max(tM, tMemP), tChainP) + tAtomic + 3.0e-6;
+                const double cost = bound(std::max(tM, tMemP), tChainP) + tPart;
                 if (best.tile < 0 || cost < best.cost) {
                     best.tile = t;
                     best.kind = 2;
@@ -681,16 +687,16 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         // left alone on its SIMD runs slower than two together.  Instead, the
         // tiles of the complete rounds of G = 256 g workgroups run whole and
         // the boxes of the remaining ones are dealt in equal runs to G more
-        // workgroups (g = 1 .. the tile's occupancy; the best is kept), which
-        // add their partial tiles into C with atomics after one pass that
-        // sets those tiles to beta * C.  Priced by cu_time for the busiest CU
-        // (two boxes of set-up per piece), the atomics (about r + G
-        // tile-sized read-modify-writes, which add about the time of a
-        // 6.8 TB/s stream of their reads and writes: measured on MI355X,
-        // where they overlap the MFMAs of other workgroups) and the scaling
-        // pass's launch.
+        // workgroups (g = 1 .. the tile's occupancy; the best is kept); the
+        // pieces of a tile shared by several of them are summed through the
+        // workspace in piece order by the last to finish.  Priced by cu_time
+        // for the busiest CU (two boxes of set-up per piece), the partial
+        // tiles' traffic (about r + G tile-sized writes and reads, which add
+        // about the time of a 6.8 TB/s stream: measured on MI355X, where they
+        // overlap the MFMAs of other workgroups) and the last piece's reads of
+        // its tile's pieces.
         const double ntile = tx * ty;
-        if (c.tail && !(flags & GETT_FLAG_DETERMINISTIC) && !an.emptyC && wpt >= 4 &&
+        if (c.tail && !(flags & GETT_FLAG_WHOLE_TILES) && !an.emptyC && wpt >= 4 &&
             b.nsteps >= 16 && ntile > 256.0 && std::fmod(ntile, 256.0) > 0.0) {
             const int occ = (int)tail_occupancy(c, itemB);
             const double boxFlops = (double)(c.mt / c.wm) * (c.nt / c.wn) * c.kt * 2.0;
@@ -708,9 +714,9 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
                                              (int)std::ceil(ts.wgs / 256.0),
                                              (double)ts.len + 2.0 * pieces);
                 const double tM = units * boxTime;
-                const double tAtomic =
-                    (double)(ntile - ts.full + ts.wgs) * c.mt * c.nt * itemB * 2.0 / 6.8e12;
-                const double cost = bound(std::max(tM, tMem), tChain) + tAtomic + 3.0e-6;
+                const double tPart = (double)(ntile - ts.full + ts.wgs) * tileBytes * 2.0 / 6.8e12 +
+                                     pieces * tileBytes / kSumBw + 1.0e-6;
+                const double cost = bound(std::max(tM, tMem), tChain) + tPart;
                 if (best.tile < 0 || cost < best.cost) {
                     best.tile = t;
                     best.kind = 3;
@@ -750,7 +756,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
             // the stream-K tail on any plan of a tile that carries it (the
             // model ranks it only where it may pay)
             if (k == 3 && c->kind == 0 && tile_shape(dtype, t).tail && !an.emptyC &&
-                !(flags & GETT_FLAG_DETERMINISTIC))
+                !(flags & GETT_FLAG_WHOLE_TILES))
                 pick.kind = 3;
         }
     }
@@ -760,7 +766,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         const int P = atoi(fs);
         if (P == 1 && pick.kind == 2) {
             if (const Candidate *c = find(pick.tile, 0)) pick = *c;
-        } else if (P > 1 && pick.kind != 1 && !an.emptyC && !(flags & GETT_FLAG_DETERMINISTIC)) {
+        } else if (P > 1 && pick.kind != 1 && !an.emptyC && !(flags & GETT_FLAG_WHOLE_TILES)) {
             pick.kind = 2;
             pick.slices = P;
         }
@@ -1043,6 +1049,22 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     }
     if (!an.emptyC && tilesX * tilesY * kslices * ts.wm * ts.wn * 64 >= (int64_t)UINT32_MAX)
         return GETT_ERROR_NOT_SUPPORTED;
+    // Workspace of the partial tiles: a counter per tile that has pieces and
+    // a slot per piece (K slices: every slice of every tile; stream-K tail:
+    // slots up to (tail workgroups - 1) + (tail tiles - 1), see the kernel).
+    int64_t wsSlots = 0, wsCounters = 0;
+    if (!an.emptyC) {
+        const int64_t tiles = tilesX * tilesY;
+        if (kslices > 1) {
+            wsSlots = tiles * kslices;
+            wsCounters = tiles;
+        } else if (kind == 3) {
+            wsCounters = tiles - d.tailFull;
+            wsSlots = d.tailWgs + wsCounters - 1;
+        }
+    }
+    plan.wsCounters = (uint64_t)wsCounters;
+    plan.wsTileBytes = (uint64_t)wsSlots * ts.mt * ts.nt * (dtype == GETT_FLOAT32 ? 4 : 8);
 
     plan.dtype = dtype;
     plan.flags = flags;
@@ -1104,6 +1126,9 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
       << "\",\"kslices\":" << kslices;
     o << ",\"tail\":{\"full_tiles\":" << d.tailFull << ",\"workgroups\":" << d.tailWgs
       << ",\"boxes\":" << d.tailLen << "}";
+    o << ",\"partials\":\"" << (kslices > 1 || kind == 3 ? "workspace" : "none")
+      << "\",\"workspace_bytes\":" << plan.wsTileBytes
+      << ",\"workspace_counters\":" << plan.wsCounters;
     o << ",\"kbox\":{\"kj\":" << kj << ",\"tj\":" << tj << ",\"elements\":" << kbox << ",\"blocks\":" << nblk
       << ",\"steps\":" << nsteps << "}";
     o << ",\"gather_x\":\"" << mode_name(xmode) << "\",\"gather_y\":\"" << mode_name(ymode)

@@ -150,48 +150,8 @@ gett_status_t gett_contract(const gett_plan_t plan, double alpha, const void *A,
                             double beta, void *C, void *stream)
 {
     if (!plan) return GETT_ERROR_INVALID_VALUE;
-    const gett_plan_s &P = *plan;
-    if (P.an.emptyC) return GETT_SUCCESS;   // C has no elements
-    const bool readAB = alpha != 0.0 && !P.an.emptySum;
-    if (!pointers_ok(P, readAB, A, B, C)) return GETT_ERROR_INVALID_VALUE;
-
-    const void *X = P.an.swapped ? B : A;
-    const void *Y = P.an.swapped ? A : B;
-    KDesc d = P.desc;
-    int xmode = P.xmode, ymode = P.ymode;
-    // 16-byte vector accesses need 16-byte aligned base pointers.
-    if (xmode != gett::kGatherScalar && ((uintptr_t)X % 16)) xmode = gett::kGatherScalar;
-    if (ymode != gett::kGatherScalar && ((uintptr_t)Y % 16)) ymode = gett::kGatherScalar;
-    if (d.cvec && ((uintptr_t)C % 16)) d.cvec = 0;
-    // Tile walk across the XCDs: consecutive tiles on one XCD suits the
-    // compute-bound and write-only walks; a read-modify-write C stream
-    // (streaming walk, beta != 0) runs faster in hardware order (measured).
-    if (d.xcdremap < 0) d.xcdremap = (d.order == 1 && beta != 0.0) ? 0 : 1;
-    int kind = P.kind == 1 || P.kind == 3 ? P.kind : 0;
-    if (!readAB) {   // alpha == 0 or empty sum: C <- beta * C, A and B untouched
-        d.nsteps = 0;
-        d.kslices = 1;
-        if (kind == 3) kind = 0;
-        X = nullptr;
-        Y = nullptr;
-    }
-    gett::LaunchFn fn = gett::launch_fn(P.dtype, P.tile, xmode, ymode, kind);
-    gett::LaunchFn fn0 = kind == 3 ? gett::launch_fn(P.dtype, P.tile, xmode, ymode, 0) : fn;
-    if (!fn || !fn0) return GETT_ERROR_NOT_SUPPORTED;
-    if (inject_launch_fault()) return GETT_ERROR_HIP;
-    if ((d.kslices > 1 || kind == 3) && beta != 1.0) {
-        // K slices and the stream-K tail add into C: first C <- beta * C
-        // (C <- 0, unread, when beta == 0) over the tiles they add into, by
-        // the macro-kernel over no K boxes with alpha = 0
-        KDesc d0 = d;
-        d0.nsteps = 0;
-        d0.kslices = 1;
-        d0.tile0 = kind == 3 ? d.tailFull : 0;
-        const hipError_t e0 = fn0(d0, nullptr, nullptr, C, 0.0, beta, (hipStream_t)stream);
-        if (e0 != hipSuccess) return GETT_ERROR_HIP;
-    }
-    const hipError_t e = fn(d, X, Y, C, alpha, beta, (hipStream_t)stream);
-    return e == hipSuccess ? GETT_SUCCESS : GETT_ERROR_HIP;
+    return gett::contract_with(*plan, alpha, A, B, beta, C, (hipStream_t)stream,
+                               gett::stream_workspace);
 }
 
 gett_status_t gett_plan_tune(gett_plan_t plan, int max_candidates, const void *A, const void *B,
@@ -303,6 +263,46 @@ const char *gett_plan_describe(const gett_plan_t plan)
 }  // extern "C"
 
 namespace gett {
+
+gett_status_t contract_with(const gett_plan_s &P, double alpha, const void *A, const void *B,
+                            double beta, void *C, hipStream_t stream, WorkspaceFn ws)
+{
+    if (P.an.emptyC) return GETT_SUCCESS;   // C has no elements
+    const bool readAB = alpha != 0.0 && !P.an.emptySum;
+    if (!operands_ok(P.dtype, P.an, readAB, A, B, C)) return GETT_ERROR_INVALID_VALUE;
+
+    const void *X = P.an.swapped ? B : A;
+    const void *Y = P.an.swapped ? A : B;
+    KDesc d = P.desc;
+    int xmode = P.xmode, ymode = P.ymode;
+    // 16-byte vector accesses need 16-byte aligned base pointers.
+    if (xmode != kGatherScalar && ((uintptr_t)X % 16)) xmode = kGatherScalar;
+    if (ymode != kGatherScalar && ((uintptr_t)Y % 16)) ymode = kGatherScalar;
+    if (d.cvec && ((uintptr_t)C % 16)) d.cvec = 0;
+    // Tile walk across the XCDs: consecutive tiles on one XCD suits the
+    // compute-bound and write-only walks; a read-modify-write C stream
+    // (streaming walk, beta != 0) runs faster in hardware order (measured).
+    if (d.xcdremap < 0) d.xcdremap = (d.order == 1 && beta != 0.0) ? 0 : 1;
+    // launch variant: 0 whole tiles, 1 streaming, 2 K slices, 3 stream-K tail
+    int kind = P.kind == 1 || P.kind == 3 ? P.kind : d.kslices > 1 ? 2 : 0;
+    if (!readAB) {   // alpha == 0 or empty sum: C <- beta * C, A and B untouched
+        d.nsteps = 0;
+        d.kslices = 1;
+        if (kind == 3 || kind == 2) kind = 0;
+        X = nullptr;
+        Y = nullptr;
+    }
+    LaunchFn fn = launch_fn(P.dtype, P.tile, xmode, ymode, kind);
+    if (!fn) return GETT_ERROR_NOT_SUPPORTED;
+    if (inject_launch_fault()) return GETT_ERROR_HIP;
+    Partials part;
+    if (kind == 2 || kind == 3) {   // partial tiles, summed through the workspace
+        const gett_status_t st = ws(stream, P.wsCounters, P.wsTileBytes, part);
+        if (st != GETT_SUCCESS) return st;
+    }
+    const hipError_t e = fn(d, X, Y, C, alpha, beta, part, stream);
+    return e == hipSuccess ? GETT_SUCCESS : GETT_ERROR_HIP;
+}
 
 LaunchFn launch_fn_f32(int tile, int xm, int ym, int kind);
 LaunchFn launch_fn_f64(int tile, int xm, int ym, int kind);

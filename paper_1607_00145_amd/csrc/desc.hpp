@@ -65,7 +65,8 @@ struct KDesc {
     int32_t yes;                   // strided vector gathers of Y: distance between the
                                    // elements of one vector (extent of the first index)
     int32_t kslices;               // workgroups per tile, each summing an equal share of
-                                   // the K boxes into C with atomics (1: one per tile)
+                                   // the K boxes (1: one per tile); their partial tiles
+                                   // are summed in slice order through the workspace
     int32_t crun;                  // > 0: C's stride-one run along y, stored in C order
                                    // through LDS (E elements; 0: per-lane stores only)
     int32_t xperm, yperm;          // > 0: element-wise gathers of X (Y) walk the tile rows

@@ -68,6 +68,11 @@ __device__ __forceinline__ f64x4 mfma16x16x4(double a, double b, f64x4 c)
 
 constexpr int kInvalidK = 0x7fffffff;
 
+// s_waitcnt operand that waits for every vector memory operation of the
+// wavefront to complete (vmcnt 0) and leaves the other counters alone
+// (expcnt 7, lgkmcnt 15; gfx9 encoding).
+constexpr int kWaitStores = (7 << 4) | (15 << 8);
+
 // Map the hardware workgroup id to a tile.  Workgroups are dealt round-robin
 // to the 8 XCDs (each with its own L2); renumber so that consecutive logical
 // tiles run on one XCD.  Then either walk tiles in bands of `group` x-tiles,
@@ -773,26 +778,64 @@ struct WaveTile {
         }
     }
 
-    // One K slice's share of the tile: C += alpha * acc with hardware float
-    // atomics (C was set to beta * C beforehand; the slices of a tile add in
-    // whatever order they finish).
-    __device__ __forceinline__ void unpack_atomic(T *__restrict__ C, const int *offCx,
-                                                  const int *offCy, T alpha) const
+    // A partial tile (one piece of a tile's K boxes) in the workspace, in
+    // lane order: element r of accumulator (a, b) of thread tid at
+    // (((a CB + b) 4 + r) NTH + tid), so each store or load instruction of a
+    // wavefront covers 64 consecutive elements and any workgroup of the same
+    // kernel reads its own registers' values back.  Written and read with
+    // device-scope accesses (relaxed atomics at agent scope): they bypass the
+    // L2 of the XCD, which other XCDs do not see, so no cache-wide write-back
+    // or invalidation (a fence) is needed between workgroups.
+    template <int NTH>
+    __device__ __forceinline__ void save(T *__restrict__ slot, int tid) const
     {
 #pragma unroll
-        for (int grp = 0; grp < RB / RX; ++grp) {
-            int ox[NR];
-            rows_of(offCx, grp, ox);
-            int oy[CB];
+        for (int a = 0; a < RB; ++a)
 #pragma unroll
-            for (int b = 0; b < CB; ++b) oy[b] = offCy[wn * WTN + block_row<RY>(b, l16)];
+            for (int b = 0; b < CB; ++b)
 #pragma unroll
-            for (int q = 0; q < NR; ++q)
+                for (int r = 0; r < 4; ++r)
+                    __hip_atomic_store(slot + (size_t)(((a * CB + b) * 4 + r) * NTH + tid),
+                                       acc[a][b][r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    // acc <- sum of the np saved pieces at slot0 + p * step (p = 0 .. np - 1,
+    // added in that order), one row block at a time: the loads of a block
+    // from up to NPB pieces are issued together (the reads come from device
+    // memory; one round trip per block and group of pieces), and no more
+    // than that are in flight (all of them would take more registers than
+    // the accumulators).
+    template <int NTH>
+    __device__ __forceinline__ void sum_saved(const T *__restrict__ slot0, size_t step, int np,
+                                              int tid)
+    {
+        constexpr int NPB = 2;
 #pragma unroll
-                for (int b = 0; b < CB; ++b) {
-                    if (ox[q] < 0 || oy[b] < 0) continue;
-                    unsafeAtomicAdd(C + ox[q] + oy[b], alpha * acc[grp * RX + q / 4][b][q % 4]);
-                }
+        for (int a = 0; a < RB; ++a) {
+            for (int p0 = 0; p0 < np; p0 += NPB) {
+                T v[NPB][CB][4];
+#pragma unroll
+                for (int q = 0; q < NPB; ++q)
+                    if (p0 + q < np) {
+                        const T *slot = slot0 + (size_t)(p0 + q) * step;
+#pragma unroll
+                        for (int b = 0; b < CB; ++b)
+#pragma unroll
+                            for (int r = 0; r < 4; ++r)
+                                v[q][b][r] = __hip_atomic_load(
+                                    slot + (size_t)(((a * CB + b) * 4 + r) * NTH + tid),
+                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
+#pragma unroll
+                for (int q = 0; q < NPB; ++q)
+                    if (p0 + q < np) {
+#pragma unroll
+                        for (int b = 0; b < CB; ++b)
+#pragma unroll
+                            for (int r = 0; r < 4; ++r)
+                                acc[a][b][r] = p0 + q == 0 ? v[q][b][r] : acc[a][b][r] + v[q][b][r];
+                    }
+            }
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 };
@@ -848,20 +891,40 @@ __device__ __forceinline__ void unpack_c_order(const WT &w, T *__restrict__ C, T
 }
 
 // ---------------------------------------------------------------------------
+// How a piece of work ends: the whole tile stored with alpha / beta, or a
+// partial tile saved to workspace slot `slot`, the last of the tile's `np`
+// pieces to arrive (counter `ctr`) summing slots base + p * step,
+// p = 0 .. np - 1, in that order and storing the tile.
+struct Part {
+    enum { kWhole = 0, kSaved = 1 };
+    int how = kWhole;
+    int np = 1, slot = 0, base = 0, step = 1, ctr = 0;
+};
+
+// ---------------------------------------------------------------------------
 // The macro-kernel: one tile per workgroup, any number of K boxes, NBUF LDS
 // buffers (one suits a contracted set that fits one box).  With PF = 1 the gathers of box s+1 are issued before the MFMAs
 // of box s; with PF = 2 there are two register stages and the gathers of box
 // s+2 are issued before the MFMAs of box s, so a gather has two boxes' worth
 // of MFMA time to arrive before its values are written to LDS.
+//
+// Kernel variants: whole tiles (SLICED = TAIL = 0: one tile per workgroup,
+// from tile tile0 on), K slices (SLICED = 1) and the stream-K tail (TAIL = 1);
+// only the last two carry the partial-tile code (its registers would cost the
+// plain kernel occupancy or spills).
 template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int WPE, int PF,
-          int NBUF, int XMODE, int YMODE, int ONEBOX = 0, int CORDER = 0, int TAIL = 0>
+          int NBUF, int XMODE, int YMODE, int ONEBOX = 0, int CORDER = 0, int TAIL = 0,
+          int SLICED = 0>
 __global__ void __launch_bounds__(WM *WN * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
-                  T *__restrict__ C, const T alpha, const T beta)
+                  T *__restrict__ C, const T alpha, const T beta, T *__restrict__ W,
+                  int *__restrict__ cnt)
 {
     static_assert(PF == 1 || PF == 2, "prefetch depth");
     static_assert(NBUF == 2 || (NBUF == 1 && PF == 1), "one LDS buffer goes with one stage");
     static_assert(!ONEBOX || (NBUF == 1 && PF == 1), "the one-box kernel has one stage");
+    static_assert(!(TAIL && SLICED), "one variant at a time");
+    constexpr bool kPartials = TAIL || SLICED;
     constexpr int NTH = WM * WN * 64;
     typedef Gather<T, MT, KT, XMODE, NTH, PF> GX;
     typedef Gather<T, NT, KT, YMODE, NTH, PF> GY;
@@ -880,17 +943,21 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     __shared__ int kX[KT], kY[KT];
     __shared__ int kco[KT];
     __shared__ int permX[XMODE == kGatherScalar ? MT : 1], permY[YMODE == kGatherScalar ? NT : 1];
+    __shared__ int lastPiece;   // this workgroup holds the last piece of its tile to arrive
+    __shared__ int zeroLds;     // 0 (see the stream-K tail)
 
     const int tid = (int)threadIdx.x;
     const int ntiles = d.tilesX * d.tilesY;
     box_tables<KT, NTH>(d, tid, kX, kY, kco);
     WT w;
-    w.init(tid);
 
     // One piece of work: boxes [s0, s0 + nsteps) of the contracted set for
-    // tile `tile` (a tile id in the order tile_of_block deals them), stored
-    // with alpha / beta, or added into C with atomics when `atomic`.
-    auto piece = [&](int tile, uint32_t s0, uint32_t nsteps, bool atomic) {
+    // tile `tile` (a tile id in the order tile_of_block deals them), finished
+    // as `part` says: the whole tile stored with alpha / beta, or a partial
+    // tile summed in a fixed order through the workspace.  `tid` is the
+    // thread index (passed in: see the stream-K tail).
+    auto piece = [&](int tile, uint32_t s0, uint32_t nsteps, const Part &part, int tid) {
+        w.init(tid);
         int tx, ty;
         tile_of_block(d, tile, ntiles, tx, ty);
         const TileBase tb = tile_base<MT, NT>(d, tx, ty);
@@ -997,9 +1064,28 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
                 if (s + 1 < nsteps) step(S1(), s + 1);
             }
         }
-        if (atomic) {
-            w.unpack_atomic(Ct, offCx, offCy, alpha);
-            return;
+        if constexpr (kPartials) {
+        if (part.how == Part::kSaved) {
+            // Save this piece, count it; the last of the tile's pieces to
+            // arrive sums all of them in piece order (a sum that does not
+            // depend on which workgroup finished when) and stores the tile.
+            // The saved values are written device-wide; each wavefront waits
+            // until its stores have completed (vmcnt 0) before the barrier, so
+            // the count that follows it comes after all of them, and the last
+            // piece's device-wide reads come after the count.
+            w.template save<NTH>(W + (size_t)part.slot * (MT * NT), tid);
+            __builtin_amdgcn_s_waitcnt(kWaitStores);
+            __syncthreads();
+            if (tid == 0)
+                lastPiece = __hip_atomic_fetch_add(cnt + part.ctr, 1, __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_AGENT) == part.np - 1;
+            __syncthreads();
+            if (!lastPiece) return;
+            w.template sum_saved<NTH>(W + (size_t)part.base * (MT * NT),
+                                      (size_t)part.step * (MT * NT), part.np, tid);
+            if (tid == 0)   // zero again for the next call
+                __hip_atomic_store(cnt + part.ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
         }
         if constexpr (CORDER && WT::kVecC) {   // compiled only into the tiles that carry it
             if (d.crun > 0 && d.cvec) {
@@ -1017,37 +1103,71 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
         // Stream-K tail: workgroups below tailFull compute one whole tile
         // each; every later one sums a run of tailLen consecutive boxes of the
         // concatenated box sequences of the remaining tiles (the end of one
-        // tile and the start of the next, possibly) and adds its partial
-        // tiles into C with atomics (C of those tiles was set to beta * C
-        // beforehand).
+        // tile and the start of the next, possibly).  A run that holds a tail
+        // tile whole stores it; the pieces of a tile shared by several runs
+        // are summed through the workspace.  Piece p of tail tile u comes from
+        // run jf(u) + p, jf(u) = floor(u nb / tailLen), and is saved in slot
+        // jf(u) + p + u: slots grow with (u, p), so they are distinct.
+        //
+        // Both kinds of workgroup walk one loop (one copy of the piece code):
+        // positions are boxes of the concatenated sequences of all tiles; a
+        // whole-tile workgroup's run is its tile.  The thread index each
+        // piece sees is read through LDS, so the compiler keeps nothing
+        // derived from it alive from one piece to the next (across the K
+        // loop, where registers are short).
+        if (tid == 0) zeroLds = 0;
+        __syncthreads();
         const int bid = (int)blockIdx.x;
-        if (bid < d.tailFull) {
-            piece(bid, 0, (uint32_t)d.nsteps, false);
-            return;
-        }
         const uint64_t nb = (uint64_t)d.nsteps;
-        const uint64_t total = (uint64_t)(ntiles - d.tailFull) * nb;
-        uint64_t pos = (uint64_t)(bid - d.tailFull) * (uint64_t)d.tailLen;
-        const uint64_t end = min(pos + (uint64_t)d.tailLen, total);
+        const uint64_t L = (uint64_t)d.tailLen;
+        const uint64_t first = (uint64_t)d.tailFull * nb;   // first box of the tail tiles
+        const int j = bid - d.tailFull;                      // tail run (j >= 0)
+        uint64_t pos = j < 0 ? (uint64_t)bid * nb : first + (uint64_t)j * L;
+        const uint64_t end = j < 0 ? pos + nb : min(pos + L, (uint64_t)ntiles * nb);
         while (pos < end) {
             const uint64_t t = pos / nb;
             const uint32_t s0 = (uint32_t)(pos - t * nb);
             const uint32_t n = (uint32_t)min(nb - s0, end - pos);
-            piece(d.tailFull + (int)t, s0, n, true);
+            const uint64_t u = t - (uint64_t)d.tailFull;   // tail tile (when j >= 0)
+            Part part;
+            if (j >= 0 && n < nb) {
+                const int jf = (int)(u * nb / L);
+                const int jl = (int)(((u + 1) * nb - 1) / L);
+                part.how = Part::kSaved;
+                part.np = jl - jf + 1;
+                part.slot = j + (int)u;
+                part.base = jf + (int)u;
+                part.step = 1;
+                part.ctr = (int)u;
+            }
+            piece((int)t, s0, n, part, tid + *reinterpret_cast<volatile int *>(&zeroLds));
             pos += n;
-            __syncthreads();   // the next piece rewrites the tables and panels
+            if (pos < end) __syncthreads();   // the next piece rewrites the tables and panels
         }
+    } else if constexpr (!SLICED) {
+        // whole tiles: workgroup b computes tile tile0 + b (tile0 > 0 for a
+        // pass that scales the tail tiles of a stream-K plan)
+        piece(d.tile0 + (int)blockIdx.x, 0, (uint32_t)d.nsteps, Part{}, tid);
     } else {
-        // K slices: workgroup b computes slice b / tiles of tile tile0 + b % tiles
-        // (tiles = the tiles from tile0 on; tile0 > 0 for a pass that scales
-        // the tail tiles of a stream-K plan).
+        // K slices: workgroup b computes slice b / tiles of tile b % tiles.
+        // Slice p of tile u is saved in slot p * tiles + u.
         const int slices = d.kslices > 1 ? d.kslices : 1;
         const int span = ntiles - d.tile0;
         const int bid = (int)blockIdx.x;
         const int slice = slices > 1 ? bid / span : 0;
         const uint32_t s0 = (uint32_t)((uint64_t)d.nsteps * slice / slices);
         const uint32_t n = (uint32_t)((uint64_t)d.nsteps * (slice + 1) / slices) - s0;
-        piece(d.tile0 + bid - slice * span, s0, n, slices > 1);
+        const int u = bid - slice * span;
+        Part part;
+        if (slices > 1) {
+            part.how = Part::kSaved;
+            part.np = slices;
+            part.slot = slice * span + u;
+            part.base = u;
+            part.step = span;
+            part.ctr = u;
+        }
+        piece(d.tile0 + u, s0, n, part, tid);
     }
 }
 

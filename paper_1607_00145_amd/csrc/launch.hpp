@@ -34,20 +34,31 @@ unsigned persistent_grid(K kernel, int threads, unsigned tiles)
 
 template <typename T, int TI, int XM, int YM, int KIND>
 hipError_t launch_one(const KDesc &d, const void *X, const void *Y, void *C, double alpha,
-                      double beta, hipStream_t stream)
+                      double beta, const Partials &w, hipStream_t stream)
 {
+    if ((KIND == 2 || KIND == 3) && (!w.tiles || !w.counters))
+        return hipErrorInvalidValue;   // partial tiles need the workspace
     constexpr TileShape t = TileTable<T>::tiles[TI];
     const unsigned tiles = (unsigned)d.tilesX * (unsigned)d.tilesY;
     if (tiles == 0) return hipSuccess;
     const int threads = t.wm * t.wn * 64;
     if constexpr (KIND == 0) {
+        if (d.kslices > 1) return hipErrorInvalidValue;   // the sliced variant (kind 2) does those
         if ((unsigned)d.tile0 >= tiles) return hipSuccess;
         hipLaunchKernelGGL(
             (gett_macro_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.wpe, t.pf, t.nbuf, XM,
                                YM, t.onebox, t.corder>),
-            dim3((tiles - (unsigned)d.tile0) * (unsigned)(d.kslices > 1 ? d.kslices : 1)),
-            dim3(threads), 0, stream, d, static_cast<const T *>(X), static_cast<const T *>(Y),
-            static_cast<T *>(C), static_cast<T>(alpha), static_cast<T>(beta));
+            dim3(tiles - (unsigned)d.tile0), dim3(threads), 0, stream, d,
+            static_cast<const T *>(X), static_cast<const T *>(Y), static_cast<T *>(C),
+            static_cast<T>(alpha), static_cast<T>(beta), static_cast<T *>(nullptr), nullptr);
+    } else if constexpr (KIND == 2) {
+        if (d.kslices < 2 || d.tile0 != 0) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(
+            (gett_macro_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.wpe, t.pf, t.nbuf, XM,
+                               YM, t.onebox, t.corder, 0, 1>),
+            dim3(tiles * (unsigned)d.kslices), dim3(threads), 0, stream, d,
+            static_cast<const T *>(X), static_cast<const T *>(Y), static_cast<T *>(C),
+            static_cast<T>(alpha), static_cast<T>(beta), static_cast<T *>(w.tiles), w.counters);
     } else if constexpr (KIND == 3) {
         if (d.tailFull < 0 || d.tailWgs < 1 || d.tailLen < 1 || (unsigned)d.tailFull >= tiles ||
             (uint64_t)d.tailWgs * (uint64_t)d.tailLen <
@@ -58,7 +69,7 @@ hipError_t launch_one(const KDesc &d, const void *X, const void *Y, void *C, dou
                                YM, t.onebox, t.corder, 1>),
             dim3((unsigned)d.tailFull + (unsigned)d.tailWgs), dim3(threads), 0, stream, d,
             static_cast<const T *>(X), static_cast<const T *>(Y), static_cast<T *>(C),
-            static_cast<T>(alpha), static_cast<T>(beta));
+            static_cast<T>(alpha), static_cast<T>(beta), static_cast<T *>(w.tiles), w.counters);
     } else {
         auto k = gett_stream_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.stream, XM, YM>;
         const unsigned grid = persistent_grid(k, threads, tiles);
@@ -78,6 +89,7 @@ LaunchFn pick_modes(int xm, int ym, int kind)
 #define GETT_CASE(a, b)                                                                       \
     if (xm == a && ym == b) {                                                                 \
         if (kind == 0) return &launch_one<T, TI, a, b, 0>;                                   \
+        if (kind == 2) return &launch_one<T, TI, a, b, 2>;                                   \
         if (kind == 1 && kStream) return &launch_one<T, TI, a, b, kStream ? 1 : 0>;          \
         if (kind == 3 && kTail) return &launch_one<T, TI, a, b, kTail ? 3 : 0>;              \
         return nullptr;                                                                       \

@@ -59,8 +59,23 @@ struct Hooks {
 };
 Hooks read_hooks();
 
+// Workspace of a launch: per-tile counters and partial-tile slots (null when
+// the plan has no partial tiles).
+struct Partials {
+    void *tiles = nullptr;
+    int *counters = nullptr;
+};
+
 typedef hipError_t (*LaunchFn)(const KDesc &, const void *, const void *, void *, double, double,
-                               hipStream_t);
+                               const Partials &, hipStream_t);
+
+// Device workspace for a launch's partial tiles: `counters` zeroed int32
+// counters and `tileBytes` bytes of slots, filled into `out`.
+typedef gett_status_t (*WorkspaceFn)(hipStream_t stream, uint64_t counters, uint64_t tileBytes,
+                                     Partials &out);
+// The library's own: a pair of buffers per (device, stream), grown on demand.
+gett_status_t stream_workspace(hipStream_t stream, uint64_t counters, uint64_t tileBytes,
+                               Partials &out);
 
 }  // namespace gett
 
@@ -85,6 +100,10 @@ struct gett_plan_s {
     double bytesAlgo;        // |A| + |B| + |C| (+|C| when beta may be read)
     std::string text;        // JSON description
     std::string hooks;       // the test / tuning hooks in force when planned (Hooks::text)
+    // device workspace a launch needs to sum its partial tiles in order (0, 0:
+    // none):
+    uint64_t wsCounters = 0;      // per-tile counters (int32, zero between launches)
+    uint64_t wsTileBytes = 0;     // partial-tile slots
 };
 
 namespace gett {
@@ -113,6 +132,10 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
                       const int64_t *sC, const char *mA, const int64_t *eA, const int64_t *sA,
                       const char *mB, const int64_t *eB, const int64_t *sB, uint32_t flags,
                       const Choice *force);
+
+// gett_contract with the workspace of partial tiles taken from `ws`.
+gett_status_t contract_with(const gett_plan_s &P, double alpha, const void *A, const void *B,
+                            double beta, void *C, hipStream_t stream, WorkspaceFn ws);
 
 // "macro", "stream", "kslices" or "tail" (Candidate::kind).
 const char *kind_name(int kind);

@@ -1,9 +1,11 @@
 """gett_contract under HIP graph capture (serving loops replay one captured
-contraction): a plain plan, a plan over K slices and one with a stream-K
-tail (two kernels each, the beta pass first) and an alpha = 0 call, each
-captured once and replayed several times
-with eager work between the replays; every replay must equal the eager
-result bit for bit (integer-valued inputs make the atomic sums exact)."""
+contraction): a plain plan, plans over K slices and with a stream-K tail
+(partial tiles summed through the library's workspace) and an alpha = 0
+call, each captured once and replayed several times with eager
+work between the replays; every replay must equal the eager result bit for
+bit (integer-valued inputs make every sum exact).  The eager call runs
+on the capture stream first: it allocates the stream's workspace, which a
+capture must not do."""
 import json
 
 import numpy as np
@@ -45,8 +47,9 @@ def test_graph_replay_matches_eager(gpu, monkeypatch, name, alpha, beta, dtype):
     nB = int(np.prod(shp(modes[2])))
     nC = int(np.prod(shp(modes[0])))
     A, B, C0 = rnd(nA), rnd(nB), rnd(nC)
+    flags = 0
     st, h = g.gett_plan(code, modes[0], shp(modes[0]), None, modes[1], shp(modes[1]), None,
-                        modes[2], shp(modes[2]), None, 0)
+                        modes[2], shp(modes[2]), None, flags)
     assert st == 0
     try:
         d = json.loads(g.gett_plan_describe(h))
@@ -54,16 +57,20 @@ def test_graph_replay_matches_eager(gpu, monkeypatch, name, alpha, beta, dtype):
             assert d["kslices"] > 1
         if name.startswith("tail"):
             assert d["kernel"] == "tail" and d["tail"]["full_tiles"] > 0
-        # eager reference
+        if d["kslices"] > 1 or d["kernel"] == "tail":
+            assert d["partials"] == "workspace"
+        # eager reference, on the stream that captures
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
         C = C0.clone()
+        torch.cuda.synchronize()
         assert g.gett_contract(h, alpha, A.data_ptr(), B.data_ptr(), beta, C.data_ptr(),
-                               torch.cuda.current_stream().cuda_stream) == 0
+                               side.cuda_stream) == 0
         torch.cuda.synchronize()
         ref = C.clone()
         # capture once
         Cg = C0.clone()
-        side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
+        torch.cuda.synchronize()
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.stream(side):
             with torch.cuda.graph(graph, stream=side):

@@ -1,6 +1,6 @@
 """GPU parity of K slices: several workgroups share one tile's contracted
-range and add their partial tiles into C with atomics, after a pass that
-sets C to beta * C.  Against the oracle for forced slice counts on random
+range; their partial tiles are summed in slice order through the library's
+workspace.  Against the oracle for forced slice counts on random
 contractions with long contracted sets, integer inputs (exact whatever the
 order of the additions), every beta path (beta = 0 with NaN in C, beta = 1
 with no scaling pass, any other beta), alpha = 0, more slices than K boxes,
@@ -52,6 +52,7 @@ def test_forced_slices(gpu, monkeypatch, name, slices, dtype):
     modes, ext = DEEP[name]
     d = describe(modes, ext, dtype)
     assert d["kslices"] == slices
+    assert d["partials"] == "workspace"
     rng = np.random.default_rng(1000 * slices + len(name))
     for alpha, beta in [(1.0, 0.0), (-0.75, 1.0), (1.5, -0.5)]:
         check_case(gpu, rng, modes, shapes(modes, ext), dtype, alpha, beta)

@@ -1,7 +1,7 @@
 """GPU parity of the stream-K tail: whole tiles for the complete rounds of
 workgroups, and the K boxes of the remaining tiles dealt in equal runs to
-further workgroups that add their partial tiles into C with atomics, after a
-pass that sets those tiles to beta * C.  Against the oracle with the tail
+further workgroups whose partial tiles are summed in piece order through the
+library's workspace.  Against the oracle with the tail
 kernel forced on tiles that carry it and the tail spread over a chosen number
 of workgroups (runs that end inside a tile, runs that cover several tiles,
 one workgroup for all of it), every beta path, alpha = 0, integer inputs
@@ -26,7 +26,7 @@ CASES = {
                        {"a": 23, "b": 17, "i": 19, "j": 21, "e": 13, "f": 11}),
     "ab-ak-kb": (("a,b", "a,k", "k,b"), {"a": 300, "b": 290, "k": 333}),
     "abc-adc-db": (("a,b,c", "a,d,c", "d,b"), {"a": 45, "b": 200, "c": 7, "d": 150}),
-    # one K box: every tail run is whole tiles, added with atomics
+    # one K box: every tail run is whole tiles
     "abcd-aeb-edc": (("a,b,c,d", "a,e,b", "e,d,c"), {"a": 30, "b": 17, "c": 29, "d": 31, "e": 16}),
 }
 
@@ -70,7 +70,9 @@ def check_cover(d):
 def test_forced_tail(gpu, monkeypatch, name, wgs, dtype):
     force_tail(monkeypatch, dtype, wgs)
     modes, ext = CASES[name]
-    check_cover(describe(modes, ext, dtype))
+    d = describe(modes, ext, dtype)
+    check_cover(d)
+    assert d["partials"] == "workspace"
     rng = np.random.default_rng(100 * wgs + len(name))
     for alpha, beta in [(1.0, 0.0), (-0.75, 1.0), (1.5, -0.5)]:
         check_case(gpu, rng, modes, shapes(modes, ext), dtype, alpha, beta)

@@ -66,3 +66,22 @@ def test_single_box_and_empty_cases_are_not_sliced():
     assert st == 0
     assert json.loads(g.gett_plan_describe(h))["kslices"] == 1
     g.gett_destroy(h)
+
+
+def test_slice_workspace_layout(monkeypatch):
+    """K slices sum through the workspace: one counter per tile, one slot per
+    (slice, tile) -- slot p * tiles + u for slice p of tile u, distinct by
+    construction -- sized tiles x slices tile-sized slots."""
+    w = wl.WORKLOADS[4]
+    monkeypatch.setenv("GETT_FORCE_KSLICES", "6")
+    d = describe(w)
+    tiles = d["grid"]["workgroups"]
+    tile_bytes = d["tile"]["mt"] * d["tile"]["nt"] * 4
+    assert d["partials"] == "workspace"
+    assert d["workspace_counters"] == tiles
+    assert d["workspace_bytes"] == 6 * tiles * tile_bytes
+    slots = {p * tiles + u for p in range(6) for u in range(tiles)}
+    assert len(slots) == 6 * tiles and max(slots) < 6 * tiles
+    monkeypatch.setenv("GETT_FORCE_KSLICES", "1")
+    n = describe(w)
+    assert n["partials"] == "none" and n["workspace_bytes"] == 0
