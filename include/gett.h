@@ -160,6 +160,31 @@ gett_status_t gett_contract(const gett_plan_t plan, double alpha, const void *A,
                             double beta, void *C, void *stream);
 
 /*
+ * gett_contract_noalloc -- gett_contract that allocates no device memory.
+ *
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture (no eager call is needed first), tight serving loops, harnesses
+ * that forbid hipMalloc.  The same kernels as gett_contract (bit-identical
+ * results), but the partial tiles of K slices and of the stream-K tail go to
+ * a fixed buffer the library holds on each GPU it runs on until the process
+ * ends: 64 MiB of partial-tile slots and 65536 per-tile counters.  Each call
+ * first zeroes the counters its plan uses (a small kernel on `stream`).
+ * Every call on one GPU shares that buffer and leaves its contents behind:
+ * calls that overlap in time on one GPU (several streams, several host
+ * threads) race and must be serialised by the caller, e.g. on one stream.
+ *
+ * Arguments, pointer rules and asynchrony as for gett_contract.  Errors as
+ * for gett_contract, and GETT_ERROR_NOT_SUPPORTED, before any launch, for a
+ * plan whose partial tiles need more than the buffer holds
+ * (gett_plan_describe: "workspace_bytes" above 64 MiB or
+ * "workspace_counters" above 65536); GETT_ERROR_HIP when the buffer's
+ * address cannot be obtained.  Calls no hipMalloc, hipFree or allocating
+ * library routine.
+ */
+gett_status_t gett_contract_noalloc(const gett_plan_t plan, double alpha, const void *A,
+                                    const void *B, double beta, void *C, void *stream);
+
+/*
  * gett_plan_tune -- time the plan's best candidates and keep the fastest.
  *
  * gett_plan ranks every compiled kernel candidate (tile shape x kernel kind)

@@ -71,6 +71,8 @@ def load_library() -> ctypes.CDLL:
     lib.gett_contract.argtypes = [ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p,
                                   ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p,
                                   ctypes.c_void_p]
+    lib.gett_contract_noalloc.restype = ctypes.c_int
+    lib.gett_contract_noalloc.argtypes = lib.gett_contract.argtypes
     lib.gett_plan_tune.restype = ctypes.c_int
     lib.gett_plan_tune.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
@@ -164,6 +166,14 @@ def gett_contract(plan, alpha: float, A: int, B: int, beta: float, C: int, strea
     """Device pointers as integers; stream as a hipStream_t integer (0 = default)."""
     return load_library().gett_contract(plan, float(alpha), A or None, B or None, float(beta),
                                         C or None, stream or None)
+
+
+def gett_contract_noalloc(plan, alpha: float, A: int, B: int, beta: float, C: int,
+                          stream: int = 0) -> int:
+    """gett_contract with the partial-tile workspace taken from the library's
+    fixed static buffer (no device allocation).  Arguments as gett_contract."""
+    return load_library().gett_contract_noalloc(plan, float(alpha), A or None, B or None,
+                                                float(beta), C or None, stream or None)
 
 
 def gett_plan_tune(plan, max_candidates: int, A: int, B: int, C: int, stream: int = 0) -> int:

@@ -26,7 +26,8 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = g.load_library()
     names = declared_functions()
-    assert names == sorted(["gett_plan", "gett_contract", "gett_plan_tune", "gett_destroy",
+    assert names == sorted(["gett_plan", "gett_contract", "gett_contract_noalloc",
+                            "gett_plan_tune", "gett_destroy",
                             "gett_status_string", "gett_plan_describe", "gett_transpose",
                             "gett_ttgt_plan", "gett_ttgt_workspace_size", "gett_ttgt_contract",
                             "gett_ttgt_destroy", "gett_ttgt_describe", "gett_log_plan",
