@@ -207,11 +207,27 @@ struct Gather {
     static constexpr int ITEMS = ROWS * KT / W;
     static constexpr int NI = (ITEMS + NTH - 1) / NTH;
     static constexpr bool kFull = ITEMS % NTH == 0;
+    // Swizzle of the k-vector gather: the VW elements of a vector go to VW
+    // LDS lines (one per contracted position), all at one row; without it
+    // the lines of the vectors a wavefront stores start at two banks only
+    // (the pitch is ROWS + VW), so these stores conflict 4-way.  Row r of
+    // line k is stored at row swz(r, k) = r ^ (VW * ((k / 4) mod 8)): lines
+    // of different groups of four shift by whole vectors, a vector's VW
+    // elements share the shift (VW divides 4), and a VW-row piece stays
+    // contiguous for the MFMA reads, which apply the same bijection (for the
+    // rows of one MFMA step the shift is a constant).
+    static constexpr bool kSwz = MODE == kGatherKVec && ROWS % (8 * VW) == 0;
+    static __device__ __forceinline__ int swz(int r, int k)
+    {
+        return kSwz ? r ^ (VW * ((k >> 2) & 7)) : r;
+    }
     // Consecutive items of one thread sit a fixed LDS distance apart when the
-    // workgroup covers whole rows (or whole K lines) per item round.
+    // workgroup covers whole rows (or whole K lines) per item round (and, with
+    // the swizzle, the rows of one round are a multiple of the shifted span).
     static constexpr bool kConst =
         NI <= 1 || (kFull && (kRowV ? NTH % (ROWS / VW) == 0
-                              : kKV ? NTH % (KT / VW) == 0
+                              : kKV ? NTH % (KT / VW) == 0 &&
+                                          (!kSwz || (NTH / (KT / VW)) % (8 * VW) == 0)
                                     : NTH % KT == 0 && NTH % ROWS == 0));
     typedef typename Traits<T>::vec vec;
 
@@ -263,7 +279,7 @@ struct Gather {
             const int ro = act ? rowoff[r] : -1;
             goff[it] = (ro < 0 ? 0 : ro) + (act ? koff[kk] : 0);
             kc[it] = ro < 0 ? kInvalidK : kco[kk];
-            const int slot = act ? kk * PITCH + r : -1;
+            const int slot = act ? kk * PITCH + swz(r, kk) : -1;
             if (kConst) {
                 if (it == 0) lds[0] = slot;
                 if (it == 1) lstep = slot - lds[0];
@@ -576,11 +592,22 @@ struct WaveTile {
     // while the MFMAs of step ks are issued (scheduling groups interleave
     // them), so one wavefront alone on its SIMD does not wait for LDS between
     // steps.
-    template <int PX, int PY, bool FIRST = false, int KU = 0, bool PIPE = false>
+    // SX / SY: the panel was stored with the k-vector swizzle (Gather::swz):
+    // row r of line k sits at r ^ (VW * ((k / 4) mod 8)); the lines of MFMA
+    // step ks are 4 ks .. 4 ks + 3, so the shift of a step is VW * (ks mod 8).
+    template <int PX, int PY, bool FIRST = false, int KU = 0, bool PIPE = false, bool SX = false,
+              bool SY = false>
     __device__ __forceinline__ void macro(const T *xs, const T *ys)
     {
-        const T *xt = xs + wm * WTM + RX * l16;
-        const T *yt = ys + wn * WTN + RY * l16;
+        const int xr = wm * WTM + RX * l16, yr = wn * WTN + RY * l16;
+        auto xat = [&](int ks, int k, int gi) {
+            const int r = xr + gi * 16 * RX;
+            return xs + k * PX + (SX ? r ^ (VW * (ks & 7)) : r);
+        };
+        auto yat = [&](int ks, int k, int gj) {
+            const int r = yr + gj * 16 * RY;
+            return ys + k * PY + (SY ? r ^ (VW * (ks & 7)) : r);
+        };
         if constexpr (PIPE) {
             typename XV::type av[2][RB / RX];
             typename YV::type bv[2][CB / RY];
@@ -588,12 +615,10 @@ struct WaveTile {
                 const int k = 4 * ks + g;
 #pragma unroll
                 for (int gi = 0; gi < RB / RX; ++gi)
-                    av[buf][gi] =
-                        *reinterpret_cast<const typename XV::type *>(xt + k * PX + gi * 16 * RX);
+                    av[buf][gi] = *reinterpret_cast<const typename XV::type *>(xat(ks, k, gi));
 #pragma unroll
                 for (int gj = 0; gj < CB / RY; ++gj)
-                    bv[buf][gj] =
-                        *reinterpret_cast<const typename YV::type *>(yt + k * PY + gj * 16 * RY);
+                    bv[buf][gj] = *reinterpret_cast<const typename YV::type *>(yat(ks, k, gj));
             };
             constexpr int NREAD = RB / RX + CB / RY;   // LDS reads per step
             constexpr int NMFMA = RB * CB;             // MFMAs per step
@@ -628,10 +653,10 @@ struct WaveTile {
             typename YV::type bv[CB / RY];
 #pragma unroll
             for (int gi = 0; gi < RB / RX; ++gi)
-                av[gi] = *reinterpret_cast<const typename XV::type *>(xt + k * PX + gi * 16 * RX);
+                av[gi] = *reinterpret_cast<const typename XV::type *>(xat(ks, k, gi));
 #pragma unroll
             for (int gj = 0; gj < CB / RY; ++gj)
-                bv[gj] = *reinterpret_cast<const typename YV::type *>(yt + k * PY + gj * 16 * RY);
+                bv[gj] = *reinterpret_cast<const typename YV::type *>(yat(ks, k, gj));
 #pragma unroll
             for (int a = 0; a < RB; ++a)
 #pragma unroll
@@ -1003,7 +1028,7 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
                 gy.template load<0>(Yt + oy, lim);
                 gy.template store<0>(ys[0]);
                 __syncthreads();
-                w.template macro<GX::PITCH, GY::PITCH, true, 2>(xs[0], ys[0]);
+                w.template macro<GX::PITCH, GY::PITCH, true, 2, false, GX::kSwz, GY::kSwz>(xs[0], ys[0]);
             } else {
                 w.zero();
                 for (uint32_t s = 0; s < nsteps; ++s) {
@@ -1013,7 +1038,7 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
                     gx.copy(Xt + ox, lim, xs[0]);
                     gy.copy(Yt + oy, lim, ys[0]);
                     __syncthreads();
-                    w.template macro<GX::PITCH, GY::PITCH, false, 2>(xs[0], ys[0]);
+                    w.template macro<GX::PITCH, GY::PITCH, false, 2, false, GX::kSwz, GY::kSwz>(xs[0], ys[0]);
                 }
             }
         } else if constexpr (PF == 1) {
@@ -1029,8 +1054,8 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
                 if (more) fetch(S0(), s + 1);
                 // one wavefront per SIMD over 4-step boxes: reads interleaved
                 // with the MFMAs (measured faster there, not for 8-step boxes)
-                w.template macro<GX::PITCH, GY::PITCH, false, 0, WPE == 1 && KT == 16>(xs[buf],
-                                                                                  ys[buf]);
+                w.template macro<GX::PITCH, GY::PITCH, false, 0, WPE == 1 && KT == 16, GX::kSwz,
+                                 GY::kSwz>(xs[buf], ys[buf]);
                 if (NBUF == 1 && more) __syncthreads();   // the single buffer is free again
                 if (more) {
                     gx.template store<0>(xs[NBUF == 2 ? buf ^ 1 : 0]);
@@ -1045,7 +1070,8 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
             auto step = [&](auto stage, uint32_t s) {
                 constexpr int B = decltype(stage)::value;
                 if (s + 2 < nsteps) fetch(stage, s + 2);
-                w.template macro<GX::PITCH, GY::PITCH>(xs[B % NBUF], ys[B % NBUF]);
+                w.template macro<GX::PITCH, GY::PITCH, false, 0, false, GX::kSwz, GY::kSwz>(
+                    xs[B % NBUF], ys[B % NBUF]);
                 if (s + 1 < nsteps) {
                     gx.template store<B ^ 1>(xs[(B ^ 1) % NBUF]);
                     gy.template store<B ^ 1>(ys[(B ^ 1) % NBUF]);
@@ -1247,7 +1273,7 @@ gett_stream_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
             gy.load(Y + (nb.y + oy0), lim);
         }
         w.zero();
-        if (withK) w.template macro<GX::PITCH, GY::PITCH>(xs, ys);
+        if (withK) w.template macro<GX::PITCH, GY::PITCH, false, 0, false, GX::kSwz, GY::kSwz>(xs, ys);
         __syncthreads();
         if (more && withK) {
             gx.store(xs);
