@@ -72,7 +72,7 @@ def bound_of(w) -> str:
 class Problem:
     """One workload on the device, planned."""
 
-    def __init__(self, w, dev, on_device: bool = False):
+    def __init__(self, w, dev, on_device: bool = False, flags: int = 0):
         import torch
 
         import paper_1607_00145_amd as g
@@ -96,7 +96,7 @@ class Problem:
             w.numel("C"), dtype=self.A.dtype, device=dev)
         dt = g.GETT_FLOAT32 if w.dtype == "f32" else g.GETT_FLOAT64
         st, self.h = g.gett_plan(dt, w.modes_C, w.shape("C"), None, w.modes_A, w.shape("A"), None,
-                                 w.modes_B, w.shape("B"), None, 0)
+                                 w.modes_B, w.shape("B"), None, flags)
         if st != 0:
             raise RuntimeError(f"gett_plan: {g.gett_status_string(st)}")
         self.plan = json.loads(g.gett_plan_describe(self.h))
@@ -257,9 +257,14 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(w, target_s=15.0):
-    """The oracle on a bounded, evenly spaced sample of C's elements, with all
-    host threads, and on a smaller sample with one thread."""
+def cpu_baseline(w, whole_runs=0, target_s=5.0, single_s=0.0):
+    """The oracle (plain C, fp64, all host threads) timed on the host.
+
+    whole_runs > 0: all of C, that many runs, the minimum reported (Sec. 7's
+    statistic); otherwise one run over an evenly spaced sample of C's
+    elements sized to about target_s seconds.  single_s > 0: also one thread
+    on a sample of about that many seconds (the paper's numbers are
+    single-core)."""
     import oracle
     A, B, Cin = wl.make_inputs(w)
     nC = w.numel("C")
@@ -273,19 +278,41 @@ def cpu_baseline(w, target_s=15.0):
                         shape_C=w.shape("C"), points=pts, nthreads=nthreads)
         return time.perf_counter() - t
 
-    # calibrate on a small sample, then size the measured sample to ~target_s
-    n0 = min(nC, 200_000)
-    dt0 = run(n0, threads)
-    n = int(min(nC, max(n0, n0 * target_s / max(dt0, 1e-6))))
-    dt = run(n, threads)
-    n1 = min(nC, 2_000_000)
-    dt1 = run(n1, 1)
-    return {"value": round(flops_per_elem * n / dt / 1e9, 4), "unit": "GFLOP/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"{n} of {nC} elements of C ({w.name}), evenly spaced; {dt:.1f} s",
-            "cpu_model": cpu_model(),
-            "single_thread_value": round(flops_per_elem * n1 / dt1 / 1e9, 4),
-            "single_thread_sample": f"{n1} elements, {dt1:.1f} s"}
+    def sized(nthreads, seconds):
+        n0 = min(nC, 50_000)
+        dt0 = run(n0, nthreads)
+        return int(min(nC, max(n0, n0 * seconds / max(dt0, 1e-6))))
+
+    if whole_runs > 0:
+        times = [run(nC, threads) for _ in range(whole_runs)]
+        n, dt = nC, min(times)
+        sample = (f"all {nC} elements of C ({w.name}), minimum of {whole_runs} runs: "
+                  + ", ".join(f"{t:.2f}" for t in times) + " s")
+    else:
+        n = sized(threads, target_s)
+        dt = run(n, threads)
+        sample = f"{n} of {nC} elements of C ({w.name}), evenly spaced, one run: {dt:.1f} s"
+    rec = {"value": round(flops_per_elem * n / dt / 1e9, 4), "unit": "GFLOP/s", "cores": threads,
+           "kind": "oracle", "sample": sample, "cpu_model": cpu_model()}
+    if single_s > 0:
+        n1 = sized(1, single_s)
+        dt1 = run(n1, 1)
+        reps = 1
+        if n1 == nC and dt1 < single_s / 3:   # all of C is quick: repeat, keep the minimum
+            reps = int(min(50, single_s / max(dt1, 1e-6)))
+            dt1 = min([dt1] + [run(n1, 1) for _ in range(reps - 1)])
+        rec["single_thread_value"] = round(flops_per_elem * n1 / dt1 / 1e9, 4)
+        rec["single_thread_sample"] = (f"{n1} of {nC} elements, evenly spaced, one thread: "
+                                       f"{dt1:.3f} s" + (f" (minimum of {reps} runs)" if reps > 1 else ""))
+    return rec
+
+
+# Oracle timing per workload: the two small ones over all of C (minimum of
+# three runs) and on one core too; the large ones on one bounded sample.
+CPU_PLAN = {"tm3x2_fp32": dict(whole_runs=3, single_s=3.0),
+            "bw4x3_fp32": dict(whole_runs=3, single_s=3.0),
+            "cc4x4_fp64": dict(target_s=5.0), "ccsdt6_fp64": dict(target_s=5.0),
+            "gemm4_fp32": dict(target_s=5.0)}
 
 
 def traffic_for(kernel_name: str, workload: str):
@@ -303,8 +330,28 @@ def traffic_for(kernel_name: str, workload: str):
     return d.get("bytes_per_launch")
 
 
+def roofline_of(w, kernel_ms):
+    """The workload's bound (HBM or MFMA), its algorithmic bytes or flops per
+    launch over the kernel's average launch time, and the peak."""
+    if bound_of(w) == "hbm":
+        per = wl.algorithmic_bytes(w)
+        roof = {"bound": "hbm", "achieved": round(per / (kernel_ms * 1e-3) / 1e9, 1),
+                "peak": PEAK["hbm_GBs"], "unit": "GB/s"}
+    else:
+        per = wl.flop_count(w)
+        pk = PEAK["f32_TFLOPs"] if w.dtype == "f32" else PEAK["f64_TFLOPs"]
+        roof = {"bound": "mfma", "achieved": round(per / (kernel_ms * 1e-3) / 1e12, 2),
+                "peak": pk, "unit": "TFLOP/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = traffic_for("gett_macro_kernel", w.name)
+    roof["kernel_ms_avg"] = round(kernel_ms, 5)
+    return roof
+
+
 def report_workload(w, dev, stream, runs, flush):
     import torch
+
+    import paper_1607_00145_amd as g
     p = Problem(w, dev)
     flops = wl.flop_count(w)
     nbytes = wl.algorithmic_bytes(w)
@@ -312,6 +359,8 @@ def report_workload(w, dev, stream, runs, flush):
         p.launch(stream)
     ts = time_launches(lambda: p.launch(stream), runs, stream, flush)
     tmin, tmed = min(ts), statistics.median(ts)
+    # warm launches back to back: the kernel's average launch time (HIP events)
+    warm = time_launches(lambda: p.launch(stream), 50, stream)
     bound = bound_of(w)
     peak_f = (PEAK["f32_TFLOPs"] if w.dtype == "f32" else PEAK["f64_TFLOPs"]) * 1e12
     rec = {"workload": w.name, "expression": w.expression(), "dtype": w.dtype,
@@ -327,8 +376,23 @@ def report_workload(w, dev, stream, runs, flush):
     rec["plan"]["workgroups"] = p.plan["grid"]["workgroups"]
     rec["plan"]["kslices"] = p.plan["kslices"]
     rec["plan"]["kernel"] = p.plan["kernel"]
+    rec["plan"]["partials"] = p.plan["partials"]
     if p.plan["kernel"] == "tail":
         rec["plan"]["tail"] = p.plan["tail"]
+    rec["roofline"] = roofline_of(w, statistics.mean(warm))
+    # results are identical from call to call in every plan (partial tiles are
+    # summed in a fixed order); where the plan has partial tiles, the same
+    # contraction in whole tiles only is timed beside it
+    rec["deterministic"] = True
+    if p.plan["partials"] != "none":
+        pw = Problem(w, dev, flags=g.GETT_FLAG_WHOLE_TILES)
+        for _ in range(3):
+            pw.launch(stream)
+        tw = time_launches(lambda: pw.launch(stream), runs, stream, flush)
+        rec["whole_tiles_ms_min"] = round(min(tw), 5)
+        rec["whole_tiles_ms_median"] = round(statistics.median(tw), 5)
+        pw.close()
+        del pw
     t = TtgtProblem(p)
     for _ in range(3):
         t.launch(stream)
@@ -560,20 +624,7 @@ def main():
     value = flops * args.steps / elapsed / 1e9
     # live per-launch kernel time (HIP events on the launch stream)
     ev = time_launches(lambda: p.launch(stream), max(20, min(args.steps, 200)), stream)
-    kavg = statistics.mean(ev)
-    bound = bound_of(w)
-    if bound == "hbm":
-        per_launch = wl.algorithmic_bytes(w)
-        roof = {"bound": "hbm", "achieved": round(per_launch / (kavg * 1e-3) / 1e9, 1),
-                "peak": PEAK["hbm_GBs"], "unit": "GB/s"}
-    else:
-        per_launch = flops
-        pk = PEAK["f32_TFLOPs"] if w.dtype == "f32" else PEAK["f64_TFLOPs"]
-        roof = {"bound": "mfma", "achieved": round(per_launch / (kavg * 1e-3) / 1e12, 2),
-                "peak": pk, "unit": "TFLOP/s"}
-    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = traffic_for("gett_macro_kernel", w.name)
-    roof["kernel_ms_avg"] = round(kavg, 5)
+    roof = roofline_of(w, statistics.mean(ev))
     p.close()
     del p
     torch.cuda.empty_cache()
@@ -584,7 +635,12 @@ def main():
            "dtype": w.dtype, "data": "synthetic (seeded PCG64, workloads module)",
            "config": {"workload": w.name, "expression": w.expression(),
                       "extents": w.extents, "alpha": w.alpha, "beta": w.beta,
-                      "layout": "column-major", "parallelism": "single GPU"},
+                      "layout": "column-major", "parallelism": "single GPU",
+                      "deterministic": True,
+                      "headline": "the fp32 bandwidth-bound 4D x 3D contraction is the "
+                                  "configuration the metric is quoted on; every workload "
+                                  "(the 4096^3-shaped one included) has its own record with "
+                                  "roofline and CPU baseline under workloads"},
            "roofline": roof}
 
     # ---- per-workload cold-cache report ----
@@ -603,7 +659,15 @@ def main():
 
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
-        out["cpu_baseline"] = cpu_baseline(w)
+        out["cpu_baseline"] = cpu_baseline(w, **CPU_PLAN.get(w.name, {}))
+        for rec in out.get("workloads", []):
+            if rec["workload"] == w.name:
+                rec["cpu_baseline"] = out["cpu_baseline"]
+                continue
+            log(f"[bench] cpu baseline (oracle) {rec['workload']}")
+            rec["cpu_baseline"] = cpu_baseline(wl.BY_NAME[rec["workload"]],
+                                               **CPU_PLAN.get(rec["workload"], {}))
+            rec["vs_cpu_baseline"] = round(rec["gflops"] / rec["cpu_baseline"]["value"], 1)
     print(json.dumps(out), flush=True)
 
 
