@@ -37,7 +37,12 @@ extern "C" {
  * sums are formed in the same type (fp32 or fp64 matrix-core arithmetic). */
 typedef enum {
     GETT_FLOAT32 = 0,
-    GETT_FLOAT64 = 1
+    GETT_FLOAT64 = 1,
+    /* Not element types: these two give the enumeration the range of a
+     * 32-bit int, so any value a caller passes is a value of the type, and an
+     * unknown one is refused with GETT_ERROR_INVALID_VALUE. */
+    GETT_DTYPE_RANGE_MIN_ = -2147483647 - 1,
+    GETT_DTYPE_RANGE_MAX_ = 2147483647
 } gett_dtype_t;
 
 typedef enum {
@@ -59,7 +64,10 @@ typedef enum {
     /* a HIP runtime call (kernel launch) or a rocBLAS call failed */
     GETT_ERROR_HIP = 4,
     /* host memory allocation failed */
-    GETT_ERROR_ALLOC = 5
+    GETT_ERROR_ALLOC = 5,
+    /* not statuses: the range of a 32-bit int (see gett_dtype_t) */
+    GETT_STATUS_RANGE_MIN_ = -2147483647 - 1,
+    GETT_STATUS_RANGE_MAX_ = 2147483647
 } gett_status_t;
 
 /* Opaque, immutable plan (host memory only). */
@@ -376,7 +384,14 @@ const char *gett_log_describe(const gett_log_plan_t plan);
  * for one contraction and runs the one chosen.
  * ------------------------------------------------------------------------ */
 
-typedef enum { GETT_METHOD_GETT = 0, GETT_METHOD_TTGT = 1, GETT_METHOD_LOG = 2 } gett_method_t;
+typedef enum {
+    GETT_METHOD_GETT = 0,
+    GETT_METHOD_TTGT = 1,
+    GETT_METHOD_LOG = 2,
+    /* not methods: the range of a 32-bit int (see gett_dtype_t) */
+    GETT_METHOD_RANGE_MIN_ = -2147483647 - 1,
+    GETT_METHOD_RANGE_MAX_ = 2147483647
+} gett_method_t;
 
 typedef struct gett_select_plan_s *gett_select_plan_t;
 

@@ -21,6 +21,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "gett_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
+_LIB_ASAN = os.path.join(_HERE, "liboracle_asan.so")
 _lib = None
 
 ERRORS = {0: "ok", -1: "invalid value", -2: "parse error", -3: "invalid indices", -4: "point out of range"}
@@ -32,14 +33,24 @@ class OracleError(RuntimeError):
         self.code = code
 
 
-def build(force: bool = True) -> str:
-    """Compile gett_oracle.c into liboracle.so (gcc -O2 -fopenmp, no fast-math)."""
-    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-        tmp = _LIB + f".tmp{os.getpid()}"
-        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c99",
-                               "-Wall", "-o", tmp, _SRC, "-lm"])
-        os.replace(tmp, _LIB)
-    return _LIB
+def build(force: bool = True, sanitize: bool = False) -> str:
+    """Compile gett_oracle.c into liboracle.so (gcc -O2 -fopenmp, no fast-math),
+    or, sanitize, into liboracle_asan.so with AddressSanitizer and
+    UndefinedBehaviorSanitizer (clang, whose runtime the sanitized library
+    shares; tests/run_sanitized.sh)."""
+    out = _LIB_ASAN if sanitize else _LIB
+    if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(_SRC):
+        tmp = out + f".tmp{os.getpid()}"
+        if sanitize:
+            cmd = ["/opt/rocm/llvm/bin/clang", "-O1", "-g", "-fsanitize=address,undefined",
+                   "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer", "-fopenmp",
+                   "-fPIC", "-shared", "-std=c99", "-Wall", "-o", tmp, _SRC, "-lm"]
+        else:
+            cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c99", "-Wall", "-o", tmp,
+                   _SRC, "-lm"]
+        subprocess.check_call(cmd)
+        os.replace(tmp, out)
+    return out
 
 
 def _open(path: str):
@@ -67,8 +78,11 @@ def _open(path: str):
 def _load():
     global _lib
     if _lib is None:
-        build(force=False)
-        _lib = _open(_LIB)
+        # ORACLE_LIBRARY may name another build of gett_oracle.c (the sanitizer build)
+        path = os.environ.get("ORACLE_LIBRARY")
+        if not path:
+            path = build(force=False)
+        _lib = _open(path)
     return _lib
 
 

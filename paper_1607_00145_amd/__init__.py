@@ -18,7 +18,9 @@ import re
 from typing import Optional, Sequence
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "lib", "libgett.so")
+# GETT_LIBRARY may name another build of the same sources (the sanitizer
+# build, lib/libgett_asan.so); there is no fallback when it is missing.
+LIB_PATH = os.environ.get("GETT_LIBRARY") or os.path.join(_HERE, "lib", "libgett.so")
 
 GETT_FLOAT32 = 0
 GETT_FLOAT64 = 1

@@ -1,9 +1,13 @@
 """Build the gfx950 shared library libgett.so from csrc/ (hipcc, in-tree).
 
-    python -m paper_1607_00145_amd.build [-j N]
+    python -m paper_1607_00145_amd.build [-j N] [--incremental] [--sanitize]
 
 Objects go to _build/ at the repository root; the library to
-paper_1607_00145_amd/lib/libgett.so.
+paper_1607_00145_amd/lib/libgett.so.  --sanitize builds
+paper_1607_00145_amd/lib/libgett_asan.so instead (objects in _build/asan/):
+the host code (planner, C interface, launchers) instrumented with
+AddressSanitizer and UndefinedBehaviorSanitizer, the device code as usual; a
+process loads it with the sanitizer runtime preloaded (tests/run_sanitized.sh).
 """
 from __future__ import annotations
 
@@ -20,6 +24,12 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIBDIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIBDIR, "libgett.so")
+LIB_ASAN = os.path.join(LIBDIR, "libgett_asan.so")
+# host-only sanitizer flags (each -fsanitize= right after -Xarch_host: the
+# device code is not instrumented)
+SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host",
+            "-fno-omit-frame-pointer", "-g"]
 ARCH = "gfx950"
 ROCM_LIB = "/opt/rocm/lib"
 
@@ -68,13 +78,14 @@ def newest_input() -> float:
     return max(os.path.getmtime(f) for f in files)
 
 
-def compile_one(job, incremental: bool = False) -> str:
+def compile_one(job, incremental: bool = False, sanitize: bool = False) -> str:
     src, tile = job
-    os.makedirs(BUILD, exist_ok=True)
-    obj = os.path.join(BUILD, src + ("" if tile is None else f".t{tile}") + ".o")
+    bdir = os.path.join(BUILD, "asan") if sanitize else BUILD
+    os.makedirs(bdir, exist_ok=True)
+    obj = os.path.join(bdir, src + ("" if tile is None else f".t{tile}") + ".o")
     if incremental and os.path.exists(obj) and os.path.getmtime(obj) >= newest_input():
         return obj
-    cmd = [hipcc()] + COMMON
+    cmd = [hipcc()] + COMMON + (SANITIZE if sanitize else [])
     if src.endswith(".hip"):
         cmd += DEVICE + ["-x", "hip"]
     if tile is not None:
@@ -91,24 +102,28 @@ def compile_one(job, incremental: bool = False) -> str:
     return obj
 
 
-def build(jobs: int = 0, incremental: bool = False) -> str:
+def build(jobs: int = 0, incremental: bool = False, sanitize: bool = False) -> str:
     """Compile every source (or, incremental, only those whose object is older
-    than the newest source or header) and link libgett.so."""
+    than the newest source or header) and link libgett.so (libgett_asan.so
+    with the host sanitizers)."""
     work = [j for src in sources() for j in jobs_of(src)]
     # the largest units first, so they do not end up last on one worker
     work.sort(key=lambda j: (j[0] not in PER_TILE, j[1] is None))
     jobs = jobs or min(len(work), os.cpu_count() or 4)
     with cf.ThreadPoolExecutor(jobs) as ex:
-        objs = list(ex.map(lambda j: compile_one(j, incremental), work))
+        objs = list(ex.map(lambda j: compile_one(j, incremental, sanitize), work))
     os.makedirs(LIBDIR, exist_ok=True)
-    tmp = LIB + f".tmp{os.getpid()}"
+    out = LIB_ASAN if sanitize else LIB
+    tmp = out + f".tmp{os.getpid()}"
     cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + objs + \
         ["-L" + ROCM_LIB, "-lrocblas", "-Wl,-rpath," + ROCM_LIB]
+    if sanitize:
+        cmd += ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":
@@ -116,5 +131,7 @@ if __name__ == "__main__":
     ap.add_argument("-j", type=int, default=0)
     ap.add_argument("--incremental", action="store_true",
                     help="recompile only objects older than the newest source or header")
+    ap.add_argument("--sanitize", action="store_true",
+                    help="host AddressSanitizer + UndefinedBehaviorSanitizer build (libgett_asan.so)")
     a = ap.parse_args()
-    print(build(a.j, a.incremental))
+    print(build(a.j, a.incremental, a.sanitize))

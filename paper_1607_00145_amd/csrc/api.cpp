@@ -251,6 +251,7 @@ const char *gett_status_string(gett_status_t s)
     case GETT_ERROR_NOT_SUPPORTED: return "not supported";
     case GETT_ERROR_HIP: return "HIP runtime error";
     case GETT_ERROR_ALLOC: return "allocation failed";
+    default: break;
     }
     return "unknown status";
 }

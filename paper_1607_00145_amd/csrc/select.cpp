@@ -71,6 +71,7 @@ gett_status_t launch(const gett_select_plan_s &p, gett_method_t m, double alpha,
     case GETT_METHOD_TTGT:
         return gett_ttgt_contract(p.ttgt, alpha, A, B, beta, C, ws, wsBytes, stream);
     case GETT_METHOD_LOG: return gett_log_contract(p.log, alpha, A, B, beta, C, stream);
+    default: break;
     }
     return GETT_ERROR_INVALID_VALUE;
 }

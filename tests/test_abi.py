@@ -216,6 +216,22 @@ def test_contract_host_side_errors():
     assert g.gett_status_string(4) == "HIP runtime error"
 
 
+@pytest.mark.parametrize("value", [2, 7, -1, -(1 << 31), (1 << 31) - 1])
+def test_any_int_of_the_enumerations_is_refused_not_undefined(value):
+    """The enumerations take the range of a 32-bit int (two range
+    enumerators), so an unknown value from a C caller is a value of the type
+    and refused; the sanitizer build checks that no load of one is undefined."""
+    st, h = g.gett_plan(value, "m,n", [2, 2], None, "m,k", [2, 2], None, "k,n", [2, 2], None)
+    assert st == g.GETT_ERROR_INVALID_VALUE and h is None
+    E = g.GETT_ERROR_INVALID_VALUE
+    assert g.gett_transpose(value, [2, 3], None, [3, 1], 1.0, 0x1000, 0.0, 0x2000) == E
+
+
+@pytest.mark.parametrize("value", [6, 99, -1, -(1 << 31), (1 << 31) - 1])
+def test_unknown_status_has_text(value):
+    assert g.gett_status_string(value) == "unknown status"
+
+
 def test_contract_empty_c_is_a_no_op():
     st, h = plan("m,n", "m,k", "k,n", {"m": 0, "n": 8, "k": 8})
     assert st == 0

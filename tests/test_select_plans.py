@@ -51,7 +51,8 @@ def test_candidates_follow_the_planners(case):
             if ok:
                 assert g.gett_select_method(s) == (0, m)
         assert json.loads(g.gett_select_describe(s))["method"] == "gett"
-        assert g.gett_select_force(s, 7) == g.GETT_ERROR_INVALID_VALUE
+        for bad in (3, 7, -1, -(1 << 31), (1 << 31) - 1):
+            assert g.gett_select_force(s, bad) == g.GETT_ERROR_INVALID_VALUE
     finally:
         g.gett_select_destroy(s)
 
