@@ -158,11 +158,13 @@ gett_status_t gett_plan(gett_plan_t *plan, gett_dtype_t dtype,
  * this keeps the result independent of timing).  The library owns that
  * memory: one set of buffers per device and stream, allocated (hipMalloc)
  * by the first call that needs it or more of it, kept until the process
- * ends.  Such a call synchronises `stream` and must not be inside a HIP graph
- * capture -- capture a plan's calls after an eager call on the same stream.
- * Calls on one stream share its buffers (they run in order); calls on
- * different streams use different ones.  Errors: GETT_ERROR_HIP also when
- * that allocation fails.
+ * ends.  Such a call synchronises `stream` (when buffers grow), and inside a
+ * HIP graph capture it is refused: capture a plan's calls after an eager
+ * call on the same stream, or use gett_contract_noalloc.  Calls on one stream
+ * share its buffers (they run in order); calls on different streams use
+ * different ones.  Errors: GETT_ERROR_HIP also when that allocation fails;
+ * GETT_ERROR_NOT_SUPPORTED, with nothing enqueued, when it would have to
+ * happen while `stream` is capturing a graph.
  */
 gett_status_t gett_contract(const gett_plan_t plan, double alpha, const void *A, const void *B,
                             double beta, void *C, void *stream);

@@ -195,7 +195,7 @@ struct BoxWalker {
 // analyser guarantees es * VW divides ROWS (KT) and that v's extent and, in
 // the K box, its block length are multiples of VW, so a vector is valid or
 // outside the tensor as a whole.
-template <typename T, int ROWS, int KT, int MODE, int NTH, int STAGES = 1>
+template <typename T, int ROWS, int KT, int MODE, int NTH, int STAGES = 1, bool SWZ = false>
 struct Gather {
     static constexpr int VW = Traits<T>::VW;
     static constexpr int PITCH = ROWS + VW;   // LDS row pitch (elements) of the [k][row] layout
@@ -215,8 +215,12 @@ struct Gather {
     // of different groups of four shift by whole vectors, a vector's VW
     // elements share the shift (VW divides 4), and a VW-row piece stays
     // contiguous for the MFMA reads, which apply the same bijection (for the
-    // rows of one MFMA step the shift is a constant).
-    static constexpr bool kSwz = MODE == kGatherKVec && ROWS % (8 * VW) == 0;
+    // rows of one MFMA step the shift is a constant).  SWZ: the kernel asks
+    // for it only when the other operand is gathered in vectors too; beside
+    // an element-wise or strided gather, whose addressing already fills the
+    // register budget, the swizzled reads made the compiler spill (64 x 256
+    // fp32 tile: 0 -> 176 bytes per lane, twice the time).
+    static constexpr bool kSwz = SWZ && MODE == kGatherKVec && ROWS % (8 * VW) == 0;
     static __device__ __forceinline__ int swz(int r, int k)
     {
         return kSwz ? r ^ (VW * ((k >> 2) & 7)) : r;
@@ -599,14 +603,26 @@ struct WaveTile {
               bool SY = false>
     __device__ __forceinline__ void macro(const T *xs, const T *ys)
     {
-        const int xr = wm * WTM + RX * l16, yr = wn * WTN + RY * l16;
+        // Fragment gi of this lane starts at row w + RX * l16 + 16 RX gi of the
+        // panel (w: the wave's first row, a multiple of 16 RX).  With the
+        // swizzle a step's rows are XORed with c = VW * (ks mod 8).  When c is
+        // below the block stride 16 RX (a power of two), the XOR touches only
+        // the bits of RX * l16 and leaves w + 16 RX gi alone, so one XOR per
+        // step serves every block and the block offset stays an immediate;
+        // otherwise (tiles with RX = 1) the whole row is XORed.
+        const int xw = wm * WTM, yw = wn * WTN, xl = RX * l16, yl = RY * l16;
+        const T *xt = xs + xw + xl, *yt = ys + yw + yl;
         auto xat = [&](int ks, int k, int gi) {
-            const int r = xr + gi * 16 * RX;
-            return xs + k * PX + (SX ? r ^ (VW * (ks & 7)) : r);
+            if constexpr (!SX) return xt + k * PX + gi * 16 * RX;
+            else if constexpr (8 * VW <= 16 * RX)
+                return xs + xw + k * PX + gi * 16 * RX + (xl ^ (VW * (ks & 7)));
+            else return xs + k * PX + ((xw + xl + gi * 16 * RX) ^ (VW * (ks & 7)));
         };
         auto yat = [&](int ks, int k, int gj) {
-            const int r = yr + gj * 16 * RY;
-            return ys + k * PY + (SY ? r ^ (VW * (ks & 7)) : r);
+            if constexpr (!SY) return yt + k * PY + gj * 16 * RY;
+            else if constexpr (8 * VW <= 16 * RY)
+                return ys + yw + k * PY + gj * 16 * RY + (yl ^ (VW * (ks & 7)));
+            else return ys + k * PY + ((yw + yl + gj * 16 * RY) ^ (VW * (ks & 7)));
         };
         if constexpr (PIPE) {
             typename XV::type av[2][RB / RX];
@@ -951,8 +967,9 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
     static_assert(!(TAIL && SLICED), "one variant at a time");
     constexpr bool kPartials = TAIL || SLICED;
     constexpr int NTH = WM * WN * 64;
-    typedef Gather<T, MT, KT, XMODE, NTH, PF> GX;
-    typedef Gather<T, NT, KT, YMODE, NTH, PF> GY;
+    // the k-vector swizzle only beside a vector gather of the other operand
+    typedef Gather<T, MT, KT, XMODE, NTH, PF, YMODE == kGatherRowVec || YMODE == kGatherKVec> GX;
+    typedef Gather<T, NT, KT, YMODE, NTH, PF, XMODE == kGatherRowVec || XMODE == kGatherKVec> GY;
     typedef WaveTile<T, MT, NT, KT, WM, WN, RX, RY> WT;
 
     // the packed panels; after the K loop the same memory stages C for
@@ -1214,8 +1231,8 @@ gett_stream_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
                    T *__restrict__ C, const T alpha, const T beta)
 {
     constexpr int NTH = WM * WN * 64;
-    typedef Gather<T, MT, KT, XMODE, NTH> GX;
-    typedef Gather<T, NT, KT, YMODE, NTH> GY;
+    typedef Gather<T, MT, KT, XMODE, NTH, 1, YMODE == kGatherRowVec || YMODE == kGatherKVec> GX;
+    typedef Gather<T, NT, KT, YMODE, NTH, 1, XMODE == kGatherRowVec || XMODE == kGatherKVec> GY;
     typedef WaveTile<T, MT, NT, KT, WM, WN, RX, RY> WT;
 
     __shared__ __attribute__((aligned(16))) T xs[KT * GX::PITCH];

@@ -7,9 +7,10 @@
 // partial-tile slots, which need no initial value.  Launches on one stream
 // run in order, so they can share the pair; launches on different streams get
 // different pairs.  A buffer grows when a plan needs more: the stream is
-// synchronised first (queued work may still use the old one), so growth must
-// not happen inside a graph capture -- an eager call of the plan on that
-// stream beforehand allocates what the captured calls use.
+// synchronised first (queued work may still use the old one).  Growth is
+// refused (GETT_ERROR_NOT_SUPPORTED, nothing enqueued) while the stream is
+// capturing a graph -- an eager call of the plan on that stream beforehand
+// allocates what the captured calls use.
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
@@ -45,6 +46,11 @@ gett_status_t stream_workspace(hipStream_t stream, uint64_t counters, uint64_t t
     Buffers &b = g_buffers[{dev, stream}];
     const uint64_t cBytes = counters * sizeof(int);
     const bool growC = cBytes > b.counterBytes, growT = tileBytes > b.tileBytes;
+    if (growC || growT) {
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(stream, &cap) != hipSuccess) return GETT_ERROR_HIP;
+        if (cap != hipStreamCaptureStatusNone) return GETT_ERROR_NOT_SUPPORTED;
+    }
     if ((growC && b.counters) || (growT && b.tiles)) {
         // queued launches on this stream may still use the old buffers
         if (hipStreamSynchronize(stream) != hipSuccess) return GETT_ERROR_HIP;

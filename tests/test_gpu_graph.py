@@ -88,3 +88,43 @@ def test_graph_replay_matches_eager(gpu, monkeypatch, name, alpha, beta, dtype):
             del junk
     finally:
         g.gett_destroy(h)
+
+
+def test_first_call_under_capture_is_refused(gpu, monkeypatch):
+    """A plan with partial tiles whose stream has no workspace yet: called
+    during a capture it is refused (GETT_ERROR_NOT_SUPPORTED) with nothing
+    enqueued -- the workspace would have to be allocated inside the capture.
+    The capture itself stays valid, and the same call made eagerly afterwards
+    allocates the workspace and computes C."""
+    import torch
+    monkeypatch.setenv("GETT_FORCE_KSLICES", "8")
+    modes, ext, _ = CASES["kslices_forced"]
+    shp = lambda m: [ext[x] for x in m.split(",")]
+    st, h = g.gett_plan(g.GETT_FLOAT64, modes[0], shp(modes[0]), None, modes[1], shp(modes[1]),
+                        None, modes[2], shp(modes[2]), None, 0)
+    assert st == 0
+    try:
+        assert json.loads(g.gett_plan_describe(h))["partials"] == "workspace"
+        n = lambda m: int(np.prod(shp(m)))
+        A = torch.ones(n(modes[1]), dtype=torch.float64, device=gpu)
+        B = torch.ones(n(modes[2]), dtype=torch.float64, device=gpu)
+        C = torch.full((n(modes[0]),), 7.0, dtype=torch.float64, device=gpu)
+        side = torch.cuda.Stream()                      # a stream never used by the library
+        side.wait_stream(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(graph, stream=side):
+                C.mul_(1.0)                             # keep the graph non-empty
+                st = g.gett_contract(h, 1.0, A.data_ptr(), B.data_ptr(), 0.0, C.data_ptr(),
+                                     side.cuda_stream)
+        assert st == g.GETT_ERROR_NOT_SUPPORTED
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.all(C == 7.0)                      # the contraction was not captured
+        assert g.gett_contract(h, 1.0, A.data_ptr(), B.data_ptr(), 0.0, C.data_ptr(),
+                               side.cuda_stream) == 0
+        torch.cuda.synchronize()
+        assert torch.all(C == float(ext["k"]))          # sum over k of 1 * 1
+    finally:
+        g.gett_destroy(h)
