@@ -231,9 +231,12 @@ const char *gett_status_string(gett_status_t status);
  * gett_plan_describe -- the plan's decisions as a JSON object (static storage
  * owned by the plan, valid until gett_destroy): index sets, merged
  * super-indices, operand exchange, loop order, stride-one choices, gather
- * modes, tile sizes, kernel kind ("macro", "stream" or "tail"), K slices,
- * the stream-K tail's whole tiles, workgroups and boxes per workgroup, grid,
- * the ranked candidates and the flop / byte counts of Eq. 12-14.
+ * modes, the tile (sizes, wavefront grid, fragment reads, wavefronts per SIMD
+ * its registers allow, prefetch depth, LDS buffers, one-box and C-order
+ * variants), kernel kind ("macro", "stream" or "tail"), K slices, the
+ * stream-K tail's whole tiles, workgroups and boxes per workgroup, the
+ * partial-tile workspace, grid, the ranked candidates and the flop / byte
+ * counts of Eq. 12-14.
  * Returns "" for NULL.
  */
 const char *gett_plan_describe(const gett_plan_t plan);

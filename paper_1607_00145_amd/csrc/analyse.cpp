@@ -1111,7 +1111,10 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     o << ",\"size_x\":" << sizeX << ",\"size_y\":" << sizeY << ",\"size_k\":" << an.sizeK;
     o << ",\"tile\":{\"id\":" << tile << ",\"mt\":" << ts.mt << ",\"nt\":" << ts.nt << ",\"kt\":" << ts.kt
       << ",\"waves\":[" << ts.wm << "," << ts.wn << "],\"reads\":[" << ts.rx << "," << ts.ry
-      << "],\"chosen_by\":\"" << how << "\",\"model_us\":" << pick.cost * 1e6 << "}";
+      << "],\"waves_per_simd\":" << ts.wpe << ",\"prefetch\":" << ts.pf
+      << ",\"lds_buffers\":" << ts.nbuf << ",\"one_box\":" << (ts.onebox ? "true" : "false")
+      << ",\"c_order_epilogue\":" << (ts.corder ? "true" : "false")
+      << ",\"chosen_by\":\"" << how << "\",\"model_us\":" << pick.cost * 1e6 << "}";
     o << ",\"candidates\":[";
     for (size_t i = 0; i < ranked.size(); ++i) {
         o << (i ? "," : "") << "{\"tile\":" << ranked[i].tile << ",\"kind\":\""
