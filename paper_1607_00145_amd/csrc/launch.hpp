@@ -3,6 +3,8 @@
 #pragma once
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+
 #include "kernel.hpp"
 #include "plan.hpp"
 #include "tiles.hpp"
@@ -20,16 +22,25 @@ template <> struct TileTable<double> {
 };
 
 // Workgroups of a persistent kernel: as many as fit on the device at once,
-// and no more than there are tiles.
+// and no more than there are tiles.  The count per device is looked up once
+// per kernel (the first launch on each device, up to 64 devices).
 template <typename K>
 unsigned persistent_grid(K kernel, int threads, unsigned tiles)
 {
-    int dev = 0, cus = 0, per = 0;
+    static std::atomic<int> cached[64];   // CUs x workgroups per CU, 0: not yet known
+    int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, 0) != hipSuccess) return 0;
-    const unsigned n = (unsigned)(cus * (per > 0 ? per : 1));
-    return n < tiles ? n : tiles;
+    int n = dev >= 0 && dev < 64 ? cached[dev].load(std::memory_order_relaxed) : 0;
+    if (n <= 0) {
+        int cus = 0, per = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, 0) != hipSuccess)
+            return 0;
+        n = cus * (per > 0 ? per : 1);
+        if (dev >= 0 && dev < 64) cached[dev].store(n, std::memory_order_relaxed);
+    }
+    return (unsigned)n < tiles ? (unsigned)n : tiles;
 }
 
 template <typename T, int TI, int XM, int YM, int KIND>
