@@ -124,6 +124,22 @@ typedef struct gett_plan_s *gett_plan_t;
  * super-index (Sec. 6, footnote 18).  An empty I_m, I_n or I_k acts as one
  * index of extent 1.  A zero extent gives an empty sum (C <- beta * C) or an
  * empty C.  No HIP call is made; the plan holds no device memory.
+ *
+ * Tuning and test hooks.  gett_plan also reads these environment variables,
+ * meant for experiments and tests (unset in normal use); the values in force
+ * are part of the plan (a choice gett_plan_tune remembers is only reused
+ * under the same values) and gett_plan_describe lists them ("hooks"):
+ *   GETT_FORCE_TILE      tile index to use (gett_plan_describe "tile.id")
+ *   GETT_FORCE_KIND      1 streaming kernel, 3 stream-K tail (on a tile that
+ *                        carries it)
+ *   GETT_FORCE_KSLICES   number of K slices
+ *   GETT_TAIL_WGS        workgroups of the stream-K tail
+ *   GETT_SPLIT_F         block size of a split index (Sec. 3.2.1)
+ *   GETT_C_ORDER=0       no C-order epilogue
+ *   GETT_LANE_PERM=0     no lane order for element-wise gathers
+ *   GETT_XCD_REMAP=0|1   tile walk in hardware order / grouped per XCD
+ * A forced choice the plan cannot honour (a tile index out of range, a kind
+ * the tile does not carry) is ignored.
  */
 gett_status_t gett_plan(gett_plan_t *plan, gett_dtype_t dtype,
                         const char *modes_C, const int64_t *extent_C, const int64_t *stride_C,
@@ -142,7 +158,10 @@ gett_status_t gett_plan(gett_plan_t *plan, gett_dtype_t dtype,
  *   beta     scale of the old C.  beta == 0: C is not read, so NaN or Inf in
  *            C does not propagate (BLAS convention).
  *   C        device pointer to element [0,...,0] of C; must not overlap A
- *            or B.
+ *            or B.  Any memory the device can read and write: C is read and
+ *            written with plain loads and stores only (no atomic operation
+ *            touches caller memory), so fine-grained or host-coherent
+ *            allocations and pinned host memory work too (slower).
  *   stream   a hipStream_t (NULL: the default stream).
  *
  * The call only enqueues work on `stream` and returns; the kernel arguments

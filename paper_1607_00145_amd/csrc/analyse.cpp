@@ -26,6 +26,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cctype>
 #include <new>
 #include <sstream>
 
@@ -205,6 +206,11 @@ Hooks read_hooks()
         *v.slot = getenv(v.name);
         if (*v.slot) h.text += std::string(v.name) + "=" + *v.slot + ";";
     }
+    // the text goes into gett_plan_describe's JSON: keep it to plain characters
+    for (char &c : h.text)
+        if (!(isalnum((unsigned char)c) || c == '_' || c == '=' || c == ';' || c == '-' ||
+              c == '.'))
+            c = '?';
     return h;
 }
 
@@ -1115,6 +1121,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
       << ",\"lds_buffers\":" << ts.nbuf << ",\"one_box\":" << (ts.onebox ? "true" : "false")
       << ",\"c_order_epilogue\":" << (ts.corder ? "true" : "false")
       << ",\"chosen_by\":\"" << how << "\",\"model_us\":" << pick.cost * 1e6 << "}";
+    o << ",\"hooks\":\"" << hk.text << "\"";
     o << ",\"candidates\":[";
     for (size_t i = 0; i < ranked.size(); ++i) {
         o << (i ? "," : "") << "{\"tile\":" << ranked[i].tile << ",\"kind\":\""

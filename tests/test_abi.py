@@ -560,3 +560,20 @@ def test_rank16_plans_keep_every_index(variant, dtype):
     assert (len(d["I_m"]), len(d["I_n"]), len(d["I_k"])) == sizes
     assert d["merges"] == []
     assert max(len(d["x_order"]), len(d["y_order"])) == max(sizes[0], sizes[1])
+
+
+def test_hooks_are_part_of_the_plan(monkeypatch):
+    """The tuning hooks in force are listed by the description (sanitised for
+    JSON) and change nothing when unset."""
+    monkeypatch.delenv("GETT_FORCE_TILE", raising=False)
+    st, h = plan("m,n", "m,k", "k,n", {"m": 64, "n": 64, "k": 64})
+    d0 = json.loads(g.gett_plan_describe(h))
+    g.gett_destroy(h)
+    assert d0["hooks"] == ""
+    monkeypatch.setenv("GETT_FORCE_TILE", "3")
+    monkeypatch.setenv("GETT_SPLIT_F", 'x"y')
+    st, h = plan("m,n", "m,k", "k,n", {"m": 64, "n": 64, "k": 64})
+    d1 = json.loads(g.gett_plan_describe(h))
+    g.gett_destroy(h)
+    assert "GETT_FORCE_TILE=3;" in d1["hooks"] and "GETT_SPLIT_F=x?y;" in d1["hooks"]
+    assert d1["tile"]["id"] == 3 and d1["tile"]["chosen_by"] == "forced"
