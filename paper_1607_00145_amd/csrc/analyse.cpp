@@ -735,8 +735,21 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
             if (best.tile >= 0) ranked.push_back(best);
         }
     }
-    std::stable_sort(ranked.begin(), ranked.end(),
-                     [](const Candidate &a, const Candidate &b) { return a.cost < b.cost; });
+    // Ties (the same estimate to 0.01 us: mirror-image tiles on a square
+    // problem) between tiles of at least 64 x 64 go to the one wider along y,
+    // whose C runs are longer (measured on MI355X: fp64 64 x 128 x 24 against
+    // 128 x 64 x 24 on the 4D x 4D contractions of Appendix A, 1-4% faster);
+    // small tiles keep the table's order (fp32 64 x 32 was 3-5% faster than
+    // 32 x 64 on the latency-bound points of Fig. 11).
+    auto wideY = [&](const Candidate &c) {
+        const TileShape &t = tile_shape(dtype, c.tile);
+        return t.mt >= 64 && t.nt >= 64 ? t.nt : 0;
+    };
+    std::stable_sort(ranked.begin(), ranked.end(), [&](const Candidate &a, const Candidate &b) {
+        const long long ka = llround(a.cost * 1e8), kb = llround(b.cost * 1e8);
+        if (ka != kb) return ka < kb;
+        return wideY(a) > wideY(b);
+    });
     Candidate pick = ranked[0];
     const char *how = "model";
     auto find = [&](int t, int k) -> const Candidate * {
