@@ -16,7 +16,9 @@ stdout.  The line also carries:
   cpu_baseline  the oracle (plain C, fp64, all host threads) on a bounded
                 sample of the same workload;
   workloads     every workload with cold-cache kernel times (minimum and
-                median over runs, each after a 1 GiB cache flush), GFLOP/s,
+                median over runs, each after reading a 1 GiB buffer, which
+                evicts the workload's data from the caches and leaves no
+                dirty lines behind), GFLOP/s,
                 GB/s, fraction of its bound, the same contraction by TTGT
                 (Sec. 4) and by LoG (Sec. 5), and an equal-size GEMM (torch -> hipBLASLt/rocBLAS)
                 timed the same way (Sec. 7: the GEMM of sizes
@@ -228,6 +230,18 @@ def time_log(p: Problem, stream, runs, flush):
     calls = lp.plan["gemm_calls"]
     lp.close()
     return t, calls
+
+
+def cache_flush(dev):
+    """Evict the caches between cold runs by reading a 1 GiB buffer (summed
+    into a preallocated scalar).  Reading rather than writing leaves no dirty
+    lines whose write-back the next kernel would pay for: a write flush adds
+    7-11% to the write-only 6D workload's median and 4% to the headline's,
+    nothing to compute-bound ones."""
+    import torch
+    buf = torch.zeros(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
+    sink = torch.empty((), dtype=torch.float32, device=dev)
+    return lambda: torch.sum(buf, 0, out=sink)
 
 
 def time_launches(fn, n, stream, flush=None):
@@ -602,8 +616,7 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": n * 4, "launches": 5}), flush=True)
         return
     if args.sweep:
-        flush_buf = torch.empty(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
-        sweep_run(args.sweep, dev, stream, args.report_runs, lambda: flush_buf.zero_(),
+        sweep_run(args.sweep, dev, stream, args.report_runs, cache_flush(dev),
                   args.max_candidates)
         return
     w = wl.BY_NAME[args.workload]
@@ -645,8 +658,7 @@ def main():
 
     # ---- per-workload cold-cache report ----
     if not args.no_report:
-        flush_buf = torch.empty(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
-        flush = lambda: flush_buf.zero_()
+        flush = cache_flush(dev)
         reps = []
         for ww in wl.WORKLOADS:
             log(f"[bench] report {ww.name}")
@@ -654,7 +666,7 @@ def main():
         out["workloads"] = reps
         log("[bench] report transpose")
         out["transpose"] = report_transpose(dev, stream, args.report_runs, flush)
-        del flush_buf
+        del flush
         torch.cuda.empty_cache()
 
     if not args.no_cpu_baseline:
