@@ -216,7 +216,7 @@ Hooks read_hooks()
 
 const char *kind_name(int k)
 {
-    return k == 1 ? "stream" : k == 2 ? "kslices" : k == 3 ? "tail" : "macro";
+    return k == 1 ? "stream" : k == 2 ? "kslices" : k == 3 ? "tail" : k == 4 ? "direct" : "macro";
 }
 
 // Workgroups of a tile resident on one CU at once: the wavefronts per SIMD its
@@ -644,6 +644,24 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
             cd.cost = bound(std::max(tMfma, tMem), tChain) * single;
             ranked.push_back(cd);
         }
+        // Direct-load kernel (tiles that carry it): both operands gathered in
+        // vectors, every tile row inside the tensors, every K box whole.  It
+        // sustains deff of the MFMA peak where the macro-kernel sustains eff;
+        // its memory stream is priced as the macro-kernel's.
+        if (c.deff > 0.0f && !slowGather && !(flags & GETT_FLAG_SCALAR) && !kSplitAhead &&
+            sizeX % c.mt == 0 && sizeY % c.nt == 0 && b.nsteps >= 1 && b.kbox == c.kt &&
+            Ik[b.kj].extent % b.tj == 0) {
+            const double tMem = (bytesC + bytesX + bytesY +
+                                 0.05 * (bytesX * (ty - 1) + bytesY * (tx - 1))) /
+                                (8.0e12 * c.bw * cuShare);
+            Candidate cd;
+            cd.tile = t;
+            cd.kind = 4;
+            cd.tMfma = tMfma * c.eff / c.deff;
+            cd.tMem = tMem;
+            cd.cost = bound(std::max(cd.tMfma, tMem), tChain);
+            ranked.push_back(cd);
+        }
         // K slices: when a contracted set of many boxes meets too few tiles to
         // give every SIMD two wavefronts, P workgroups share each tile's
         // boxes.  Their partial tiles go to the workspace and the last of a
@@ -791,7 +809,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         }
     }
     const int tile = pick.tile;
-    const int kind = pick.kind;
+    int kind = pick.kind;
     const int kslices = kind == 2 ? pick.slices : 1;
     const double bestMfma = pick.tMfma, bestMem = pick.tMem;
     const TileShape &ts = tile_shape(dtype, tile);
@@ -933,6 +951,12 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         else if (row_vec_ok(Iy, sY)) ymode = kGatherRowVec;
         else if (k_vec_ok(Iy, sY)) ymode = kGatherKVec;
     }
+    // The direct-load kernel takes vector gathers, whole tiles and whole K
+    // boxes; a plan that ends up otherwise runs its tile's macro-kernel.
+    if (kind == 4 && !(xmode <= kGatherKVec && ymode <= kGatherKVec && sizeX % ts.mt == 0 &&
+                       sizeY % ts.nt == 0 && nsteps >= 1 && kbox == ts.kt &&
+                       Ik[kj].extent % tj == 0))
+        kind = 0;
     bool cvec = !(flags & GETT_FLAG_SCALAR) && Iy[0].strC == 1 && Iy[0].extent % VW == 0;
     for (auto &x : Ix) if (x.strC % VW) cvec = false;
     for (size_t i = 1; i < Iy.size(); ++i) if (Iy[i].strC % VW) cvec = false;
@@ -1145,7 +1169,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     }
     o << "]";
     o << ",\"streaming\":" << (streaming ? "true" : "false");
-    o << ",\"kernel\":\"" << (kind == 1 ? "stream" : kind == 3 ? "tail" : "macro")
+    o << ",\"kernel\":\"" << (kind == 1 ? "stream" : kind == 3 ? "tail" : kind == 4 ? "direct" : "macro")
       << "\",\"kslices\":" << kslices;
     o << ",\"tail\":{\"full_tiles\":" << d.tailFull << ",\"workgroups\":" << d.tailWgs
       << ",\"boxes\":" << d.tailLen << "}";

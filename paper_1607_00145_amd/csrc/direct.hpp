@@ -1,0 +1,314 @@
+// direct.hpp -- the direct-load variant of the macro-kernel (device code).
+//
+// When both operands are gathered in 16-byte vectors (row or k vectors) and
+// every tile row and every K box lies inside the tensors, packing (Eq. 9-10)
+// needs no registers: the load unit copies each 16-byte piece from device
+// memory straight into LDS (global_load_lds_dwordx4: lane i of one
+// instruction fills bytes [16 i, 16 i + 16) after a wave-uniform LDS base).
+// The LDS layout of an operand tile is then fixed by which piece each lane
+// loads:
+//   row-vector operand: [k][row], as the macro-kernel packs it (no padding);
+//   k-vector operand:   [row][k], the pieces of row r XOR-permuted by
+//                       (r / 4) mod (pieces per row), so that the lanes of an
+//                       MFMA read, which take rows 4 apart at one k piece,
+//                       fall on different banks.
+// A k-vector piece holds VW consecutive contracted positions, and one LDS
+// read hands them to VW consecutive MFMA steps: the position lane group g
+// supplies in step s is
+//   kp(s, g) = 4 VW floor(s / VW) + VW g + (s mod VW)
+// on both operands (a bijection of the box's KT positions onto the (s, g)
+// pairs, so each product still pairs matching indices and the sum is the
+// same up to rounding order).
+//
+// Pipeline, two LDS buffers, box s in buffer s mod 2:
+//   MFMAs of box s's first step groups, from registers;
+//   wait for this wavefront's loads of box s + 1; barrier (all loads of box
+//     s + 1 have landed, every wavefront is done reading box s);
+//   loads of box s + 2 into box s's buffer;
+//   LDS reads of box s + 1's fragments, interleaved with the MFMAs of box s's
+//     last step group.
+// Nothing is staged in registers but the fragments, so a workgroup of eight
+// wavefronts (two per SIMD) fits a 256 x 128 fp32 tile.
+#pragma once
+#include "kernel.hpp"
+
+namespace gett {
+
+typedef __attribute__((address_space(1))) void global_void;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// The pieces of one operand tile (ROWS x KT elements) one thread loads per
+// box: J per thread, piece p = (j * NW + wave) * 64 + lane of the tile's LDS
+// image.
+template <typename T, int ROWS, int KT, int MODE, int NTH>
+struct DirectOperand {
+    static constexpr int VW = Traits<T>::VW;
+    static constexpr int NW = NTH / 64;
+    static constexpr int PIECES = ROWS * KT / VW;
+    static constexpr int J = PIECES / NTH;
+    static constexpr int CPR = KT / VW;     // k-vector layout: pieces per row
+    static constexpr int RPL = ROWS / VW;   // row-vector layout: pieces per line
+    static_assert(MODE == kGatherRowVec || MODE == kGatherKVec, "vector gathers only");
+    static_assert(PIECES % NTH == 0 && J >= 1, "whole pieces per thread");
+    static_assert(ROWS % VW == 0 && KT % VW == 0, "whole vectors");
+    static_assert((CPR & (CPR - 1)) == 0, "the k-vector permutation needs 2^n pieces per row");
+
+    int goff[J];   // element offset of each piece (tile base and box origin excluded)
+
+    // LDS column (in pieces) of piece c of row r in the k-vector layout; an
+    // involution, so it also maps an LDS column back to its piece
+    static __device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 2) & (CPR - 1)); }
+
+    __device__ __forceinline__ void setup(int tid, const int *rowoff, const int *koff)
+    {
+        const int lane = tid & 63, w = tid >> 6;
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const int p = (j * NW + w) * 64 + lane;
+            if constexpr (MODE == kGatherKVec) {
+                const int r = p / CPR;
+                goff[j] = rowoff[r] + koff[VW * swz(r, p % CPR)];
+            } else {
+                goff[j] = rowoff[VW * (p % RPL)] + koff[p / RPL];
+            }
+        }
+    }
+
+    // copy this thread's pieces of the box at `base` into the tile image `dst`
+    __device__ __forceinline__ void issue(const T *base, T *dst, int w) const
+    {
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+            __builtin_amdgcn_global_load_lds((global_void *)(base + goff[j]),
+                                             (lds_void *)(dst + (j * NW + w) * 64 * VW), 16, 0,
+                                             0);
+    }
+};
+
+// Fragments of one step group (VW MFMA steps) for the NB blocks of one side
+// of a wavefront's register tile.  Block b's lane l16 stands for tile row
+// w0 + block_row<R>(b, l16), as in WaveTile.
+template <typename T, int MODE, int NB, int R, int ROWS, int KT>
+struct DirectFrag {
+    static constexpr int VW = Traits<T>::VW;
+    typedef typename Traits<T>::vec vec;
+    typedef RVec<T, R> RV;
+    static constexpr bool kKV = MODE == kGatherKVec;
+    static constexpr int CPR = KT / VW;
+    static constexpr int kReads = kKV ? NB : VW * (NB / R);   // LDS reads per group
+    // k-vector: one piece per block (VW positions of its row); row-vector:
+    // one read of R rows per block group for each of the VW steps
+    vec kv[kKV ? NB : 1];
+    typename RV::type rv[kKV ? 1 : VW][kKV ? 1 : NB / R];
+
+    __device__ __forceinline__ void read(const T *tile, int w0, int l16, int g, int grp)
+    {
+        if constexpr (kKV) {
+            const int q = 4 * grp + g;   // piece of positions kp(VW grp .. VW grp + VW - 1, g)
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                const int r = w0 + block_row<R>(b, l16);
+                kv[b] = *reinterpret_cast<const vec *>(tile + r * KT +
+                                                      VW * (q ^ ((r >> 2) & (CPR - 1))));
+            }
+        } else {
+#pragma unroll
+            for (int s4 = 0; s4 < VW; ++s4) {
+                const int k = 4 * VW * grp + VW * g + s4;
+#pragma unroll
+                for (int gi = 0; gi < NB / R; ++gi)
+                    rv[s4][gi] = *reinterpret_cast<const typename RV::type *>(
+                        tile + k * ROWS + w0 + gi * 16 * R + R * l16);
+            }
+        }
+    }
+    // the value block b supplies in step s4 of the group
+    __device__ __forceinline__ T at(int b, int s4) const
+    {
+        if constexpr (kKV) return kv[b][s4];
+        else return RV::at(rv[s4][b / R], b % R);
+    }
+};
+
+// Origins of the K boxes, taken in order (every box whole): the block along
+// index kj advances by one; when it wraps, the next contracted index
+// advances; only when that one wraps too is the origin decomposed afresh
+// (box_origin).  The state is the same on every lane and is kept in scalar
+// registers (as vector registers it cost the K loop 3% on the 4096^3-shaped
+// fp32 contraction).
+struct DirectWalk {
+    int64_t ox, oy;     // origin of box `next` in X and Y
+    int64_t bx, by;     // step of one block along index kj
+    int64_t sx1, sy1;   // strides of index kj + 1
+    uint32_t next;
+    int blk, c1, nblk, e1;
+
+    __device__ __forceinline__ void init(const KDesc &d)
+    {
+        nblk = d.nblk > 0 ? d.nblk : 1;
+        bx = (int64_t)d.tj * d.strXk[d.kj];
+        by = (int64_t)d.tj * d.strYk[d.kj];
+        const bool later = d.kj + 1 < d.nk;
+        e1 = later ? d.extK[d.kj + 1] : 0;
+        sx1 = later ? d.strXk[d.kj + 1] : 0;
+        sy1 = later ? d.strYk[d.kj + 1] : 0;
+        next = 0;
+        blk = 0;
+        c1 = 0;
+        box_origin(d, 0, ox, oy);
+    }
+    // origin of box `next`; then step to the box after it
+    __device__ __forceinline__ void take(const KDesc &d, int64_t &x, int64_t &y)
+    {
+        x = ox;
+        y = oy;
+        ++next;
+        if (++blk < nblk) {
+            ox += bx;
+            oy += by;
+        } else if (++c1 < e1) {
+            blk = 0;
+            ox += sx1 - (int64_t)(nblk - 1) * bx;
+            oy += sy1 - (int64_t)(nblk - 1) * by;
+        } else {
+            blk = 0;
+            c1 = 0;
+            box_origin(d, next, ox, oy);
+        }
+        blk = uniform(blk);
+        c1 = uniform(c1);
+        ox = uniform(ox);
+        oy = uniform(oy);
+    }
+};
+
+template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int XMODE,
+          int YMODE>
+__global__ void __launch_bounds__(WM *WN * 64) __attribute__((amdgpu_waves_per_eu(2)))
+gett_direct_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
+                   T *__restrict__ C, const T alpha, const T beta)
+{
+    constexpr int NTH = WM * WN * 64;
+    constexpr int VW = Traits<T>::VW;
+    constexpr int NG = KT / (4 * VW);   // step groups per box
+    static_assert(KT % (4 * VW) == 0, "whole step groups");
+    typedef WaveTile<T, MT, NT, KT, WM, WN, RX, RY> WT;
+    typedef DirectOperand<T, MT, KT, XMODE, NTH> OX;
+    typedef DirectOperand<T, NT, KT, YMODE, NTH> OY;
+    typedef DirectFrag<T, XMODE, WT::RB, RX, MT, KT> FX;
+    typedef DirectFrag<T, YMODE, WT::CB, RY, NT, KT> FY;
+    constexpr int STAGE = (MT + NT) * KT;
+
+    // the two box buffers: dynamic LDS of 2 * STAGE elements (the compiler
+    // then does not wait for the loads in flight into one buffer before
+    // reading the other)
+    extern __shared__ __attribute__((aligned(16))) char dyn_lds[];
+    T *panels = reinterpret_cast<T *>(dyn_lds);
+    __shared__ int rowX[MT], rowY[NT], offCx[MT], offCy[NT];
+    __shared__ int kX[KT], kY[KT], kco[KT];
+
+    const int tid = (int)threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int ntiles = d.tilesX * d.tilesY;
+    box_tables<KT, NTH>(d, tid, kX, kY, kco);
+    WT w;
+    w.init(tid);
+    int tx, ty;
+    tile_of_block(d, d.tile0 + (int)blockIdx.x, ntiles, tx, ty);
+    const TileBase tb = tile_base<MT, NT>(d, tx, ty);
+    tile_tables<MT, NT, NTH>(d, tx, ty, tb, tid, rowX, offCx, rowY, offCy);
+    const T *Xt = X + tb.x;
+    const T *Yt = Y + tb.y;
+    T *Ct = C + (tb.cx + tb.cy);
+    __syncthreads();
+
+    OX ox;
+    OY oy;
+    ox.setup(tid, rowX, kX);
+    oy.setup(tid, rowY, kY);
+    w.zero();
+    const uint32_t nsteps = (uint32_t)d.nsteps;
+    const int l16 = tid & 15, g = (tid & 63) >> 4;
+    const int xw = w.wm * WT::WTM, yw = w.wn * WT::WTN;
+
+    DirectWalk walk;
+    if (nsteps > 0) walk.init(d);
+    auto issue = [&](int buf) {   // the boxes in order: 0, 1, 2, ...
+        int64_t bx, by;
+        walk.take(d, bx, by);
+        T *st = panels + buf * STAGE;
+        ox.issue(Xt + bx, st, wave);
+        oy.issue(Yt + by, st + MT * KT, wave);
+    };
+    auto read = [&](FX (&fx)[NG], FY (&fy)[NG], int buf) {
+        const T *st = panels + buf * STAGE;
+#pragma unroll
+        for (int grp = 0; grp < NG; ++grp) {
+            fx[grp].read(st, xw, l16, g, grp);
+            fy[grp].read(st + MT * KT, yw, l16, g, grp);
+        }
+    };
+    auto mma = [&](const FX &fx, const FY &fy) {
+#pragma unroll
+        for (int s4 = 0; s4 < VW; ++s4)
+#pragma unroll
+            for (int a = 0; a < WT::RB; ++a)
+#pragma unroll
+                for (int b = 0; b < WT::CB; ++b)
+                    w.acc[a][b] = mfma16x16x4(fx.at(a, s4), fy.at(b, s4), w.acc[a][b]);
+    };
+    // s_barrier with no fence: a workgroup-scope release would wait for the
+    // loads in flight into the other buffer (they count as LDS writes)
+    auto barrier = []() { asm volatile("s_barrier" ::: "memory"); };
+    constexpr int LOADS = OX::J + OY::J;   // load instructions per box and thread
+    // s_waitcnt: vmcnt n (gfx9 encoding: low bits 3:0, high bits 15:14),
+    // expcnt and lgkmcnt untouched / lgkmcnt 0
+    constexpr int kVm0 = (7 << 4) | (15 << 8);
+    constexpr int kVmBox = (LOADS & 15) | ((LOADS >> 4) << 14) | (7 << 4) | (15 << 8);
+    constexpr int kVmLgk0 = 7 << 4;
+    static_assert(LOADS < 64, "vmcnt range");
+
+    if (nsteps > 0) {
+        FX fx[NG];
+        FY fy[NG];
+        issue(0);
+        if (nsteps > 1) {
+            issue(1);
+            __builtin_amdgcn_s_waitcnt(kVmBox);   // box 0's loads (box 1's may be in flight)
+        } else {
+            __builtin_amdgcn_s_waitcnt(kVm0);
+        }
+        barrier();
+        read(fx, fy, 0);
+        for (uint32_t s = 0; s + 1 < nsteps; ++s) {
+#pragma unroll
+            for (int grp = 0; grp + 1 < NG; ++grp) mma(fx[grp], fy[grp]);
+            __builtin_amdgcn_s_waitcnt(kVmLgk0);   // box s + 1 loaded, box s read
+            barrier();
+            if (s + 2 < nsteps) issue((int)(s & 1));   // box s + 2
+            FX gx[NG];
+            FY gy[NG];
+            read(gx, gy, (int)((s + 1) & 1));
+            mma(fx[NG - 1], fy[NG - 1]);
+            // one fragment read after every few MFMAs of the last group
+            constexpr int NREAD = NG * (FX::kReads + FY::kReads);
+            constexpr int NMFMA = VW * WT::RB * WT::CB;
+#pragma unroll
+            for (int r = 0; r < NREAD; ++r) {
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, NMFMA / NREAD > 0 ? NMFMA / NREAD : 1,
+                                                     0);
+            }
+#pragma unroll
+            for (int grp = 0; grp < NG; ++grp) {
+                fx[grp] = gx[grp];
+                fy[grp] = gy[grp];
+            }
+        }
+#pragma unroll
+        for (int grp = 0; grp < NG; ++grp) mma(fx[grp], fy[grp]);
+    }
+    w.template unpack<1>(Ct, offCx, offCy, alpha, beta, d.cvec != 0);
+}
+
+}  // namespace gett

@@ -5,6 +5,7 @@
 
 #include <atomic>
 
+#include "direct.hpp"
 #include "kernel.hpp"
 #include "plan.hpp"
 #include "tiles.hpp"
@@ -41,6 +42,22 @@ unsigned persistent_grid(K kernel, int threads, unsigned tiles)
         if (dev >= 0 && dev < 64) cached[dev].store(n, std::memory_order_relaxed);
     }
     return (unsigned)n < tiles ? (unsigned)n : tiles;
+}
+
+// Let a kernel take `bytes` of dynamic LDS (above the default cap), once per
+// kernel and device (up to 64 devices; a later device asks again).
+template <typename K>
+hipError_t allow_dynamic_lds(K kernel, size_t bytes)
+{
+    static std::atomic<int> done[64];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev >= 0 && dev < 64 && done[dev].load(std::memory_order_relaxed)) return hipSuccess;
+    e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e == hipSuccess && dev >= 0 && dev < 64) done[dev].store(1, std::memory_order_relaxed);
+    return e;
 }
 
 template <typename T, int TI, int XM, int YM, int KIND>
@@ -81,6 +98,20 @@ hipError_t launch_one(const KDesc &d, const void *X, const void *Y, void *C, dou
             dim3((unsigned)d.tailFull + (unsigned)d.tailWgs), dim3(threads), 0, stream, d,
             static_cast<const T *>(X), static_cast<const T *>(Y), static_cast<T *>(C),
             static_cast<T>(alpha), static_cast<T>(beta), static_cast<T *>(w.tiles), w.counters);
+    } else if constexpr (KIND == 4) {
+        // every tile row and K box inside the tensors, whole tiles only
+        if (d.kslices > 1 || d.sizeX % t.mt || d.sizeY % t.nt ||
+            (d.nsteps > 0 && (d.kbox != t.kt || d.extK[d.kj] % d.tj)))
+            return hipErrorInvalidValue;
+        if ((unsigned)d.tile0 >= tiles) return hipSuccess;
+        auto k = gett_direct_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, XM, YM>;
+        constexpr size_t lds = 2 * (size_t)(t.mt + t.nt) * t.kt * sizeof(T);
+        const hipError_t e = allow_dynamic_lds(k, lds);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(
+            k, dim3(tiles - (unsigned)d.tile0), dim3(threads), lds, stream, d,
+            static_cast<const T *>(X), static_cast<const T *>(Y), static_cast<T *>(C),
+            static_cast<T>(alpha), static_cast<T>(beta));
     } else {
         auto k = gett_stream_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.stream, XM, YM>;
         const unsigned grid = persistent_grid(k, threads, tiles);
@@ -97,12 +128,15 @@ LaunchFn pick_modes(int xm, int ym, int kind)
 {
     constexpr bool kStream = TileTable<T>::tiles[TI].stream != 0;
     constexpr bool kTail = TileTable<T>::tiles[TI].tail != 0;
+    constexpr bool kDirect = TileTable<T>::tiles[TI].deff > 0.0f;
 #define GETT_CASE(a, b)                                                                       \
     if (xm == a && ym == b) {                                                                 \
+        constexpr bool kDir = kDirect && a <= 1 && b <= 1;   /* vector gathers only */       \
         if (kind == 0) return &launch_one<T, TI, a, b, 0>;                                   \
         if (kind == 2) return &launch_one<T, TI, a, b, 2>;                                   \
         if (kind == 1 && kStream) return &launch_one<T, TI, a, b, kStream ? 1 : 0>;          \
         if (kind == 3 && kTail) return &launch_one<T, TI, a, b, kTail ? 3 : 0>;              \
+        if (kind == 4 && kDir) return &launch_one<T, TI, a, b, kDir ? 4 : 0>;                \
         return nullptr;                                                                       \
     }
     GETT_CASE(0, 0) GETT_CASE(0, 1) GETT_CASE(0, 2) GETT_CASE(0, 3) GETT_CASE(0, 4)

@@ -32,7 +32,8 @@ struct Analysis {
 struct Candidate {
     int tile = 0, kind = 0;                 // kind 0: macro-kernel, 1: streaming kernel,
                                             // 2: macro-kernel over K slices,
-                                            // 3: stream-K tail kernel
+                                            // 3: stream-K tail kernel,
+                                            // 4: direct-load kernel
     int slices = 1;                         // workgroups per tile (kind 2), tail
                                             // workgroups (kind 3)
     double tMfma = 0, tMem = 0, cost = 0;   // seconds
@@ -89,7 +90,8 @@ struct gett_plan_s {
     int xmode, ymode;        // gather modes of the preferred kernel
     int kind;                // 0: macro-kernel, 1: persistent streaming kernel,
                              // 2: macro-kernel over K slices (desc.kslices > 1),
-                             // 3: stream-K tail kernel (desc.tailFull ...)
+                             // 3: stream-K tail kernel (desc.tailFull ...),
+                             // 4: direct-load kernel
     std::vector<gett::Candidate> ranked;   // every candidate, best model estimate first
     // the arguments of gett_plan, kept to re-plan with another candidate
     std::string modes[3];
@@ -137,7 +139,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
 gett_status_t contract_with(const gett_plan_s &P, double alpha, const void *A, const void *B,
                             double beta, void *C, hipStream_t stream, WorkspaceFn ws);
 
-// "macro", "stream", "kslices" or "tail" (Candidate::kind).
+// "macro", "stream", "kslices", "tail" or "direct" (Candidate::kind).
 const char *kind_name(int kind);
 // Launch table lookup (defined with the kernel instantiations).  kind 0: the
 // macro-kernel, 1: the persistent streaming kernel.

@@ -27,6 +27,9 @@ struct TileShape {
                  // for contracted sets that fit one K box; fewer registers live at once
     int corder;  // 1: the kernel carries the C-order epilogue (unpack_c_order)
     int tail;    // 1: also compiled as the stream-K tail kernel
+    float deff;  // > 0: also compiled as the direct-load kernel (operands copied
+                 // straight into LDS), which sustains this fraction of the MFMA
+                 // peak when compute-bound
 };
 
 constexpr TileShape kTilesF32[] = {
@@ -34,9 +37,10 @@ constexpr TileShape kTilesF32[] = {
     {64, 64, 16, 1, 1, 4, 4, 1, 1, 2, 0, 0.67f, 0.62f, 0.0f, 0, 1},
     {128, 128, 16, 2, 2, 4, 4, 3, 1, 2, 2, 0.71f, 0.675f, 0.64f, 0, 1, 1},
     {64, 256, 16, 1, 4, 4, 4, 3, 1, 2, 2, 0.70f, 0.70f, 0.63f, 0, 1},
-    {128, 128, 32, 2, 2, 4, 4, 1, 1, 2, 0, 0.806f, 0.61f, 0.0f, 0, 1},
+    {128, 128, 32, 2, 2, 4, 4, 1, 1, 2, 0, 0.806f, 0.61f, 0.0f, 0, 1, 0, 0.87f},
     {64, 32, 32, 2, 2, 2, 1, 2, 2, 2, 0, 0.64f, 0.35f, 0.0f},
     {32, 64, 32, 2, 2, 1, 2, 2, 2, 2, 0, 0.65f, 0.35f, 0.0f},
+    {256, 128, 32, 4, 2, 4, 4, 2, 1, 2, 0, 0.75f, 0.55f, 0.0f, 0, 0, 0, 0.89f},
 };
 constexpr TileShape kTilesF64[] = {
     {128, 128, 16, 2, 2, 2, 2, 1, 2, 2, 0, 0.65f, 0.34f, 0.0f},

@@ -7,8 +7,9 @@ tests cannot see it (the 64 x 256 fp32 tile beside an element-wise gather
 once spilled 176 bytes per lane and ran twice as long).  For each workload
 and a few Appendix A contractions whose kernels sit at their register caps,
 the kernel of the model's plan must not spill (the stream-K tail kernel,
-whose piece loop carries more state, within a small budget), and the
-one-box fp64 tile must stay within 128 VGPRs: four wavefronts per SIMD."""
+whose piece loop carries more state, within a small budget), the one-box
+fp64 tile must stay within 128 VGPRs (four wavefronts per SIMD), and the
+direct-load kernels within 256 (two)."""
 import json
 import os
 import re
@@ -28,6 +29,7 @@ MODES = {"row-vector": 0, "k-vector": 1, "scalar": 2, "row-vector-strided": 3,
          "k-vector-strided": 4}
 BUNDLE = b"__CLANG_OFFLOAD_BUNDLE__"
 NAME = re.compile(r"_ZN4gett17gett_macro_kernelI([fd])((?:Li\d+E)+)EEv")
+DIRECT = re.compile(r"_ZN4gett18gett_direct_kernelI([fd])((?:Li\d+E)+)EEv")
 TAIL_SCRATCH_BUDGET = 64   # bytes per lane
 
 
@@ -71,13 +73,15 @@ def kernels():
             notes = subprocess.run([f"{LLVM}/llvm-readelf", "--notes", path], check=True,
                                    capture_output=True, text=True).stdout
             for blk in notes.split("\n  - ")[1:]:
-                m = NAME.search(blk)
+                m, kind = NAME.search(blk), "macro"
+                if not m:
+                    m, kind = DIRECT.search(blk), "direct"
                 if not m:
                     continue
                 field = lambda key: int(re.search(rf"\.{key}:\s+(\d+)", blk).group(1))
                 args = tuple(int(x) for x in re.findall(r"Li(\d+)E", m.group(2)))
-                res[(m.group(1), args)] = (field("private_segment_fixed_size"),
-                                           field("vgpr_count"))
+                key = (m.group(1), args) if kind == "macro" else ("direct", m.group(1), args)
+                res[key] = (field("private_segment_fixed_size"), field("vgpr_count"))
     finally:
         shutil.rmtree(tmp)
     assert len(res) > 100, "too few kernels found in the library's code objects"
@@ -86,8 +90,9 @@ def kernels():
 
 def plan_kernel(w, kernels):
     """The resources of the kernel the model's plan for workload w launches.
-    Template integer arguments: MT NT KT WM WN RX RY WPE PF NBUF XMODE YMODE
-    ONEBOX CORDER TAIL SLICED, all given by the plan's description."""
+    Template integer arguments of the macro-kernel: MT NT KT WM WN RX RY WPE
+    PF NBUF XMODE YMODE ONEBOX CORDER TAIL SLICED; of the direct-load kernel:
+    MT NT KT WM WN RX RY XMODE YMODE; all given by the plan's description."""
     code = g.GETT_FLOAT32 if w.dtype == "f32" else g.GETT_FLOAT64
     st, h = g.gett_plan(code, w.modes_C, w.shape("C"), None, w.modes_A, w.shape("A"), None,
                         w.modes_B, w.shape("B"), None, 0)
@@ -97,14 +102,19 @@ def plan_kernel(w, kernels):
     finally:
         g.gett_destroy(h)
     t = d["tile"]
+    T = "f" if w.dtype == "f32" else "d"
+    if d["kernel"] == "direct":
+        args = (t["mt"], t["nt"], t["kt"], t["waves"][0], t["waves"][1], t["reads"][0],
+                t["reads"][1], MODES[d["gather_x"]], MODES[d["gather_y"]])
+        assert ("direct", T, args) in kernels, (w.name, args)
+        return d, args, kernels[("direct", T, args)]
     want = {0: t["mt"], 1: t["nt"], 2: t["kt"], 3: t["waves"][0], 4: t["waves"][1],
             5: t["reads"][0], 6: t["reads"][1], 7: t["waves_per_simd"], 8: t["prefetch"],
             9: t["lds_buffers"], 10: MODES[d["gather_x"]], 11: MODES[d["gather_y"]],
             12: int(t["one_box"]), 13: int(t["c_order_epilogue"]),
             14: int(d["kernel"] == "tail"), 15: int(d["kslices"] > 1)}
-    T = "f" if w.dtype == "f32" else "d"
-    hits = [(a, v) for (tt, a), v in kernels.items()
-            if tt == T and all(a[i] == x for i, x in want.items())]
+    hits = [(a, v) for key, v in kernels.items() if len(key) == 2
+            for (tt, a) in [key] if tt == T and all(a[i] == x for i, x in want.items())]
     assert len(hits) == 1, (w.name, d["tile"], d["kernel"], hits)
     return d, hits[0][0], hits[0][1]
 
@@ -124,6 +134,21 @@ def test_model_kernel_does_not_spill(kernels, name, w):
     d, args, (scratch, vgprs) = plan_kernel(w, kernels)
     budget = TAIL_SCRATCH_BUDGET if d["kernel"] == "tail" else 0
     assert scratch <= budget, f"{name}: kernel {args} spills {scratch} bytes per lane"
+
+
+def test_direct_kernels_keep_two_wavefronts_per_simd(kernels):
+    """Every direct-load kernel: no spills, at most 256 VGPRs (two
+    wavefronts per SIMD: the 256 x 128 tile's eight, or two workgroups of
+    four)."""
+    direct = {k: v for k, v in kernels.items() if k[0] == "direct"}
+    assert len(direct) >= 8, "the direct-load kernels of both fp32 tiles"
+    for key, (scratch, vgprs) in direct.items():
+        assert scratch == 0 and vgprs <= 256, (key, scratch, vgprs)
+
+
+def test_compute_bound_fp32_workload_runs_direct(kernels):
+    d, args, (scratch, vgprs) = plan_kernel(wl.BY_NAME["gemm4_fp32"], kernels)
+    assert d["kernel"] == "direct" and (args[0], args[1]) == (256, 128)
 
 
 def test_one_box_tile_keeps_four_wavefronts_per_simd(kernels):
