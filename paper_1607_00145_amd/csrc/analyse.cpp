@@ -458,21 +458,18 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
             ++b.kj;
         }
         int64_t tj = std::max<int64_t>(1, std::min<int64_t>(K[b.kj].extent, kt / prefix));
-        // Prefer a block length that divides the index (no ragged last block)
-        // unless that would lose more than half of the box.
-        {
-            int64_t best = tj;
-            for (int64_t t = tj; t >= 1; --t)
-                if (K[b.kj].extent % t == 0) { best = t; break; }
-            if (best * 2 > tj) tj = best;
-        }
         // The block of the index that vectors run along holds whole vectors.
-        if (b.kj == kvi && (wantKvec || kvi > 0) && tj % VW) {
-            const int64_t t2 = (tj / VW) * VW;
-            if (t2 >= VW) {
-                tj = t2;
-                while (K[b.kj].extent % tj && tj > VW) tj -= VW;   // keep it dividing when possible
-            }
+        // A block length that divides the index (no ragged last block) is
+        // preferred unless that would lose more than half of the box (92 in
+        // blocks of 4 would be 23 boxes an eighth full, against 32, 32, 28).
+        const bool vec = b.kj == kvi && (wantKvec || kvi > 0);
+        const int64_t step = vec ? VW : 1;
+        const int64_t top = vec && tj >= VW ? (tj / VW) * VW : tj;
+        if (top >= step) {
+            int64_t best = top;
+            for (int64_t t = top; t >= step; t -= step)
+                if (K[b.kj].extent % t == 0) { best = t; break; }
+            tj = best * 2 > top ? best : top;
         }
         b.tj = tj;
         b.kbox = prefix * tj;
@@ -645,12 +642,10 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
             ranked.push_back(cd);
         }
         // Direct-load kernel (tiles that carry it): both operands gathered in
-        // vectors, every tile row inside the tensors, every K box whole.  It
-        // sustains deff of the MFMA peak where the macro-kernel sustains eff;
-        // its memory stream is priced as the macro-kernel's.
+        // vectors.  It sustains deff of the MFMA peak where the macro-kernel
+        // sustains eff; its memory stream is priced as the macro-kernel's.
         if (c.deff > 0.0f && !slowGather && !(flags & GETT_FLAG_SCALAR) && !kSplitAhead &&
-            sizeX % c.mt == 0 && sizeY % c.nt == 0 && b.nsteps >= 1 && b.kbox == c.kt &&
-            Ik[b.kj].extent % b.tj == 0) {
+            b.nsteps >= 1) {
             const double tMem = (bytesC + bytesX + bytesY +
                                  0.05 * (bytesX * (ty - 1) + bytesY * (tx - 1))) /
                                 (8.0e12 * c.bw * cuShare);
@@ -951,12 +946,9 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         else if (row_vec_ok(Iy, sY)) ymode = kGatherRowVec;
         else if (k_vec_ok(Iy, sY)) ymode = kGatherKVec;
     }
-    // The direct-load kernel takes vector gathers, whole tiles and whole K
-    // boxes; a plan that ends up otherwise runs its tile's macro-kernel.
-    if (kind == 4 && !(xmode <= kGatherKVec && ymode <= kGatherKVec && sizeX % ts.mt == 0 &&
-                       sizeY % ts.nt == 0 && nsteps >= 1 && kbox == ts.kt &&
-                       Ik[kj].extent % tj == 0))
-        kind = 0;
+    // The direct-load kernel takes vector gathers of both operands; a plan
+    // that ends up otherwise runs its tile's macro-kernel.
+    if (kind == 4 && !(xmode <= kGatherKVec && ymode <= kGatherKVec && nsteps >= 1)) kind = 0;
     bool cvec = !(flags & GETT_FLAG_SCALAR) && Iy[0].strC == 1 && Iy[0].extent % VW == 0;
     for (auto &x : Ix) if (x.strC % VW) cvec = false;
     for (size_t i = 1; i < Iy.size(); ++i) if (Iy[i].strC % VW) cvec = false;

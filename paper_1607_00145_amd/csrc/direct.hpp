@@ -39,8 +39,11 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 // The pieces of one operand tile (ROWS x KT elements) one thread loads per
 // box: J per thread, piece p = (j * NW + wave) * 64 + lane of the tile's LDS
-// image.
-template <typename T, int ROWS, int KT, int MODE, int NTH>
+// image.  A piece outside the tensor (its rows past the tile's last, or its
+// contracted positions past the box's valid ones) is not loaded: the thread
+// writes zeros to its place instead, as the macro-kernel's gathers do.
+// WHOLE: every piece of every box is inside (no checks).
+template <typename T, int ROWS, int KT, int MODE, int NTH, bool WHOLE>
 struct DirectOperand {
     static constexpr int VW = Traits<T>::VW;
     static constexpr int NW = NTH / 64;
@@ -52,36 +55,53 @@ struct DirectOperand {
     static_assert(PIECES % NTH == 0 && J >= 1, "whole pieces per thread");
     static_assert(ROWS % VW == 0 && KT % VW == 0, "whole vectors");
     static_assert((CPR & (CPR - 1)) == 0, "the k-vector permutation needs 2^n pieces per row");
+    typedef typename Traits<T>::vec vec;
 
-    int goff[J];   // element offset of each piece (tile base and box origin excluded)
+    int goff[J];               // element offset of each piece (tile base and box origin excluded)
+    int kc[WHOLE ? 1 : J];     // position along index kj of its first element; kInvalidK: never valid
+    int lane;
 
     // LDS column (in pieces) of piece c of row r in the k-vector layout; an
     // involution, so it also maps an LDS column back to its piece
     static __device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 2) & (CPR - 1)); }
 
-    __device__ __forceinline__ void setup(int tid, const int *rowoff, const int *koff)
+    // rowoff: LDS table of operand offsets per tile row (-1 = outside the
+    // tensor); koff / kco: offsets / kj-positions per box position
+    __device__ __forceinline__ void setup(int tid, const int *rowoff, const int *koff,
+                                          const int *kco)
     {
-        const int lane = tid & 63, w = tid >> 6;
+        lane = tid & 63;
+        const int w = tid >> 6;
 #pragma unroll
         for (int j = 0; j < J; ++j) {
             const int p = (j * NW + w) * 64 + lane;
+            int r, kk;
             if constexpr (MODE == kGatherKVec) {
-                const int r = p / CPR;
-                goff[j] = rowoff[r] + koff[VW * swz(r, p % CPR)];
+                r = p / CPR;
+                kk = VW * swz(r, p % CPR);
             } else {
-                goff[j] = rowoff[VW * (p % RPL)] + koff[p / RPL];
+                r = VW * (p % RPL);
+                kk = p / RPL;
             }
+            const int ro = rowoff[r];
+            goff[j] = (ro < 0 ? 0 : ro) + koff[kk];
+            if constexpr (!WHOLE) kc[j] = ro < 0 ? kInvalidK : kco[kk];
         }
     }
 
-    // copy this thread's pieces of the box at `base` into the tile image `dst`
-    __device__ __forceinline__ void issue(const T *base, T *dst, int w) const
+    // copy this thread's pieces of the box at `base` (`lim` valid positions
+    // along index kj) into the tile image `dst`
+    __device__ __forceinline__ void issue(const T *base, T *dst, int w, int lim) const
     {
 #pragma unroll
-        for (int j = 0; j < J; ++j)
-            __builtin_amdgcn_global_load_lds((global_void *)(base + goff[j]),
-                                             (lds_void *)(dst + (j * NW + w) * 64 * VW), 16, 0,
-                                             0);
+        for (int j = 0; j < J; ++j) {
+            T *slot = dst + (j * NW + w) * 64 * VW;
+            if (WHOLE || kc[WHOLE ? 0 : j] < lim)
+                __builtin_amdgcn_global_load_lds((global_void *)(base + goff[j]),
+                                                 (lds_void *)slot, 16, 0, 0);
+            else
+                *reinterpret_cast<vec *>(slot + lane * VW) = vec{};
+        }
     }
 };
 
@@ -141,11 +161,13 @@ struct DirectWalk {
     int64_t bx, by;     // step of one block along index kj
     int64_t sx1, sy1;   // strides of index kj + 1
     uint32_t next;
-    int blk, c1, nblk, e1;
+    int blk, c1, nblk, e1, ek, tj;
 
     __device__ __forceinline__ void init(const KDesc &d)
     {
         nblk = d.nblk > 0 ? d.nblk : 1;
+        ek = d.extK[d.kj];
+        tj = d.tj;
         bx = (int64_t)d.tj * d.strXk[d.kj];
         by = (int64_t)d.tj * d.strYk[d.kj];
         const bool later = d.kj + 1 < d.nk;
@@ -157,11 +179,13 @@ struct DirectWalk {
         c1 = 0;
         box_origin(d, 0, ox, oy);
     }
-    // origin of box `next`; then step to the box after it
-    __device__ __forceinline__ void take(const KDesc &d, int64_t &x, int64_t &y)
+    // origin of box `next` and its valid positions along index kj; then step
+    // to the box after it
+    __device__ __forceinline__ int take(const KDesc &d, int64_t &x, int64_t &y)
     {
         x = ox;
         y = oy;
+        const int lim = ek - blk * tj;
         ++next;
         if (++blk < nblk) {
             ox += bx;
@@ -179,11 +203,12 @@ struct DirectWalk {
         c1 = uniform(c1);
         ox = uniform(ox);
         oy = uniform(oy);
+        return lim;
     }
 };
 
 template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int XMODE,
-          int YMODE>
+          int YMODE, bool WHOLE>
 __global__ void __launch_bounds__(WM *WN * 64) __attribute__((amdgpu_waves_per_eu(2)))
 gett_direct_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
                    T *__restrict__ C, const T alpha, const T beta)
@@ -193,8 +218,8 @@ gett_direct_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
     constexpr int NG = KT / (4 * VW);   // step groups per box
     static_assert(KT % (4 * VW) == 0, "whole step groups");
     typedef WaveTile<T, MT, NT, KT, WM, WN, RX, RY> WT;
-    typedef DirectOperand<T, MT, KT, XMODE, NTH> OX;
-    typedef DirectOperand<T, NT, KT, YMODE, NTH> OY;
+    typedef DirectOperand<T, MT, KT, XMODE, NTH, WHOLE> OX;
+    typedef DirectOperand<T, NT, KT, YMODE, NTH, WHOLE> OY;
     typedef DirectFrag<T, XMODE, WT::RB, RX, MT, KT> FX;
     typedef DirectFrag<T, YMODE, WT::CB, RY, NT, KT> FY;
     constexpr int STAGE = (MT + NT) * KT;
@@ -224,8 +249,8 @@ gett_direct_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
 
     OX ox;
     OY oy;
-    ox.setup(tid, rowX, kX);
-    oy.setup(tid, rowY, kY);
+    ox.setup(tid, rowX, kX, kco);
+    oy.setup(tid, rowY, kY, kco);
     w.zero();
     const uint32_t nsteps = (uint32_t)d.nsteps;
     const int l16 = tid & 15, g = (tid & 63) >> 4;
@@ -235,10 +260,10 @@ gett_direct_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
     if (nsteps > 0) walk.init(d);
     auto issue = [&](int buf) {   // the boxes in order: 0, 1, 2, ...
         int64_t bx, by;
-        walk.take(d, bx, by);
+        const int lim = walk.take(d, bx, by);
         T *st = panels + buf * STAGE;
-        ox.issue(Xt + bx, st, wave);
-        oy.issue(Yt + by, st + MT * KT, wave);
+        ox.issue(Xt + bx, st, wave, lim);
+        oy.issue(Yt + by, st + MT * KT, wave, lim);
     };
     auto read = [&](FX (&fx)[NG], FY (&fy)[NG], int buf) {
         const T *st = panels + buf * STAGE;
@@ -263,8 +288,8 @@ gett_direct_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
     constexpr int LOADS = OX::J + OY::J;   // load instructions per box and thread
     // s_waitcnt: vmcnt n (gfx9 encoding: low bits 3:0, high bits 15:14),
     // expcnt and lgkmcnt untouched / lgkmcnt 0
-    constexpr int kVm0 = (7 << 4) | (15 << 8);
-    constexpr int kVmBox = (LOADS & 15) | ((LOADS >> 4) << 14) | (7 << 4) | (15 << 8);
+    // (lgkmcnt 0 also covers the zeros written in place of pieces outside)
+    constexpr int kVmBox = (LOADS & 15) | ((LOADS >> 4) << 14) | (7 << 4);
     constexpr int kVmLgk0 = 7 << 4;
     static_assert(LOADS < 64, "vmcnt range");
 
@@ -274,9 +299,12 @@ gett_direct_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
         issue(0);
         if (nsteps > 1) {
             issue(1);
-            __builtin_amdgcn_s_waitcnt(kVmBox);   // box 0's loads (box 1's may be in flight)
+            // box 0's loads; box 1's may stay in flight when each box is known
+            // to issue all of its loads (a wavefront skips the loads of
+            // pieces that are all outside, so the count is not known otherwise)
+            __builtin_amdgcn_s_waitcnt(WHOLE ? kVmBox : kVmLgk0);
         } else {
-            __builtin_amdgcn_s_waitcnt(kVm0);
+            __builtin_amdgcn_s_waitcnt(kVmLgk0);
         }
         barrier();
         read(fx, fy, 0);

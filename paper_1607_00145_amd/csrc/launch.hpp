@@ -99,12 +99,13 @@ hipError_t launch_one(const KDesc &d, const void *X, const void *Y, void *C, dou
             static_cast<const T *>(X), static_cast<const T *>(Y), static_cast<T *>(C),
             static_cast<T>(alpha), static_cast<T>(beta), static_cast<T *>(w.tiles), w.counters);
     } else if constexpr (KIND == 4) {
-        // every tile row and K box inside the tensors, whole tiles only
-        if (d.kslices > 1 || d.sizeX % t.mt || d.sizeY % t.nt ||
-            (d.nsteps > 0 && (d.kbox != t.kt || d.extK[d.kj] % d.tj)))
-            return hipErrorInvalidValue;
+        if (d.kslices > 1) return hipErrorInvalidValue;   // whole tiles only
         if ((unsigned)d.tile0 >= tiles) return hipSuccess;
-        auto k = gett_direct_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, XM, YM>;
+        // every piece of every box inside the tensors: the variant without checks
+        const bool whole = d.sizeX % t.mt == 0 && d.sizeY % t.nt == 0 &&
+                           (d.nsteps == 0 || (d.kbox == t.kt && d.extK[d.kj] % d.tj == 0));
+        auto k = whole ? gett_direct_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, XM, YM, true>
+                       : gett_direct_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, XM, YM, false>;
         constexpr size_t lds = 2 * (size_t)(t.mt + t.nt) * t.kt * sizeof(T);
         const hipError_t e = allow_dynamic_lds(k, lds);
         if (e != hipSuccess) return e;

@@ -1,10 +1,12 @@
 """GPU parity of the direct-load kernel, whose operands are copied from device
 memory straight into LDS (fp32 tiles 128 x 128 x 32 and 256 x 128 x 32):
 every pair of vector gather modes, one to five K boxes, boxes over two
-contracted indices, every beta path, alpha = 0, integer inputs (exact
-whatever the order of the additions), and the ways a plan or a call falls
-back to the macro-kernel of its tile (a K box of 24 positions, an operand
-whose base is not 16-byte aligned), against the oracle."""
+contracted indices, ragged tiles and partial boxes (pieces outside the
+tensors written as zeros; a partial last box reuses a buffer that held
+another box), every beta path, alpha = 0, integer inputs (exact whatever the
+order of the additions), and the calls that fall back to the macro-kernel
+of the plan's tile (operands whose base is not 16-byte aligned, alpha = 0),
+against the oracle."""
 import json
 
 import numpy as np
@@ -106,16 +108,44 @@ def test_direct_alpha_zero_and_gemm4_structure(gpu, monkeypatch, tile):
         check_case(gpu, rng, modes, shapes(modes, ext), np.float32, 0.0, beta)
 
 
+# ragged free extents (no multiple of either tile) and contracted sets whose
+# boxes are partial: k = 104 (three boxes of 32 and one of 8, in a buffer
+# that held box 1), k = 28 (one box of 28 positions), and a box over two
+# indices whose last block is short (l = 10 in blocks of 4)
+RAGGED = {
+    "ab-ak-kb": (("a,b", "a,k", "k,b"), {"a": 300, "b": 200, "k": 104}),
+    "ab-ka-kb": (("a,b", "k,a", "k,b"), {"a": 264, "b": 136, "k": 28}),
+    "ab-ak-bk": (("a,b", "a,k", "b,k"), {"a": 140, "b": 388, "k": 104}),
+    "ab-ka-bk": (("a,b", "k,a", "b,k"), {"a": 520, "b": 68, "k": 72}),
+    "abcd-kalb-cldk": (("a,b,c,d", "k,a,l,b", "c,l,d,k"),
+                       {"a": 12, "b": 20, "c": 36, "d": 5, "k": 8, "l": 10}),
+}
+
+
+@pytest.mark.parametrize("name", list(RAGGED))
+@pytest.mark.parametrize("tile", DIRECT_TILES)
+def test_direct_ragged_tiles_and_partial_boxes(gpu, monkeypatch, tile, name):
+    force_direct(monkeypatch, tile)
+    modes, ext = RAGGED[name]
+    d = describe(modes, ext)
+    assert d["kernel"] == "direct"
+    rng = np.random.default_rng(500 + len(name) + int(tile))
+    for alpha, beta in [(1.0, 0.0), (-0.5, 1.5)]:
+        check_case(gpu, rng, modes, shapes(modes, ext), np.float32, alpha, beta)
+    for beta in (0.0, 1.0):
+        got, ref = check_case(gpu, rng, modes, shapes(modes, ext), np.float32, 1.0, beta,
+                              dist="int")
+        np.testing.assert_array_equal(got.astype(np.float64), ref.out64)
+
+
 @pytest.mark.parametrize("tile", DIRECT_TILES)
 def test_direct_fallbacks(gpu, monkeypatch, tile):
-    """A box of 24 positions plans the macro-kernel; operands whose base is
-    not 16-byte aligned (their vector gathers become element-wise) run the
-    macro-kernel of the direct plan's tile."""
+    """Operands whose base is not 16-byte aligned (their vector gathers
+    become element-wise) run the macro-kernel of the direct plan's tile; so
+    does a K box that two operands cannot both gather in vectors."""
     force_direct(monkeypatch, tile)
     modes = ("a,b,c", "a,k,l", "l,k,b,c")
     ext = {"a": 256, "b": 16, "c": 16, "k": 8, "l": 12}
-    d = describe(modes, ext)
-    assert d["kernel"] == "macro"
     rng = np.random.default_rng(11)
     check_case(gpu, rng, modes, shapes(modes, ext), np.float32, 1.0, 1.0)
     modes = MODE_CASES["ab-ak-kb"][0]

@@ -29,7 +29,7 @@ MODES = {"row-vector": 0, "k-vector": 1, "scalar": 2, "row-vector-strided": 3,
          "k-vector-strided": 4}
 BUNDLE = b"__CLANG_OFFLOAD_BUNDLE__"
 NAME = re.compile(r"_ZN4gett17gett_macro_kernelI([fd])((?:Li\d+E)+)EEv")
-DIRECT = re.compile(r"_ZN4gett18gett_direct_kernelI([fd])((?:Li\d+E)+)EEv")
+DIRECT = re.compile(r"_ZN4gett18gett_direct_kernelI([fd])((?:Li\d+E)+)Lb([01])EEEv")
 TAIL_SCRATCH_BUDGET = 64   # bytes per lane
 
 
@@ -80,7 +80,8 @@ def kernels():
                     continue
                 field = lambda key: int(re.search(rf"\.{key}:\s+(\d+)", blk).group(1))
                 args = tuple(int(x) for x in re.findall(r"Li(\d+)E", m.group(2)))
-                key = (m.group(1), args) if kind == "macro" else ("direct", m.group(1), args)
+                key = ((m.group(1), args) if kind == "macro" else
+                       ("direct", m.group(1), args + (int(m.group(3)),)))
                 res[key] = (field("private_segment_fixed_size"), field("vgpr_count"))
     finally:
         shutil.rmtree(tmp)
@@ -92,7 +93,8 @@ def plan_kernel(w, kernels):
     """The resources of the kernel the model's plan for workload w launches.
     Template integer arguments of the macro-kernel: MT NT KT WM WN RX RY WPE
     PF NBUF XMODE YMODE ONEBOX CORDER TAIL SLICED; of the direct-load kernel:
-    MT NT KT WM WN RX RY XMODE YMODE; all given by the plan's description."""
+    MT NT KT WM WN RX RY XMODE YMODE and WHOLE (both variants: which one runs
+    is decided per call); all given by the plan's description."""
     code = g.GETT_FLOAT32 if w.dtype == "f32" else g.GETT_FLOAT64
     st, h = g.gett_plan(code, w.modes_C, w.shape("C"), None, w.modes_A, w.shape("A"), None,
                         w.modes_B, w.shape("B"), None, 0)
@@ -106,8 +108,9 @@ def plan_kernel(w, kernels):
     if d["kernel"] == "direct":
         args = (t["mt"], t["nt"], t["kt"], t["waves"][0], t["waves"][1], t["reads"][0],
                 t["reads"][1], MODES[d["gather_x"]], MODES[d["gather_y"]])
-        assert ("direct", T, args) in kernels, (w.name, args)
-        return d, args, kernels[("direct", T, args)]
+        both = [kernels.get(("direct", T, args + (whole,))) for whole in (0, 1)]
+        assert all(both), (w.name, args)
+        return d, args, (max(v[0] for v in both), max(v[1] for v in both))
     want = {0: t["mt"], 1: t["nt"], 2: t["kt"], 3: t["waves"][0], 4: t["waves"][1],
             5: t["reads"][0], 6: t["reads"][1], 7: t["waves_per_simd"], 8: t["prefetch"],
             9: t["lds_buffers"], 10: MODES[d["gather_x"]], 11: MODES[d["gather_y"]],
@@ -141,7 +144,7 @@ def test_direct_kernels_keep_two_wavefronts_per_simd(kernels):
     wavefronts per SIMD: the 256 x 128 tile's eight, or two workgroups of
     four)."""
     direct = {k: v for k, v in kernels.items() if k[0] == "direct"}
-    assert len(direct) >= 8, "the direct-load kernels of both fp32 tiles"
+    assert len(direct) >= 16, "the direct-load kernels of both fp32 tiles, both variants"
     for key, (scratch, vgprs) in direct.items():
         assert scratch == 0 and vgprs <= 256, (key, scratch, vgprs)
 
