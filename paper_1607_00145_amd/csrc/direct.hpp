@@ -9,9 +9,9 @@
 // loads:
 //   row-vector operand: [k][row], as the macro-kernel packs it (no padding);
 //   k-vector operand:   [row][k], the pieces of row r XOR-permuted by
-//                       (r / 4) mod (pieces per row), so that the lanes of an
-//                       MFMA read, which take rows 4 apart at one k piece,
-//                       fall on different banks.
+//                       (r / R) mod (pieces per row), so that the lanes of an
+//                       MFMA read, which take rows R apart at one k piece
+//                       (R = 4 in fp32, 2 in fp64), fall on different banks.
 // A k-vector piece holds VW consecutive contracted positions, and one LDS
 // read hands them to VW consecutive MFMA steps: the position lane group g
 // supplies in step s is
@@ -42,8 +42,10 @@ typedef __attribute__((address_space(3))) void lds_void;
 // image.  A piece outside the tensor (its rows past the tile's last, or its
 // contracted positions past the box's valid ones) is not loaded: the thread
 // writes zeros to its place instead, as the macro-kernel's gathers do.
-// WHOLE: every piece of every box is inside (no checks).
-template <typename T, int ROWS, int KT, int MODE, int NTH, bool WHOLE>
+// WHOLE: every piece of every box is inside (no checks).  R: rows one lane
+// reads together from the [row][k] layout (RX / RY), which sets the row
+// period of the k-vector permutation.
+template <typename T, int ROWS, int KT, int MODE, int NTH, bool WHOLE, int R>
 struct DirectOperand {
     static constexpr int VW = Traits<T>::VW;
     static constexpr int NW = NTH / 64;
@@ -63,7 +65,7 @@ struct DirectOperand {
 
     // LDS column (in pieces) of piece c of row r in the k-vector layout; an
     // involution, so it also maps an LDS column back to its piece
-    static __device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 2) & (CPR - 1)); }
+    static __device__ __forceinline__ int swz(int r, int c) { return c ^ ((r / R) & (CPR - 1)); }
 
     // rowoff: LDS table of operand offsets per tile row (-1 = outside the
     // tensor); koff / kco: offsets / kj-positions per box position
@@ -129,7 +131,7 @@ struct DirectFrag {
             for (int b = 0; b < NB; ++b) {
                 const int r = w0 + block_row<R>(b, l16);
                 kv[b] = *reinterpret_cast<const vec *>(tile + r * KT +
-                                                      VW * (q ^ ((r >> 2) & (CPR - 1))));
+                                                      VW * (q ^ ((r / R) & (CPR - 1))));
             }
         } else {
 #pragma unroll
@@ -218,8 +220,8 @@ gett_direct_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
     constexpr int NG = KT / (4 * VW);   // step groups per box
     static_assert(KT % (4 * VW) == 0, "whole step groups");
     typedef WaveTile<T, MT, NT, KT, WM, WN, RX, RY> WT;
-    typedef DirectOperand<T, MT, KT, XMODE, NTH, WHOLE> OX;
-    typedef DirectOperand<T, NT, KT, YMODE, NTH, WHOLE> OY;
+    typedef DirectOperand<T, MT, KT, XMODE, NTH, WHOLE, RX> OX;
+    typedef DirectOperand<T, NT, KT, YMODE, NTH, WHOLE, RY> OY;
     typedef DirectFrag<T, XMODE, WT::RB, RX, MT, KT> FX;
     typedef DirectFrag<T, YMODE, WT::CB, RY, NT, KT> FY;
     constexpr int STAGE = (MT + NT) * KT;

@@ -10,7 +10,7 @@ import paper_1607_00145_amd as g
 import workloads as wl
 from gpu_util import split
 
-DIRECT_TILES = {4, 7}   # fp32 tiles that carry the direct-load kernel
+DIRECT_TILES = {4, 7}   # fp32 tiles that carry the direct-load kernel (none in fp64)
 
 
 def describe(modes, ext, dtype=g.GETT_FLOAT32, strides=(None, None, None)):
