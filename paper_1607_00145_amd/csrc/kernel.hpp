@@ -1220,10 +1220,13 @@ gett_macro_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ 
 // stream.  A persistent workgroup walks tiles t = blockIdx.x, + gridDim.x, ...
 // in C's memory order (y fastest), so the workgroups running together write
 // neighbouring stretches of C, and overlaps each tile's stores with the next
-// tile's packing:
-//   tables(t+1); barrier; issue the gathers of t+1;
-//   macro(t) from the packed panels; barrier;
-//   store the gathered panels of t+1 to LDS; unpack(t); barrier.
+// tile's packing and MFMAs.  With tile t's results in the accumulators:
+//   tables(t+1); barrier; issue the gathers of t+1; unpack(t);
+//   store the gathered panels of t+1 to LDS; barrier; macro(t+1).
+// A wavefront's vector memory operations count down in the order they were
+// issued, so waiting for the gathers of t+1 -- issued before the stores of
+// t -- does not wait for those stores: they drain behind the packing and
+// the MFMAs of t+1.
 template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int WPE, int XMODE,
           int YMODE>
 __global__ void __launch_bounds__(WM *WN * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
@@ -1262,6 +1265,7 @@ gett_stream_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
     GY gy;
     WT w;
     w.init(tid);
+    w.zero();
     if (withK) {
         gx.setup(tid, rowX[0], kX, kco, d.xscalar_kfast);
         gy.setup(tid, rowY[0], kY, kco, d.yscalar_kfast, d.yes);
@@ -1269,36 +1273,39 @@ gett_stream_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
         gy.load(Y + (cb.y + oy0), lim);
         gx.store(xs);
         gy.store(ys);
+        __syncthreads();
+        w.template macro<GX::PITCH, GY::PITCH, true, 0, false, GX::kSwz, GY::kSwz>(xs, ys);
     }
-    __syncthreads();
 
     for (int j = 0; t < ntiles; ++j, t += G) {
         const int cur = j & 1;
         const int tn = t + G;
         const bool more = tn < ntiles;
         TileBase nb = cb;
+        // the tables of t+1 go to the other set: tile t's gathers took theirs
+        // into registers, and tile t-1's stores have their addresses
         if (more) {
             nb = tile_base<MT, NT>(d, tn / d.tilesY, tn % d.tilesY);
             tile_tables<MT, NT, NTH>(d, tn / d.tilesY, tn % d.tilesY, nb, tid, rowX[cur ^ 1],
                                      offCx[cur ^ 1], rowY[cur ^ 1], offCy[cur ^ 1]);
         }
-        __syncthreads();
+        __syncthreads();   // tables of t+1 written; every wavefront's MFMAs of t read the panels
         if (more && withK) {
             gx.setup(tid, rowX[cur ^ 1], kX, kco, d.xscalar_kfast);
             gy.setup(tid, rowY[cur ^ 1], kY, kco, d.yscalar_kfast, d.yes);
             gx.load(X + (nb.x + ox0), lim);
             gy.load(Y + (nb.y + oy0), lim);
         }
-        w.zero();
-        if (withK) w.template macro<GX::PITCH, GY::PITCH, false, 0, false, GX::kSwz, GY::kSwz>(xs, ys);
-        __syncthreads();
-        if (more && withK) {
+        w.template unpack<2>(C + (cb.cx + cb.cy), offCx[cur], offCy[cur], alpha, beta, d.cvec != 0);
+        cb = nb;
+        if (!more) break;
+        if (withK) {
             gx.store(xs);
             gy.store(ys);
         }
-        w.unpack(C + (cb.cx + cb.cy), offCx[cur], offCy[cur], alpha, beta, d.cvec != 0);
-        cb = nb;
-        __syncthreads();
+        __syncthreads();   // panels of t+1 written
+        if (withK) w.template macro<GX::PITCH, GY::PITCH, true, 0, false, GX::kSwz, GY::kSwz>(xs, ys);
+        else w.zero();
     }
 }
 

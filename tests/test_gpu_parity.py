@@ -184,15 +184,17 @@ def test_plan_class_on_torch_views(gpu):
     assert p.describe()["dtype"] == "f64"
 
 
-TILES = {np.float32: 7, np.float64: 15}
+TILES = {np.float32: 8, np.float64: 15}
 
 
 @pytest.mark.parametrize("dtype,tile", [(dt, t) for dt in DTYPES for t in range(TILES[dt])])
-@pytest.mark.parametrize("kind", [0, 1])
+@pytest.mark.parametrize("kind", [0, 1, 4])
 @pytest.mark.parametrize("case", ["random", "smallk", "scaled2", "scaled3", "scaled4"])
 def test_every_tile_shape(gpu, monkeypatch, dtype, tile, kind, case):
     """Each compiled tile shape and kernel kind (macro-kernel / persistent
-    streaming kernel), forced through the analyser's test hooks."""
+    streaming kernel / direct-load kernel), forced through the analyser's
+    test hooks (a kind the tile does not carry, or the plan cannot take,
+    runs the tile's macro-kernel)."""
     monkeypatch.setenv("GETT_FORCE_TILE", str(tile))
     monkeypatch.setenv("GETT_FORCE_KIND", str(kind))
     rng = np.random.default_rng(30_000 + 10 * tile + kind)
