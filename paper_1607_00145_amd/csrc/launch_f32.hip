@@ -21,10 +21,11 @@ template <> LaunchFn pick_tile<float, 4>(int, int, int);
 template <> LaunchFn pick_tile<float, 5>(int, int, int);
 template <> LaunchFn pick_tile<float, 6>(int, int, int);
 template <> LaunchFn pick_tile<float, 7>(int, int, int);
+template <> LaunchFn pick_tile<float, 8>(int, int, int);
 
 LaunchFn launch_fn_f32(int tile, int xm, int ym, int kind)
 {
-    static_assert(kNumTilesF32 == 8, "update the tile switch");
+    static_assert(kNumTilesF32 == 9, "update the tile switch");
     switch (tile) {
     case 0: return pick_tile<float, 0>(xm, ym, kind);
     case 1: return pick_tile<float, 1>(xm, ym, kind);
@@ -34,6 +35,7 @@ LaunchFn launch_fn_f32(int tile, int xm, int ym, int kind)
     case 5: return pick_tile<float, 5>(xm, ym, kind);
     case 6: return pick_tile<float, 6>(xm, ym, kind);
     case 7: return pick_tile<float, 7>(xm, ym, kind);
+    case 8: return pick_tile<float, 8>(xm, ym, kind);
     }
     return nullptr;
 }

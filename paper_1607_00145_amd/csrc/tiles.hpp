@@ -41,6 +41,7 @@ constexpr TileShape kTilesF32[] = {
     {64, 32, 32, 2, 2, 2, 1, 2, 2, 2, 0, 0.64f, 0.35f, 0.0f},
     {32, 64, 32, 2, 2, 1, 2, 2, 2, 2, 0, 0.65f, 0.35f, 0.0f},
     {256, 128, 32, 4, 2, 4, 4, 2, 1, 2, 0, 0.75f, 0.55f, 0.0f, 0, 0, 0, 0.89f},
+    {128, 256, 32, 2, 4, 4, 4, 2, 1, 2, 0, 0.75f, 0.55f, 0.0f, 0, 0, 0, 0.89f},
 };
 constexpr TileShape kTilesF64[] = {
     {128, 128, 16, 2, 2, 2, 2, 1, 2, 2, 0, 0.65f, 0.34f, 0.0f},

@@ -10,7 +10,7 @@ import paper_1607_00145_amd as g
 import workloads as wl
 from gpu_util import split
 
-DIRECT_TILES = {4, 7}   # fp32 tiles that carry the direct-load kernel (none in fp64)
+DIRECT_TILES = {4, 7, 8}   # fp32 tiles that carry the direct-load kernel (none in fp64)
 
 
 def describe(modes, ext, dtype=g.GETT_FLOAT32, strides=(None, None, None)):
@@ -27,7 +27,7 @@ def describe(modes, ext, dtype=g.GETT_FLOAT32, strides=(None, None, None)):
 def test_compute_bound_workload_is_direct():
     w = wl.BY_NAME["gemm4_fp32"]
     d = describe((w.modes_C, w.modes_A, w.modes_B), w.extents)
-    assert d["kernel"] == "direct" and (d["tile"]["mt"], d["tile"]["nt"]) == (256, 128)
+    assert d["kernel"] == "direct" and (d["tile"]["mt"], d["tile"]["nt"]) == (128, 256)
     assert d["partials"] == "none" and d["kslices"] == 1
 
 

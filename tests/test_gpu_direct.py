@@ -1,5 +1,6 @@
 """GPU parity of the direct-load kernel, whose operands are copied from device
-memory straight into LDS (fp32 tiles 128 x 128 x 32 and 256 x 128 x 32):
+memory straight into LDS (fp32 tiles 128 x 128 x 32, 256 x 128 x 32 and
+128 x 256 x 32):
 every pair of vector gather modes, one to five K boxes, boxes over two
 contracted indices, ragged tiles and partial boxes (pieces outside the
 tensors written as zeros; a partial last box reuses a buffer that held
@@ -18,8 +19,8 @@ from test_gpu_parity import check_case
 
 pytestmark = pytest.mark.gpu
 # (dtype, tile) pairs that carry the direct-load kernel
-DIRECT_TILES = [(np.float32, "4"), (np.float32, "7")]
-IDS = ["f32-4", "f32-7"]
+DIRECT_TILES = [(np.float32, "4"), (np.float32, "7"), (np.float32, "8")]
+IDS = ["f32-4", "f32-7", "f32-8"]
 BOX = {np.float32: 32, np.float64: 16}   # KT of those tiles
 
 # name: (modes of C, A, B), gather modes (x, y) of the plan; the free extents

@@ -184,7 +184,7 @@ def test_plan_class_on_torch_views(gpu):
     assert p.describe()["dtype"] == "f64"
 
 
-TILES = {np.float32: 8, np.float64: 15}
+TILES = {np.float32: 9, np.float64: 15}
 
 
 @pytest.mark.parametrize("dtype,tile", [(dt, t) for dt in DTYPES for t in range(TILES[dt])])
