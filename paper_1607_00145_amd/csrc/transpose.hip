@@ -226,16 +226,26 @@ gett_status_t transpose_launch(gett_dtype_t dtype, int rank, const int64_t *ext,
     }
     const int kTP = dtype == GETT_FLOAT32 ? Shape<float>::TP : Shape<double>::TP;
     const int kTQ = dtype == GETT_FLOAT32 ? Shape<float>::TQ : Shape<double>::TQ;
-    // P: by input stride until the tile edge is covered; Q: by output stride
+    // P: by input stride until the tile edge is covered; Q: by output stride.
+    // The output's stride-one index leads Q unless it is the input's too
+    // (then the writes run along P): P takes no other index before it, or a
+    // batched transposition such as (a,b,c,d) -> (b,a,d,c) would put b second
+    // in P and write along P with a's output stride.
     std::vector<Idx> byIn = v, P, Q, R;
     std::stable_sort(byIn.begin(), byIn.end(), [](const Idx &a, const Idx &b) { return a.sin < b.sin; });
+    size_t o1 = 0;
+    for (size_t k = 1; k < byIn.size(); ++k)
+        if (byIn[k].sout < byIn[o1].sout) o1 = k;
     int64_t sp = 1, sq = 1;
-    size_t i = 0;
-    for (; i < byIn.size() && sp < kTP; ++i) {
-        P.push_back(byIn[i]);
-        sp *= byIn[i].ext;
+    std::vector<Idx> others;
+    for (size_t k = 0; k < byIn.size(); ++k) {
+        if (sp < kTP && (k != o1 || k == 0)) {
+            P.push_back(byIn[k]);
+            sp *= byIn[k].ext;
+        } else {
+            others.push_back(byIn[k]);
+        }
     }
-    std::vector<Idx> others(byIn.begin() + i, byIn.end());
     std::stable_sort(others.begin(), others.end(), [](const Idx &a, const Idx &b) { return a.sout < b.sout; });
     size_t j = 0;
     for (; j < others.size() && sq < kTQ; ++j) {

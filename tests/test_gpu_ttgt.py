@@ -84,6 +84,9 @@ def test_transpose_random(gpu, seed, dtype):
     ([68, 5, 7], [0, 2, 1]),          # vector writes along the shared stride-one index
     ([8, 12, 20], [2, 0, 1]),         # vector reads over a compound tile side
     ([36, 6, 10], [1, 2, 0]),
+    ([40, 36, 12, 8], [1, 0, 3, 2]),  # batched pair swaps: the output's stride-one
+    ([20, 140, 6], [1, 0, 2]),        # index is second by input stride (not in P)
+    ([8, 3, 44, 12], [2, 1, 0, 3]),
 ])
 def test_transpose_shapes(gpu, dtype, shape, perm):
     rng = np.random.default_rng(61_000 + sum(shape))
