@@ -52,7 +52,7 @@ def log(*a):
 # Sources that decide what the GETT kernel does for a given contraction (the
 # analyser's plan, the launch and the kernel templates).  The committed HBM
 # traffic figure is used only while these are unchanged.
-KERNEL_SOURCES = ("analyse.cpp", "api.cpp", "desc.hpp", "kernel.hpp", "launch.hpp",
+KERNEL_SOURCES = ("analyse.cpp", "api.cpp", "desc.hpp", "direct.hpp", "kernel.hpp", "launch.hpp",
                   "launch_f32.hip", "launch_f64.hip", "plan.hpp", "tiles.hpp")
 
 

@@ -599,8 +599,17 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
                 : perSimd;
         const double kpad = (double)std::max<int64_t>(b.nsteps, 1) * c.kt;
         const double waveFlops = (double)(c.mt / c.wm) * (c.nt / c.wn) * kpad * 2.0;
-        const double tMfma = perSimdRun * waveFlops / (peakSimd * c.eff) *
-                             (kSplitAhead && c.nbuf == 1 && b.nsteps > 1 ? 1.4 : 1.0);
+        // A K split gathers both operands in 16-byte runs whose cache lines
+        // return late: a single LDS buffer waits for them (1.4), and so does a
+        // tile with one wavefront per SIMD (1.7: on the fp32 4D x 4D
+        // contractions 28 and 30 of Appendix A the 128 x 128 x 32 tile took
+        // 17.7 ms, the 128 x 256 x 32 tile with two wavefronts per SIMD
+        // 10.5 ms).
+        const double kSplitWait = !kSplitAhead || b.nsteps <= 1 ? 1.0
+                                  : c.nbuf == 1                 ? 1.4
+                                  : c.wpe == 1                  ? 1.7
+                                                                : 1.0;
+        const double tMfma = perSimdRun * waveFlops / (peakSimd * c.eff) * kSplitWait;
         // The persistent streaming kernel needs the contracted set in one box.
         const bool canStream = c.stream && b.nsteps <= 1;
         // A stream carried by fewer workgroups than CUs gets that share of the
