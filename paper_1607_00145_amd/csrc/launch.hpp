@@ -44,10 +44,12 @@ unsigned persistent_grid(K kernel, int threads, unsigned tiles)
     return (unsigned)n < tiles ? (unsigned)n : tiles;
 }
 
-// Let a kernel take `bytes` of dynamic LDS (above the default cap), once per
-// kernel and device (up to 64 devices; a later device asks again).
-template <typename K>
-hipError_t allow_dynamic_lds(K kernel, size_t bytes)
+// Let the kernel take `bytes` of dynamic LDS (above the default cap), once per
+// kernel and device (up to 64 devices; a later device asks again).  The flag
+// lives in the instantiation for that kernel: kernels that share a signature
+// each ask for themselves.
+template <auto kernel>
+hipError_t allow_dynamic_lds(size_t bytes)
 {
     static std::atomic<int> done[64];
     int dev = 0;
@@ -104,10 +106,14 @@ hipError_t launch_one(const KDesc &d, const void *X, const void *Y, void *C, dou
         // every piece of every box inside the tensors: the variant without checks
         const bool whole = d.sizeX % t.mt == 0 && d.sizeY % t.nt == 0 &&
                            (d.nsteps == 0 || (d.kbox == t.kt && d.extK[d.kj] % d.tj == 0));
-        auto k = whole ? gett_direct_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, XM, YM, true>
-                       : gett_direct_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, XM, YM, false>;
+        constexpr auto kWhole =
+            gett_direct_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, XM, YM, true>;
+        constexpr auto kPart =
+            gett_direct_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, XM, YM, false>;
         constexpr size_t lds = 2 * (size_t)(t.mt + t.nt) * t.kt * sizeof(T);
-        const hipError_t e = allow_dynamic_lds(k, lds);
+        const auto k = whole ? kWhole : kPart;
+        const hipError_t e =
+            whole ? allow_dynamic_lds<kWhole>(lds) : allow_dynamic_lds<kPart>(lds);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(
             k, dim3(tiles - (unsigned)d.tile0), dim3(threads), lds, stream, d,

@@ -1,7 +1,7 @@
 """gett_contract under HIP graph capture (serving loops replay one captured
 contraction): a plain plan, plans over K slices and with a stream-K tail
-(partial tiles summed through the library's workspace) and an alpha = 0
-call, each captured once and replayed several times with eager
+(partial tiles summed through the library's workspace), the direct-load
+kernel and an alpha = 0 call, each captured once and replayed several times with eager
 work between the replays; every replay must equal the eager result bit for
 bit (integer-valued inputs make every sum exact).  The eager call runs
 on the capture stream first: it allocates the stream's workspace, which a
@@ -23,6 +23,10 @@ CASES = {
                        {"GETT_FORCE_KSLICES": "8"}),
     "tail_forced": (("a,b", "a,k", "k,b"), {"a": 300, "b": 290, "k": 333},
                     {"GETT_FORCE_KIND": "3", "GETT_TAIL_WGS": "5"}),
+    # the direct-load kernel (fp32 only; fp64 runs the tile's macro-kernel):
+    # dynamic LDS, loads straight into LDS, ragged tiles and a partial box
+    "direct_forced": (("a,b", "a,k", "k,b"), {"a": 300, "b": 260, "k": 104},
+                      {"GETT_FORCE_TILE": "8", "GETT_FORCE_KIND": "4"}),
 }
 TAIL_TILE = {np.float32: "2", np.float64: "8"}
 
@@ -57,6 +61,8 @@ def test_graph_replay_matches_eager(gpu, monkeypatch, name, alpha, beta, dtype):
             assert d["kslices"] > 1
         if name.startswith("tail"):
             assert d["kernel"] == "tail" and d["tail"]["full_tiles"] > 0
+        if name.startswith("direct") and dtype == np.float32:
+            assert d["kernel"] == "direct"
         if d["kslices"] > 1 or d["kernel"] == "tail":
             assert d["partials"] == "workspace"
         # eager reference, on the stream that captures
