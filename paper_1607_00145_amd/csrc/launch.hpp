@@ -24,9 +24,11 @@ template <> struct TileTable<double> {
 
 // Workgroups of a persistent kernel: as many as fit on the device at once,
 // and no more than there are tiles.  The count per device is looked up once
-// per kernel (the first launch on each device, up to 64 devices).
-template <typename K>
-unsigned persistent_grid(K kernel, int threads, unsigned tiles)
+// per kernel (the first launch on each device, up to 64 devices); the cache
+// lives in the instantiation for that kernel, since kernels that share a
+// signature can differ in occupancy.
+template <auto kernel>
+unsigned persistent_grid(int threads, unsigned tiles)
 {
     static std::atomic<int> cached[64];   // CUs x workgroups per CU, 0: not yet known
     int dev = 0;
@@ -120,8 +122,9 @@ hipError_t launch_one(const KDesc &d, const void *X, const void *Y, void *C, dou
             static_cast<const T *>(X), static_cast<const T *>(Y), static_cast<T *>(C),
             static_cast<T>(alpha), static_cast<T>(beta));
     } else {
-        auto k = gett_stream_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.stream, XM, YM>;
-        const unsigned grid = persistent_grid(k, threads, tiles);
+        constexpr auto k =
+            gett_stream_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.stream, XM, YM>;
+        const unsigned grid = persistent_grid<k>(threads, tiles);
         if (grid == 0) return hipErrorInvalidValue;
         hipLaunchKernelGGL(k, dim3(grid), dim3(threads), 0, stream, d,
                            static_cast<const T *>(X), static_cast<const T *>(Y),

@@ -23,6 +23,8 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <atomic>
+#include <type_traits>
 #include <vector>
 
 #include "transpose.hpp"
@@ -43,7 +45,33 @@ struct TDesc {
     int32_t size[3];                 // products of the extents of P, Q, R
     int32_t tiles[2];                // tiles along P and Q
     int32_t alongP;                  // the output's stride-one index is in P
+    int32_t group;                   // > 0: walk tiles in bands of this many P tiles
 };
+
+// Tile (tp, tq) and point r of R moved by workgroup b.  Tiles run P-fastest:
+// the workgroups resident at one time read neighbouring stretches of the
+// same input rows and, when they span several Q tiles, write neighbouring
+// stretches of the same output rows.  When one row of P tiles alone fills
+// the device, bands of `group` P tiles keep several Q tiles in flight, or
+// every write run of 16-byte vectors would stand alone in its DRAM page.
+__device__ inline void tile_of(const TDesc &d, uint32_t b, int32_t &tp, int32_t &tq, int32_t &r)
+{
+    const uint32_t t0 = (uint32_t)d.tiles[0], t1 = (uint32_t)d.tiles[1];
+    const uint32_t per = t0 * t1;
+    r = (int32_t)(b / per);
+    const uint32_t t = b - (uint32_t)r * per;
+    if (d.group <= 0) {
+        tp = (int32_t)(t % t0);
+        tq = (int32_t)(t / t0);
+        return;
+    }
+    const uint32_t g = (uint32_t)d.group, band = g * t1;
+    const uint32_t first = (t / band) * g;
+    const uint32_t gsz = min(t0 - first, g);
+    const uint32_t in = t - (t / band) * band;
+    tp = (int32_t)(first + in % gsz);
+    tq = (int32_t)(in / gsz);
+}
 
 // Offsets of the linear position `lin` of group g in the input and output.
 __device__ inline void decode(const TDesc &d, int g, int32_t lin, int32_t &oi, int32_t &oo)
@@ -63,136 +91,202 @@ template <typename T> struct Vec;
 template <> struct Vec<float> { typedef float __attribute__((ext_vector_type(4))) type; static constexpr int n = 4; };
 template <> struct Vec<double> { typedef double __attribute__((ext_vector_type(2))) type; static constexpr int n = 2; };
 
-// VL / VS: 16-byte vector reads along P / writes along the output's
-// stride-one side (the host has checked that every vector lies within one
-// index run and is aligned); ALONGP: the output's stride-one index is in P.
+// The phases of moving one tile.  VL / VS: 16-byte vector reads along P /
+// writes along the output's stride-one side (the host has checked that every
+// vector lies within one index run and is aligned); ALONGP: the output's
+// stride-one index is in P.
 template <typename T, bool VL, bool VS, bool ALONGP>
-__global__ __launch_bounds__(Shape<T>::TH) void transpose_kernel(const TDesc d, const T *__restrict__ in,
-                                                                 T *__restrict__ out, T alpha, T beta)
-{
-    constexpr int kTP = Shape<T>::TP, kTQ = Shape<T>::TQ, kThreads = Shape<T>::TH;
+struct Mover {
+    static constexpr int kTP = Shape<T>::TP, kTQ = Shape<T>::TQ, kThreads = Shape<T>::TH;
     typedef typename Vec<T>::type vec;
-    constexpr int VW = Vec<T>::n;
-    constexpr int RL = VL ? VW : 1;   // elements per read
-    constexpr int RS = VS ? VW : 1;   // elements per write
-    __shared__ T tile[kTQ][kTP + 1];   // [q][p]
-    __shared__ int32_t pin[kTP], pout[kTP], qin[kTQ], qout[kTQ];
-
-    const uint32_t b = blockIdx.x;
-    const int32_t tp = (int32_t)(b % (uint32_t)d.tiles[0]);
-    const uint32_t rest = b / (uint32_t)d.tiles[0];
-    const int32_t tq = (int32_t)(rest % (uint32_t)d.tiles[1]);
-    const int32_t r = (int32_t)(rest / (uint32_t)d.tiles[1]);
-    int32_t rin, rout;
-    decode(d, 2, r, rin, rout);
-
-    const int t = threadIdx.x;
+    static constexpr int VW = Vec<T>::n;
+    static constexpr int RL = VL ? VW : 1;   // elements per read
+    static constexpr int RS = VS ? VW : 1;   // elements per write
+    static constexpr int PERL = kTP / RL;    // reading threads per Q row
+    static constexpr int NL = kTQ * PERL / kThreads;
     static_assert(kTP + kTQ <= kThreads, "one table entry per thread");
-    if (t < kTP) {
-        const int32_t p = tp * kTP + t;
-        int32_t oi = -1, oo = -1;
-        if (p < d.size[0]) decode(d, 0, p, oi, oo);
-        pin[t] = oi;
-        pout[t] = oo;
-    } else if (t < kTP + kTQ) {
-        const int32_t q = tq * kTQ + (t - kTP);
-        int32_t oi = -1, oo = -1;
-        if (q < d.size[1]) decode(d, 1, q, oi, oo);
-        qin[t - kTP] = oi;
-        qout[t - kTP] = oo;
-    }
-    __syncthreads();
 
-    const T *src = in + rin;
-    T *dst = out + rout;
-    const bool readIn = alpha != T(0);
-    const bool readOut = beta != T(0);
-    // read along P: a thread takes RL consecutive P positions of one Q row
-    if (readIn) {
-        constexpr int PER = kTP / RL;   // threads per Q row
-        constexpr int N = kTQ * PER / kThreads;
-        const int pl = (t % PER) * RL;
+    // offset tables of tile b (-1: outside the tensor) and its R offsets
+    static __device__ __forceinline__ void tables(const TDesc &d, uint32_t b, int t,
+                                                  int32_t *pin, int32_t *pout, int32_t *qin,
+                                                  int32_t *qout, int32_t &rin, int32_t &rout)
+    {
+        int32_t tp, tq, r;
+        tile_of(d, b, tp, tq, r);
+        decode(d, 2, r, rin, rout);
+        if (t < kTP) {
+            const int32_t p = tp * kTP + t;
+            int32_t oi = -1, oo = -1;
+            if (p < d.size[0]) decode(d, 0, p, oi, oo);
+            pin[t] = oi;
+            pout[t] = oo;
+        } else if (t < kTP + kTQ) {
+            const int32_t q = tq * kTQ + (t - kTP);
+            int32_t oi = -1, oo = -1;
+            if (q < d.size[1]) decode(d, 1, q, oi, oo);
+            qin[t - kTP] = oi;
+            qout[t - kTP] = oo;
+        }
+    }
+
+    // read along P: a thread takes RL consecutive P positions of NL Q rows
+    static __device__ __forceinline__ void load(const T *src, const int32_t *pin,
+                                                const int32_t *qin, int t, T (&v)[NL][RL])
+    {
+        const int pl = (t % PERL) * RL;
         const int32_t oi = pin[pl];
-        T v[N][RL];
+        int32_t qo[NL];   // every table read first: one LDS wait, then the loads
 #pragma unroll
-        for (int j = 0; j < N; ++j) {
-            const int ql = t / PER + (kThreads / PER) * j;
-            const int32_t qo = qin[ql];
-            if (oi >= 0 && qo >= 0) {
+        for (int j = 0; j < NL; ++j) qo[j] = qin[t / PERL + (kThreads / PERL) * j];
+#pragma unroll
+        for (int j = 0; j < NL; ++j) {
+            if (oi >= 0 && qo[j] >= 0) {
                 if constexpr (VL) {
-                    const vec x = *reinterpret_cast<const vec *>(src + oi + qo);
+                    const vec x = *reinterpret_cast<const vec *>(src + oi + qo[j]);
 #pragma unroll
                     for (int e = 0; e < RL; ++e) v[j][e] = x[e];
                 } else {
-                    v[j][0] = src[oi + qo];
+                    v[j][0] = src[oi + qo[j]];
                 }
             } else {
 #pragma unroll
                 for (int e = 0; e < RL; ++e) v[j][e] = T(0);
             }
         }
+    }
+
+    static __device__ __forceinline__ void stash(T (*tile)[kTP + 1], int t, const T (&v)[NL][RL])
+    {
+        const int pl = (t % PERL) * RL;
 #pragma unroll
-        for (int j = 0; j < N; ++j) {
-            const int ql = t / PER + (kThreads / PER) * j;
+        for (int j = 0; j < NL; ++j) {
+            const int ql = t / PERL + (kThreads / PERL) * j;
 #pragma unroll
             for (int e = 0; e < RL; ++e) tile[ql][pl + e] = v[j][e];
         }
     }
-    __syncthreads();
+
     // write: a thread takes RS consecutive positions along the output's
     // stride-one side (P when ALONGP, else Q)
-    constexpr int LEN = ALONGP ? kTP : kTQ;   // tile edge along the write direction
-    constexpr int PER = LEN / RS;
-    constexpr int N = (kTP * kTQ / LEN) * PER / kThreads;
-    const int a = (t % PER) * RS;   // position along the write direction
+    static __device__ __forceinline__ void write(T *dst, const int32_t *pout, const int32_t *qout,
+                                                 const T (*tile)[kTP + 1], int t, T alpha, T beta,
+                                                 bool readIn, bool readOut)
+    {
+        constexpr int LEN = ALONGP ? kTP : kTQ;   // tile edge along the write direction
+        constexpr int PER = LEN / RS;
+        constexpr int N = (kTP * kTQ / LEN) * PER / kThreads;
+        const int a = (t % PER) * RS;   // position along the write direction
+        int32_t off[N];                   // output offsets, -1 outside the tensor
 #pragma unroll
-    for (int j = 0; j < N; ++j) {
-        const int c = t / PER + (kThreads / PER) * j;   // position across it
-        const int pl = ALONGP ? a : c, ql = ALONGP ? c : a;
-        const int32_t oo = pout[pl], qo = qout[ql];
-        if (oo < 0 || qo < 0) continue;
-        T *o = dst + oo + qo;
-        T w[RS];
+        for (int j = 0; j < N; ++j) {
+            const int c = t / PER + (kThreads / PER) * j;   // position across it
+            const int pl = ALONGP ? a : c, ql = ALONGP ? c : a;
+            const int32_t oo = pout[pl], qo = qout[ql];
+            off[j] = oo < 0 || qo < 0 ? -1 : oo + qo;
+        }
 #pragma unroll
-        for (int e = 0; e < RS; ++e)
-            w[e] = readIn ? alpha * (ALONGP ? tile[ql][pl + e] : tile[ql + e][pl]) : T(0);
-        if constexpr (VS) {
-            vec x;
-            if (readOut) {
-                const vec old = *reinterpret_cast<const vec *>(o);
+        for (int j = 0; j < N; ++j) {
+            const int c = t / PER + (kThreads / PER) * j;
+            const int pl = ALONGP ? a : c, ql = ALONGP ? c : a;
+            if (off[j] < 0) continue;
+            T *o = dst + off[j];
+            T w[RS];
 #pragma unroll
-                for (int e = 0; e < RS; ++e) x[e] = beta * old[e] + w[e];
+            for (int e = 0; e < RS; ++e)
+                w[e] = readIn ? alpha * (ALONGP ? tile[ql][pl + e] : tile[ql + e][pl]) : T(0);
+            if constexpr (VS) {
+                vec x;
+                if (readOut) {
+                    const vec old = *reinterpret_cast<const vec *>(o);
+#pragma unroll
+                    for (int e = 0; e < RS; ++e) x[e] = beta * old[e] + w[e];
+                } else {
+#pragma unroll
+                    for (int e = 0; e < RS; ++e) x[e] = w[e];
+                }
+                *reinterpret_cast<vec *>(o) = x;
             } else {
-#pragma unroll
-                for (int e = 0; e < RS; ++e) x[e] = w[e];
+                *o = readOut ? beta * *o + w[0] : w[0];
             }
-            *reinterpret_cast<vec *>(o) = x;
-        } else {
-            *o = readOut ? beta * *o + w[0] : w[0];
         }
     }
+};
+
+// One tile per workgroup: tables, read into LDS, write out.
+template <typename T, bool VL, bool VS, bool ALONGP>
+__global__ __launch_bounds__(Shape<T>::TH) void transpose_kernel(const TDesc d, const T *__restrict__ in,
+                                                                 T *__restrict__ out, T alpha, T beta)
+{
+    typedef Mover<T, VL, VS, ALONGP> M;
+    __shared__ T tile[M::kTQ][M::kTP + 1];   // [q][p]
+    __shared__ int32_t pin[M::kTP], pout[M::kTP], qin[M::kTQ], qout[M::kTQ];
+    const int t = threadIdx.x;
+    int32_t rin, rout;
+    M::tables(d, blockIdx.x, t, pin, pout, qin, qout, rin, rout);
+    __syncthreads();
+    const bool readIn = alpha != T(0);
+    const bool readOut = beta != T(0);
+    if (readIn) {
+        T v[M::NL][M::RL];
+        M::load(in + rin, pin, qin, t, v);
+        M::stash(tile, t, v);
+    }
+    __syncthreads();
+    M::write(out + rout, pout, qout, tile, t, alpha, beta, readIn, readOut);
 }
 
-template <typename T, bool VL, bool VS>
-void launch_t(bool alongP, unsigned blocks, hipStream_t s, const TDesc &d, const void *in, void *out,
-              double alpha, double beta)
+// Workgroups of the kernel resident on the device at once (looked up once
+// per kernel and device, up to 64 devices; 0 when the runtime cannot say).
+template <auto kernel>
+unsigned resident(int threads)
 {
-    if (alongP)
-        hipLaunchKernelGGL((transpose_kernel<T, VL, VS, true>), dim3(blocks), dim3(Shape<T>::TH), 0, s, d,
-                           static_cast<const T *>(in), static_cast<T *>(out), (T)alpha, (T)beta);
-    else
-        hipLaunchKernelGGL((transpose_kernel<T, VL, VS, false>), dim3(blocks), dim3(Shape<T>::TH), 0, s, d,
-                           static_cast<const T *>(in), static_cast<T *>(out), (T)alpha, (T)beta);
+    static std::atomic<int> cached[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    int n = dev >= 0 && dev < 64 ? cached[dev].load(std::memory_order_relaxed) : 0;
+    if (n <= 0) {
+        int cus = 0, per = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, 0) != hipSuccess)
+            return 0;
+        n = cus * (per > 0 ? per : 1);
+        if (dev >= 0 && dev < 64) cached[dev].store(n, std::memory_order_relaxed);
+    }
+    return (unsigned)n;
+}
+
+// P tiles per band when one row of P tiles would hold more than half of the
+// resident workgroups (fp32 76832 x 2048 transposed: 4.9 TB/s walking
+// P-fastest, 5.6 in bands of 32; no band width helps the other shapes)
+constexpr int kBand = 32;
+
+template <typename T, bool VL, bool VS, bool ALONGP>
+hipError_t launch_t(unsigned blocks, hipStream_t s, TDesc d, const void *in, void *out,
+                    double alpha, double beta)
+{
+    constexpr auto k = transpose_kernel<T, VL, VS, ALONGP>;
+    const unsigned n = resident<k>(Shape<T>::TH);
+    if (n == 0) return hipErrorInvalidValue;
+    d.group = 2u * (unsigned)d.tiles[0] > n ? kBand : 0;
+    hipLaunchKernelGGL(k, dim3(blocks), dim3(Shape<T>::TH), 0, s, d, static_cast<const T *>(in),
+                       static_cast<T *>(out), (T)alpha, (T)beta);
+    return hipGetLastError();
 }
 
 template <typename T>
-void launch_typed(bool vl, bool vs, bool alongP, unsigned blocks, hipStream_t s, const TDesc &d,
-                  const void *in, void *out, double alpha, double beta)
+hipError_t launch_typed(bool vl, bool vs, bool alongP, unsigned blocks, hipStream_t s,
+                        const TDesc &d, const void *in, void *out, double alpha, double beta)
 {
-    if (vl && vs) launch_t<T, true, true>(alongP, blocks, s, d, in, out, alpha, beta);
-    else if (vl) launch_t<T, true, false>(alongP, blocks, s, d, in, out, alpha, beta);
-    else if (vs) launch_t<T, false, true>(alongP, blocks, s, d, in, out, alpha, beta);
-    else launch_t<T, false, false>(alongP, blocks, s, d, in, out, alpha, beta);
+    auto go = [&](auto VLc, auto VSc) {
+        return alongP ? launch_t<T, VLc.value, VSc.value, true>(blocks, s, d, in, out, alpha, beta)
+                      : launch_t<T, VLc.value, VSc.value, false>(blocks, s, d, in, out, alpha, beta);
+    };
+    using Y = std::true_type;
+    using N = std::false_type;
+    if (vl && vs) return go(Y{}, Y{});
+    if (vl) return go(Y{}, N{});
+    if (vs) return go(N{}, Y{});
+    return go(N{}, N{});
 }
 
 struct Idx {
@@ -308,11 +402,13 @@ gett_status_t transpose_launch(gett_dtype_t dtype, int rank, const int64_t *ext,
     };
     const bool vl = alpha != 0.0 && vec_ok(P, true, in);
     const bool vs = vec_ok(d.alongP ? P : Q, false, out);
-    if (dtype == GETT_FLOAT32)
-        launch_typed<float>(vl, vs, d.alongP != 0, (unsigned)blocks, stream, d, in, out, alpha, beta);
-    else
-        launch_typed<double>(vl, vs, d.alongP != 0, (unsigned)blocks, stream, d, in, out, alpha, beta);
-    return hipGetLastError() == hipSuccess ? GETT_SUCCESS : GETT_ERROR_HIP;
+    const hipError_t e =
+        dtype == GETT_FLOAT32
+            ? launch_typed<float>(vl, vs, d.alongP != 0, (unsigned)blocks, stream, d, in, out, alpha,
+                                  beta)
+            : launch_typed<double>(vl, vs, d.alongP != 0, (unsigned)blocks, stream, d, in, out,
+                                   alpha, beta);
+    return e == hipSuccess ? GETT_SUCCESS : GETT_ERROR_HIP;
 }
 
 }  // namespace gett

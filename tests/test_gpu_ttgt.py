@@ -87,6 +87,8 @@ def test_transpose_random(gpu, seed, dtype):
     ([40, 36, 12, 8], [1, 0, 3, 2]),  # batched pair swaps: the output's stride-one
     ([20, 140, 6], [1, 0, 2]),        # index is second by input stride (not in P)
     ([8, 3, 44, 12], [2, 1, 0, 3]),
+    ([35001, 300], [1, 0]),           # more P tiles than half the resident workgroups:
+    ([33001, 130, 2], [1, 0, 2]),     # bands of P tiles, the last one short
 ])
 def test_transpose_shapes(gpu, dtype, shape, perm):
     rng = np.random.default_rng(61_000 + sum(shape))
