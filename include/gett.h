@@ -131,10 +131,11 @@ typedef struct gett_plan_s *gett_plan_t;
  * under the same values) and gett_plan_describe lists them ("hooks"):
  *   GETT_FORCE_TILE      tile index to use (gett_plan_describe "tile.id")
  *   GETT_FORCE_KIND      1 streaming kernel, 3 stream-K tail, 4 direct-load
- *                        kernel (on a tile that carries it; the direct-load
- *                        kernel also needs vector gathers of both operands,
- *                        whole tiles and whole K boxes, else the plan runs
- *                        the tile's macro-kernel)
+ *                        kernel, 5 persistent direct-load kernel (on a tile
+ *                        that carries it; the direct-load kernels also need
+ *                        vector gathers of both operands, and the persistent
+ *                        one a contracted set in one K box, else the plan
+ *                        runs the tile's macro-kernel)
  *   GETT_FORCE_KSLICES   number of K slices
  *   GETT_TAIL_WGS        workgroups of the stream-K tail
  *   GETT_SPLIT_F         block size of a split index (Sec. 3.2.1)
@@ -255,8 +256,10 @@ const char *gett_status_string(gett_status_t status);
  * super-indices, operand exchange, loop order, stride-one choices, gather
  * modes, the tile (sizes, wavefront grid, fragment reads, wavefronts per SIMD
  * its registers allow, prefetch depth, LDS buffers, one-box and C-order
- * variants), kernel kind ("macro", "stream", "tail" or "direct": operands
- * copied from device memory straight into LDS), K slices, the
+ * variants), kernel kind ("macro", "stream", "tail", "direct": operands
+ * copied from device memory straight into LDS, or "direct-stream": the same,
+ * by persistent workgroups that copy the next tile's operands while storing
+ * the current tile), K slices, the
  * stream-K tail's whole tiles, workgroups and boxes per workgroup, the
  * partial-tile workspace, grid, the ranked candidates and the flop / byte
  * counts of Eq. 12-14.

@@ -216,7 +216,12 @@ Hooks read_hooks()
 
 const char *kind_name(int k)
 {
-    return k == 1 ? "stream" : k == 2 ? "kslices" : k == 3 ? "tail" : k == 4 ? "direct" : "macro";
+    return k == 1   ? "stream"
+           : k == 2 ? "kslices"
+           : k == 3 ? "tail"
+           : k == 4 ? "direct"
+           : k == 5 ? "direct-stream"
+                    : "macro";
 }
 
 // Workgroups of a tile resident on one CU at once: the wavefronts per SIMD its
@@ -666,6 +671,22 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
             cd.cost = bound(std::max(cd.tMfma, tMem), tChain);
             ranked.push_back(cd);
         }
+        // Persistent direct-load kernel (tiles that carry it): a contracted
+        // set in one box, both operands gathered in vectors; its C stream is
+        // priced at dsbw of the HBM peak.
+        if (c.dsbw > 0.0f && !slowGather && !(flags & GETT_FLAG_SCALAR) && !kSplitAhead &&
+            b.nsteps == 1) {
+            const double tMem = (bytesC + bytesX + bytesY +
+                                 0.05 * (bytesX * (ty - 1) + bytesY * (tx - 1))) /
+                                (8.0e12 * c.dsbw * cuShare);
+            Candidate cd;
+            cd.tile = t;
+            cd.kind = 5;
+            cd.tMfma = tMfma;
+            cd.tMem = tMem;
+            cd.cost = bound(std::max(tMfma, tMem), tChain);
+            ranked.push_back(cd);
+        }
         // K slices: when a contracted set of many boxes meets too few tiles to
         // give every SIMD two wavefronts, P workgroups share each tile's
         // boxes.  Their partial tiles go to the workspace and the last of a
@@ -958,6 +979,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     // The direct-load kernel takes vector gathers of both operands; a plan
     // that ends up otherwise runs its tile's macro-kernel.
     if (kind == 4 && !(xmode <= kGatherKVec && ymode <= kGatherKVec && nsteps >= 1)) kind = 0;
+    if (kind == 5 && !(xmode <= kGatherKVec && ymode <= kGatherKVec && nsteps == 1)) kind = 0;
     bool cvec = !(flags & GETT_FLAG_SCALAR) && Iy[0].strC == 1 && Iy[0].extent % VW == 0;
     for (auto &x : Ix) if (x.strC % VW) cvec = false;
     for (size_t i = 1; i < Iy.size(); ++i) if (Iy[i].strC % VW) cvec = false;
@@ -1170,7 +1192,7 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     }
     o << "]";
     o << ",\"streaming\":" << (streaming ? "true" : "false");
-    o << ",\"kernel\":\"" << (kind == 1 ? "stream" : kind == 3 ? "tail" : kind == 4 ? "direct" : "macro")
+    o << ",\"kernel\":\"" << (kind == 2 ? "macro" : kind_name(kind))
       << "\",\"kslices\":" << kslices;
     o << ",\"tail\":{\"full_tiles\":" << d.tailFull << ",\"workgroups\":" << d.tailWgs
       << ",\"boxes\":" << d.tailLen << "}";

@@ -285,17 +285,19 @@ gett_status_t contract_with(const gett_plan_s &P, double alpha, const void *A, c
     // (streaming walk, beta != 0) runs faster in hardware order (measured).
     if (d.xcdremap < 0) d.xcdremap = (d.order == 1 && beta != 0.0) ? 0 : 1;
     // launch variant: 0 whole tiles, 1 streaming, 2 K slices, 3 stream-K tail,
-    // 4 direct-load
-    int kind = P.kind == 1 || P.kind == 3 || P.kind == 4 ? P.kind : d.kslices > 1 ? 2 : 0;
+    // 4 direct-load, 5 persistent direct-load (one K box)
+    int kind = P.kind == 1 || P.kind == 3 || P.kind == 4 || P.kind == 5 ? P.kind
+               : d.kslices > 1                                            ? 2
+                                                                          : 0;
     if (!readAB) {   // alpha == 0 or empty sum: C <- beta * C, A and B untouched
         d.nsteps = 0;
         d.kslices = 1;
-        if (kind == 3 || kind == 2 || kind == 4) kind = 0;
+        if (kind == 3 || kind == 2 || kind == 4 || kind == 5) kind = 0;
         X = nullptr;
         Y = nullptr;
     }
-    // the direct-load kernel needs both vector gathers (aligned operands)
-    if (kind == 4 && (xmode > kGatherKVec || ymode > kGatherKVec)) kind = 0;
+    // the direct-load kernels need both vector gathers (aligned operands)
+    if ((kind == 4 || kind == 5) && (xmode > kGatherKVec || ymode > kGatherKVec)) kind = 0;
     LaunchFn fn = launch_fn(P.dtype, P.tile, xmode, ymode, kind);
     if (!fn) return GETT_ERROR_NOT_SUPPORTED;
     if (inject_launch_fault()) return GETT_ERROR_HIP;

@@ -9,9 +9,11 @@
 // loads:
 //   row-vector operand: [k][row], as the macro-kernel packs it (no padding);
 //   k-vector operand:   [row][k], the pieces of row r XOR-permuted by
-//                       (r / R) mod (pieces per row), so that the lanes of an
-//                       MFMA read, which take rows R apart at one k piece
-//                       (R = 4 in fp32, 2 in fp64), fall on different banks.
+//                       (r / R) mod (pieces per row) -- rotated by r / R when
+//                       the pieces per row are not a power of two -- so that
+//                       the lanes of an MFMA read, which take rows R apart at
+//                       one k piece (R = 4 in fp32, 2 in fp64), fall on
+//                       different banks.
 // A k-vector piece holds VW consecutive contracted positions, and one LDS
 // read hands them to VW consecutive MFMA steps: the position lane group g
 // supplies in step s is
@@ -37,6 +39,23 @@ namespace gett {
 typedef __attribute__((address_space(1))) void global_void;
 typedef __attribute__((address_space(3))) void lds_void;
 
+// k-vector layout: LDS column of piece c of row r (CPR pieces per row, rows
+// read R at a time).  With 2^n pieces per row the pieces are XOR-permuted by
+// (r / R) mod CPR (an involution); otherwise rotated by r / R.
+template <int CPR, int R>
+__device__ __forceinline__ int kvec_col(int r, int c)
+{
+    if constexpr ((CPR & (CPR - 1)) == 0) return c ^ ((r / R) & (CPR - 1));
+    else return (c + r / R) % CPR;
+}
+// the piece of row r held in LDS column c
+template <int CPR, int R>
+__device__ __forceinline__ int kvec_piece(int r, int c)
+{
+    if constexpr ((CPR & (CPR - 1)) == 0) return c ^ ((r / R) & (CPR - 1));
+    else return (c + CPR - (r / R) % CPR) % CPR;
+}
+
 // The pieces of one operand tile (ROWS x KT elements) one thread loads per
 // box: J per thread, piece p = (j * NW + wave) * 64 + lane of the tile's LDS
 // image.  A piece outside the tensor (its rows past the tile's last, or its
@@ -56,16 +75,15 @@ struct DirectOperand {
     static_assert(MODE == kGatherRowVec || MODE == kGatherKVec, "vector gathers only");
     static_assert(PIECES % NTH == 0 && J >= 1, "whole pieces per thread");
     static_assert(ROWS % VW == 0 && KT % VW == 0, "whole vectors");
-    static_assert((CPR & (CPR - 1)) == 0, "the k-vector permutation needs 2^n pieces per row");
     typedef typename Traits<T>::vec vec;
 
     int goff[J];               // element offset of each piece (tile base and box origin excluded)
     int kc[WHOLE ? 1 : J];     // position along index kj of its first element; kInvalidK: never valid
     int lane;
 
-    // LDS column (in pieces) of piece c of row r in the k-vector layout; an
-    // involution, so it also maps an LDS column back to its piece
-    static __device__ __forceinline__ int swz(int r, int c) { return c ^ ((r / R) & (CPR - 1)); }
+    // piece of row r held in LDS column c of the k-vector layout (the inverse
+    // of kvec_col)
+    static __device__ __forceinline__ int swz(int r, int c) { return kvec_piece<CPR, R>(r, c); }
 
     // rowoff: LDS table of operand offsets per tile row (-1 = outside the
     // tensor); koff / kco: offsets / kj-positions per box position
@@ -130,8 +148,7 @@ struct DirectFrag {
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
                 const int r = w0 + block_row<R>(b, l16);
-                kv[b] = *reinterpret_cast<const vec *>(tile + r * KT +
-                                                      VW * (q ^ ((r / R) & (CPR - 1))));
+                kv[b] = *reinterpret_cast<const vec *>(tile + r * KT + VW * kvec_col<CPR, R>(r, q));
             }
         } else {
 #pragma unroll
@@ -339,6 +356,141 @@ gett_direct_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__
         for (int grp = 0; grp < NG; ++grp) mma(fx[grp], fy[grp]);
     }
     w.template unpack<1>(Ct, offCx, offCy, alpha, beta, d.cvec != 0);
+}
+
+// Persistent direct-load kernel for plans whose contracted set is one K box.
+// Workgroups walk tiles t = tile0 + blockIdx.x, + gridDim.x, ...; tile t's box
+// sits in LDS buffer t mod 2 (per workgroup).  Per tile:
+//   LDS reads of tile t's fragments; offset tables of the next tile (second
+//     table set); barrier;
+//   the copy of the next tile's box into the other buffer;
+//   MFMAs of tile t; its C stores (unpack);
+//   wait for this wavefront's copy; barrier.
+// The copy is issued before the C stores of tile t, so it does not queue
+// behind them (a CU serves its vector memory instructions in order), and the
+// wait for it leaves those stores in flight: vmcnt counts in issue order and
+// every tile issues at least kStores vector memory instructions after its
+// copy when every piece is inside the tensors (WHOLE); otherwise the wait
+// is for everything (vmcnt 0).
+template <typename T, int MT, int NT, int KT, int WM, int WN, int RX, int RY, int XMODE, int YMODE,
+          bool WHOLE>
+__global__ __launch_bounds__(WM * WN * 64) __attribute__((amdgpu_waves_per_eu(2))) void
+gett_direct_stream_kernel(const KDesc d, const T *__restrict__ X, const T *__restrict__ Y,
+                          T *__restrict__ C, const T alpha, const T beta)
+{
+    constexpr int NTH = WM * WN * 64;
+    constexpr int VW = Traits<T>::VW;
+    constexpr int NG = KT / (4 * VW);   // step groups per box
+    static_assert(KT % (4 * VW) == 0, "whole step groups");
+    typedef WaveTile<T, MT, NT, KT, WM, WN, RX, RY> WT;
+    typedef DirectOperand<T, MT, KT, XMODE, NTH, WHOLE, RX> OX;
+    typedef DirectOperand<T, NT, KT, YMODE, NTH, WHOLE, RY> OY;
+    typedef DirectFrag<T, XMODE, WT::RB, RX, MT, KT> FX;
+    typedef DirectFrag<T, YMODE, WT::CB, RY, NT, KT> FY;
+    constexpr int STAGE = (MT + NT) * KT;
+    // vector memory instructions each wavefront issues after a copy: the C
+    // stores of one tile, vectors or single elements (C loads with beta != 0
+    // only add to them)
+    constexpr int kStores = (WT::RB / RX) * WT::NR * (WT::kVecC ? WT::CGV : WT::CB);
+    constexpr int kAfter = kStores < 63 ? kStores : 63;
+    // s_waitcnt (gfx9 encoding): vmcnt kAfter / vmcnt 0, lgkmcnt 0 / lgkmcnt
+    // 0 alone (vmcnt 63), expcnt untouched
+    constexpr int kVmAfter = (kAfter & 15) | ((kAfter >> 4) << 14) | (7 << 4) | (15 << 8);
+    constexpr int kVmLgk0 = 7 << 4;
+    constexpr int kLgk0 = 15 | (3 << 14) | (7 << 4);
+
+    extern __shared__ __attribute__((aligned(16))) char dyn_lds[];
+    T *panels = reinterpret_cast<T *>(dyn_lds);
+    __shared__ int rowX[2][MT], rowY[2][NT], offCx[2][MT], offCy[2][NT];
+    __shared__ int kX[KT], kY[KT], kco[KT];
+
+    const int tid = (int)threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int ntiles = d.tilesX * d.tilesY;
+    box_tables<KT, NTH>(d, tid, kX, kY, kco);
+    int64_t bx0, by0;
+    const int lim = box_origin(d, 0, bx0, by0);
+    WT w;
+    w.init(tid);
+    const int l16 = tid & 15, g = (tid & 63) >> 4;
+    const int xw = w.wm * WT::WTM, yw = w.wn * WT::WTN;
+    OX ox;
+    OY oy;
+    auto barrier = []() { asm volatile("s_barrier" ::: "memory"); };
+    // offset tables of tile t into table set `set`; the tile's operand and C bases
+    auto prepare = [&](int t, int set, const T *&Xt, const T *&Yt, T *&Ct) {
+        int tx, ty;
+        tile_of_block(d, t, ntiles, tx, ty);
+        const TileBase tb = tile_base<MT, NT>(d, tx, ty);
+        tile_tables<MT, NT, NTH>(d, tx, ty, tb, tid, rowX[set], offCx[set], rowY[set], offCy[set]);
+        Xt = X + (tb.x + bx0);
+        Yt = Y + (tb.y + by0);
+        Ct = C + (tb.cx + tb.cy);
+    };
+    auto issue = [&](int set, const T *Xt, const T *Yt, int buf) {
+        ox.setup(tid, rowX[set], kX, kco);
+        oy.setup(tid, rowY[set], kY, kco);
+        T *st = panels + buf * STAGE;
+        ox.issue(Xt, st, wave, lim);
+        oy.issue(Yt, st + MT * KT, wave, lim);
+    };
+    auto mma = [&](const FX &fx, const FY &fy) {
+#pragma unroll
+        for (int s4 = 0; s4 < VW; ++s4)
+#pragma unroll
+            for (int a = 0; a < WT::RB; ++a)
+#pragma unroll
+                for (int b = 0; b < WT::CB; ++b)
+                    w.acc[a][b] = mfma16x16x4(fx.at(a, s4), fy.at(b, s4), w.acc[a][b]);
+    };
+
+    int t = d.tile0 + (int)blockIdx.x;   // the grid holds no more workgroups than tiles
+    const T *Xt, *Yt;
+    T *Ct;
+    prepare(t, 0, Xt, Yt, Ct);
+    __syncthreads();
+    issue(0, Xt, Yt, 0);
+    __builtin_amdgcn_s_waitcnt(kVmLgk0);
+    barrier();
+    int cur = 0;
+    for (;;) {
+        FX fx[NG];
+        FY fy[NG];
+        const T *st = panels + cur * STAGE;
+#pragma unroll
+        for (int grp = 0; grp < NG; ++grp) {
+            fx[grp].read(st, xw, l16, g, grp);
+            fy[grp].read(st + MT * KT, yw, l16, g, grp);
+        }
+        const int tn = t + (int)gridDim.x;
+        const bool more = tn < ntiles;
+        const T *Xn = Xt, *Yn = Yt;
+        T *Cn = Ct;
+        if (more) prepare(tn, cur ^ 1, Xn, Yn, Cn);
+        // this tile's fragments are in registers, the next tile's tables complete
+        __builtin_amdgcn_s_waitcnt(kLgk0);
+        barrier();
+        if (more) issue(cur ^ 1, Xn, Yn, cur ^ 1);
+        // the copy stays ahead of the stores below in issue order
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("" ::: "memory");
+        w.zero();
+#pragma unroll
+        for (int grp = 0; grp < NG; ++grp) mma(fx[grp], fy[grp]);
+        w.template unpack<1, WHOLE>(Ct, offCx[cur], offCy[cur], alpha, beta, d.cvec != 0);
+        if (!more) break;
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("" ::: "memory");
+        // the next tile's box has landed (this wavefront's part; the barrier
+        // covers the others); this tile's stores may still be in flight
+        __builtin_amdgcn_s_waitcnt(WHOLE ? kVmAfter : kVmLgk0);
+        barrier();
+        t = tn;
+        Xt = Xn;
+        Yt = Yn;
+        Ct = Cn;
+        cur ^= 1;
+    }
 }
 
 }  // namespace gett

@@ -456,29 +456,43 @@ template <int MT, int NT, int NTH>
 __device__ __forceinline__ void tile_tables(const KDesc &d, int tx, int ty, const TileBase &b,
                                             int tid, int *rowX, int *offCx, int *rowY, int *offCy)
 {
-    for (int r = tid; r < MT + NT; r += NTH) {
-        const bool isx = r < MT;
-        const int rr = isx ? r : r - MT;
-        uint32_t v = (uint32_t)(isx ? tx * MT : ty * NT) + rr;
-        int oo = -1, oc = -1;
-        if ((int64_t)v < (isx ? d.sizeX : d.sizeY)) {
-            int64_t o64 = 0, c64 = 0;
-            const int n = isx ? d.nx : d.ny;
-            for (int i = 0; i < n; ++i) {
-                const uint32_t e = (uint32_t)(isx ? d.extX[i] : d.extY[i]);
-                const uint32_t q = v / e;
-                const uint32_t id = v - q * e;
-                v = q;
-                o64 += (int64_t)id * (isx ? d.strXop[i] : d.strYop[i]);
-                c64 += (int64_t)id * (isx ? d.strCx[i] : d.strCy[i]);
-            }
-            oo = (int)(o64 - (isx ? b.x : b.y));
-            oc = (int)(c64 - (isx ? b.cx : b.cy));
+    // the x and y sides in separate branches: each reads its descriptor
+    // arrays at wave-uniform indices (scalar loads, which do not wait behind
+    // the wavefront's vector memory instructions in flight)
+    auto decode = [](uint32_t v, int n, const int32_t *ext, const int64_t *so, const int64_t *sc,
+                     int64_t &o64, int64_t &c64) {
+        o64 = 0;
+        c64 = 0;
+        for (int i = 0; i < n; ++i) {
+            const uint32_t e = (uint32_t)ext[i];
+            const uint32_t q = v / e;
+            const uint32_t id = v - q * e;
+            v = q;
+            o64 += (int64_t)id * so[i];
+            c64 += (int64_t)id * sc[i];
         }
-        if (isx) {
-            rowX[rr] = oo;
-            offCx[rr] = oc;
+    };
+    for (int r = tid; r < MT + NT; r += NTH) {
+        int64_t o64, c64;
+        if (r < MT) {
+            const uint32_t v = (uint32_t)(tx * MT) + r;
+            int oo = -1, oc = -1;
+            if ((int64_t)v < d.sizeX) {
+                decode(v, d.nx, d.extX, d.strXop, d.strCx, o64, c64);
+                oo = (int)(o64 - b.x);
+                oc = (int)(c64 - b.cx);
+            }
+            rowX[r] = oo;
+            offCx[r] = oc;
         } else {
+            const int rr = r - MT;
+            const uint32_t v = (uint32_t)(ty * NT) + rr;
+            int oo = -1, oc = -1;
+            if ((int64_t)v < d.sizeY) {
+                decode(v, d.ny, d.extY, d.strYop, d.strCy, o64, c64);
+                oo = (int)(o64 - b.y);
+                oc = (int)(c64 - b.cy);
+            }
             rowY[rr] = oo;
             offCy[rr] = oc;
         }
@@ -740,7 +754,10 @@ struct WaveTile {
     // E > 0 (vector C accesses only): skip the column groups that lie in a run
     // of E columns wholly inside the tile's columns [y0, ylim) -- those are
     // stored in C's memory order by unpack_c_order.
-    template <int PARTS = 1>
+    //
+    // ALL: every row and column of the tile lies inside C (no offset checks,
+    // so every wavefront issues every store).
+    template <int PARTS = 1, bool ALL = false>
     __device__ __forceinline__ void unpack(T *__restrict__ C, const int *offCx, const int *offCy,
                                            T alpha, T beta, bool cvec, int y0 = 0, int ylim = 0,
                                            int E = 0) const
@@ -768,7 +785,7 @@ struct WaveTile {
                         for (int p = 0; p < NP; ++p)
 #pragma unroll
                             for (int cg = 0; cg < CGV; ++cg)
-                                if (ox[part * NP + p] >= 0 && oy[cg] >= 0)
+                                if (ALL || (ox[part * NP + p] >= 0 && oy[cg] >= 0))
                                     cv[p][cg] = __builtin_nontemporal_load(reinterpret_cast<const vec *>(
                                         C + ox[part * NP + p] + oy[cg]));
                     }
@@ -777,7 +794,7 @@ struct WaveTile {
 #pragma unroll
                         for (int cg = 0; cg < CGV; ++cg) {
                             const int q = part * NP + p;
-                            if (ox[q] < 0 || oy[cg] < 0) continue;
+                            if (!ALL && (ox[q] < 0 || oy[cg] < 0)) continue;
                             vec out;
 #pragma unroll
                             for (int j = 0; j < VW; ++j) {
@@ -801,7 +818,7 @@ struct WaveTile {
                         for (int p = 0; p < NP; ++p)
 #pragma unroll
                             for (int b = 0; b < CB; ++b)
-                                if (ox[part * NP + p] >= 0 && oy[b] >= 0)
+                                if (ALL || (ox[part * NP + p] >= 0 && oy[b] >= 0))
                                     cv[p][b] = __builtin_nontemporal_load(C + ox[part * NP + p] + oy[b]);
                     }
 #pragma unroll
@@ -809,7 +826,7 @@ struct WaveTile {
 #pragma unroll
                         for (int b = 0; b < CB; ++b) {
                             const int q = part * NP + p;
-                            if (ox[q] < 0 || oy[b] < 0) continue;
+                            if (!ALL && (ox[q] < 0 || oy[b] < 0)) continue;
                             const T a = alpha * acc[grp * RX + q / 4][b][q % 4];
                             __builtin_nontemporal_store(readC ? a + beta * cv[p][b] : a,
                                                         C + ox[q] + oy[b]);

@@ -28,7 +28,7 @@ template <> struct TileTable<double> {
 // lives in the instantiation for that kernel, since kernels that share a
 // signature can differ in occupancy.
 template <auto kernel>
-unsigned persistent_grid(int threads, unsigned tiles)
+unsigned persistent_grid(int threads, unsigned tiles, size_t lds = 0)
 {
     static std::atomic<int> cached[64];   // CUs x workgroups per CU, 0: not yet known
     int dev = 0;
@@ -38,7 +38,7 @@ unsigned persistent_grid(int threads, unsigned tiles)
         int cus = 0, per = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
             return 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, 0) != hipSuccess)
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, lds) != hipSuccess)
             return 0;
         n = cus * (per > 0 ? per : 1);
         if (dev >= 0 && dev < 64) cached[dev].store(n, std::memory_order_relaxed);
@@ -121,6 +121,26 @@ hipError_t launch_one(const KDesc &d, const void *X, const void *Y, void *C, dou
             k, dim3(tiles - (unsigned)d.tile0), dim3(threads), lds, stream, d,
             static_cast<const T *>(X), static_cast<const T *>(Y), static_cast<T *>(C),
             static_cast<T>(alpha), static_cast<T>(beta));
+    } else if constexpr (KIND == 5) {
+        if (d.kslices > 1 || d.nsteps != 1) return hipErrorInvalidValue;   // one K box
+        if ((unsigned)d.tile0 >= tiles) return hipSuccess;
+        const bool whole = d.sizeX % t.mt == 0 && d.sizeY % t.nt == 0 && d.kbox == t.kt &&
+                           d.extK[d.kj] % d.tj == 0;
+        constexpr auto kWhole =
+            gett_direct_stream_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, XM, YM, true>;
+        constexpr auto kPart =
+            gett_direct_stream_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, XM, YM, false>;
+        constexpr size_t lds = 2 * (size_t)(t.mt + t.nt) * t.kt * sizeof(T);
+        const auto k = whole ? kWhole : kPart;
+        hipError_t e = whole ? allow_dynamic_lds<kWhole>(lds) : allow_dynamic_lds<kPart>(lds);
+        if (e != hipSuccess) return e;
+        const unsigned left = tiles - (unsigned)d.tile0;
+        const unsigned grid = whole ? persistent_grid<kWhole>(threads, left, lds)
+                                    : persistent_grid<kPart>(threads, left, lds);
+        if (grid == 0) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(k, dim3(grid), dim3(threads), lds, stream, d,
+                           static_cast<const T *>(X), static_cast<const T *>(Y),
+                           static_cast<T *>(C), static_cast<T>(alpha), static_cast<T>(beta));
     } else {
         constexpr auto k =
             gett_stream_kernel<T, t.mt, t.nt, t.kt, t.wm, t.wn, t.rx, t.ry, t.stream, XM, YM>;
@@ -139,6 +159,7 @@ LaunchFn pick_modes(int xm, int ym, int kind)
     constexpr bool kStream = TileTable<T>::tiles[TI].stream != 0;
     constexpr bool kTail = TileTable<T>::tiles[TI].tail != 0;
     constexpr bool kDirect = TileTable<T>::tiles[TI].deff > 0.0f;
+    constexpr bool kDStream = TileTable<T>::tiles[TI].dsbw > 0.0f;
 #define GETT_CASE(a, b)                                                                       \
     if (xm == a && ym == b) {                                                                 \
         constexpr bool kDir = kDirect && a <= 1 && b <= 1;   /* vector gathers only */       \
@@ -147,6 +168,8 @@ LaunchFn pick_modes(int xm, int ym, int kind)
         if (kind == 1 && kStream) return &launch_one<T, TI, a, b, kStream ? 1 : 0>;          \
         if (kind == 3 && kTail) return &launch_one<T, TI, a, b, kTail ? 3 : 0>;              \
         if (kind == 4 && kDir) return &launch_one<T, TI, a, b, kDir ? 4 : 0>;                \
+        constexpr bool kDS = kDStream && a <= 1 && b <= 1;                                    \
+        if (kind == 5 && kDS) return &launch_one<T, TI, a, b, kDS ? 5 : 0>;                  \
         return nullptr;                                                                       \
     }
     GETT_CASE(0, 0) GETT_CASE(0, 1) GETT_CASE(0, 2) GETT_CASE(0, 3) GETT_CASE(0, 4)

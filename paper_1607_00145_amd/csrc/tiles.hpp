@@ -30,6 +30,9 @@ struct TileShape {
     float deff;  // > 0: also compiled as the direct-load kernel (operands copied
                  // straight into LDS), which sustains this fraction of the MFMA
                  // peak when compute-bound
+    float dsbw;  // > 0: also compiled as the persistent direct-load kernel for
+                 // plans whose contracted set is one K box, which sustains this
+                 // fraction of the HBM peak when streaming C
 };
 
 constexpr TileShape kTilesF32[] = {
@@ -58,7 +61,7 @@ constexpr TileShape kTilesF64[] = {
     {64, 128, 24, 2, 2, 2, 2, 3, 1, 1, 0, 0.785f, 0.668f, 0.0f, 0, 0, 1},
     {64, 32, 16, 2, 2, 2, 1, 2, 2, 2, 0, 0.70f, 0.485f, 0.0f},
     {32, 64, 16, 2, 2, 1, 2, 2, 2, 2, 0, 0.71f, 0.49f, 0.0f},
-    {64, 128, 24, 2, 2, 2, 2, 4, 1, 1, 0, 0.785f, 0.70f, 0.0f, 1},
+    {64, 128, 24, 2, 2, 2, 2, 4, 1, 1, 0, 0.785f, 0.70f, 0.0f, 1, 0, 0, 0.0f, 0.75f},
 };
 constexpr int kNumTilesF32 = sizeof(kTilesF32) / sizeof(kTilesF32[0]);
 constexpr int kNumTilesF64 = sizeof(kTilesF64) / sizeof(kTilesF64[0]);

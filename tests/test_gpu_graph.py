@@ -1,8 +1,8 @@
 """gett_contract under HIP graph capture (serving loops replay one captured
 contraction): a plain plan, plans over K slices and with a stream-K tail
 (partial tiles summed through the library's workspace), the direct-load
-kernel and an alpha = 0 call, each captured once and replayed several times with eager
-work between the replays; every replay must equal the eager result bit for
+kernels and an alpha = 0 call, each captured once and replayed several
+times with eager work between the replays; every replay must equal the eager result bit for
 bit (integer-valued inputs make every sum exact).  The eager call runs
 on the capture stream first: it allocates the stream's workspace, which a
 capture must not do."""
@@ -27,6 +27,10 @@ CASES = {
     # dynamic LDS, loads straight into LDS, ragged tiles and a partial box
     "direct_forced": (("a,b", "a,k", "k,b"), {"a": 300, "b": 260, "k": 104},
                       {"GETT_FORCE_TILE": "8", "GETT_FORCE_KIND": "4"}),
+    # the persistent direct-load kernel (fp64 only): workgroups that walk
+    # several tiles, a partial K box
+    "direct_stream_forced": (("a,b", "a,k", "k,b"), {"a": 2000, "b": 2600, "k": 22},
+                             {"GETT_FORCE_TILE": "14", "GETT_FORCE_KIND": "5"}),
 }
 TAIL_TILE = {np.float32: "2", np.float64: "8"}
 
@@ -61,8 +65,10 @@ def test_graph_replay_matches_eager(gpu, monkeypatch, name, alpha, beta, dtype):
             assert d["kslices"] > 1
         if name.startswith("tail"):
             assert d["kernel"] == "tail" and d["tail"]["full_tiles"] > 0
-        if name.startswith("direct") and dtype == np.float32:
+        if name.startswith("direct_forced") and dtype == np.float32:
             assert d["kernel"] == "direct"
+        if name.startswith("direct_stream") and dtype == np.float64:
+            assert d["kernel"] == "direct-stream"
         if d["kslices"] > 1 or d["kernel"] == "tail":
             assert d["partials"] == "workspace"
         # eager reference, on the stream that captures

@@ -8,8 +8,8 @@ once spilled 176 bytes per lane and ran twice as long).  For each workload
 and a few Appendix A contractions whose kernels sit at their register caps,
 the kernel of the model's plan must not spill (the stream-K tail kernel,
 whose piece loop carries more state, within a small budget), the one-box
-fp64 tile must stay within 128 VGPRs (four wavefronts per SIMD), and the
-direct-load kernels within 256 (two)."""
+fp64 tile's macro-kernels must stay within 128 VGPRs (four wavefronts per
+SIMD), and the direct-load kernels, persistent or not, within 256 (two)."""
 import json
 import os
 import re
@@ -30,6 +30,7 @@ MODES = {"row-vector": 0, "k-vector": 1, "scalar": 2, "row-vector-strided": 3,
 BUNDLE = b"__CLANG_OFFLOAD_BUNDLE__"
 NAME = re.compile(r"_ZN4gett17gett_macro_kernelI([fd])((?:Li\d+E)+)EEv")
 DIRECT = re.compile(r"_ZN4gett18gett_direct_kernelI([fd])((?:Li\d+E)+)Lb([01])EEEv")
+DSTREAM = re.compile(r"_ZN4gett25gett_direct_stream_kernelI([fd])((?:Li\d+E)+)Lb([01])EEEv")
 TAIL_SCRATCH_BUDGET = 64   # bytes per lane
 
 
@@ -61,7 +62,8 @@ def code_objects(lib):
 @pytest.fixture(scope="module")
 def kernels():
     """(type, template integer arguments) -> (scratch bytes per lane, VGPRs)
-    for every gett_macro_kernel instantiation in the library."""
+    for every gett_macro_kernel instantiation in the library; ("direct" or
+    "dstream", type, arguments + (WHOLE,)) for the direct-load kernels."""
     if not os.path.exists(f"{LLVM}/llvm-readelf"):
         pytest.skip("llvm-readelf not found")
     res = {}
@@ -77,11 +79,13 @@ def kernels():
                 if not m:
                     m, kind = DIRECT.search(blk), "direct"
                 if not m:
+                    m, kind = DSTREAM.search(blk), "dstream"
+                if not m:
                     continue
                 field = lambda key: int(re.search(rf"\.{key}:\s+(\d+)", blk).group(1))
                 args = tuple(int(x) for x in re.findall(r"Li(\d+)E", m.group(2)))
                 key = ((m.group(1), args) if kind == "macro" else
-                       ("direct", m.group(1), args + (int(m.group(3)),)))
+                       (kind, m.group(1), args + (int(m.group(3)),)))
                 res[key] = (field("private_segment_fixed_size"), field("vgpr_count"))
     finally:
         shutil.rmtree(tmp)
@@ -105,10 +109,11 @@ def plan_kernel(w, kernels):
         g.gett_destroy(h)
     t = d["tile"]
     T = "f" if w.dtype == "f32" else "d"
-    if d["kernel"] == "direct":
+    if d["kernel"] in ("direct", "direct-stream"):
+        kind = "direct" if d["kernel"] == "direct" else "dstream"
         args = (t["mt"], t["nt"], t["kt"], t["waves"][0], t["waves"][1], t["reads"][0],
                 t["reads"][1], MODES[d["gather_x"]], MODES[d["gather_y"]])
-        both = [kernels.get(("direct", T, args + (whole,))) for whole in (0, 1)]
+        both = [kernels.get((kind, T, args + (whole,))) for whole in (0, 1)]
         assert all(both), (w.name, args)
         return d, args, (max(v[0] for v in both), max(v[1] for v in both))
     want = {0: t["mt"], 1: t["nt"], 2: t["kt"], 3: t["waves"][0], 4: t["waves"][1],
@@ -140,11 +145,14 @@ def test_model_kernel_does_not_spill(kernels, name, w):
 
 
 def test_direct_kernels_keep_two_wavefronts_per_simd(kernels):
-    """Every direct-load kernel: no spills, at most 256 VGPRs (two
-    wavefronts per SIMD: the 256 x 128 and 128 x 256 tiles' eight, or two
-    workgroups of four)."""
+    """Every direct-load kernel, persistent or not: no spills, at most 256
+    VGPRs (two wavefronts per SIMD: the 256 x 128 and 128 x 256 tiles' eight,
+    or two workgroups of four)."""
     direct = {k: v for k, v in kernels.items() if k[0] == "direct"}
     assert len(direct) >= 24, "the direct-load kernels of the fp32 tiles, both variants"
+    dstream = {k: v for k, v in kernels.items() if k[0] == "dstream"}
+    assert len(dstream) >= 8, "the persistent kernels of the fp64 one-box tile, both variants"
+    direct.update(dstream)
     for key, (scratch, vgprs) in direct.items():
         assert scratch == 0 and vgprs <= 256, (key, scratch, vgprs)
 
@@ -155,7 +163,16 @@ def test_compute_bound_fp32_workload_runs_direct(kernels):
 
 
 def test_one_box_tile_keeps_four_wavefronts_per_simd(kernels):
-    """ccsdt6's one-box fp64 tile: four workgroups per CU need <= 128 VGPRs."""
+    """ccsdt6's tile runs the persistent direct-load kernel (two workgroups
+    per CU: at most 256 VGPRs); its one-box macro-kernel, which runs the calls
+    that kernel does not take, keeps four workgroups per CU (<= 128 VGPRs)."""
     d, args, (scratch, vgprs) = plan_kernel(wl.BY_NAME["ccsdt6_fp64"], kernels)
-    assert args[12] == 1, "the plan should use the one-box tile"
-    assert vgprs <= 128 and scratch == 0, (args, vgprs, scratch)
+    assert d["kernel"] == "direct-stream" and args[:3] == (64, 128, 24)
+    assert vgprs <= 256 and scratch == 0, (args, vgprs, scratch)
+    modes = (MODES[d["gather_x"]], MODES[d["gather_y"]])
+    onebox = {k: v for k, v in kernels.items()
+              if len(k) == 2 and k[0] == "d" and k[1][:3] == (64, 128, 24) and k[1][12] == 1
+              and k[1][10:12] == modes and k[1][14:] == (0, 0)}
+    assert onebox, "the one-box macro-kernels of the 64 x 128 x 24 fp64 tile"
+    for key, (scratch, vgprs) in onebox.items():
+        assert vgprs <= 128 and scratch == 0, (key, vgprs, scratch)
