@@ -570,6 +570,12 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
     // workspace: the stream of partial tiles and one workgroup's reads of a
     // tile's pieces are priced at these rates (MI355X).
     constexpr double kPartialBw = 5.0e12, kSumBw = 1.0e11;
+    // C's run along y: the leading y indices that follow one another in C
+    int64_t cRunY = 0;
+    if (!Iy.empty() && Iy[0].strC == 1) {
+        cRunY = Iy[0].extent;
+        for (size_t i = 1; i < Iy.size() && Iy[i].strC == cRunY; ++i) cRunY *= Iy[i].extent;
+    }
     // Every (tile, kernel kind) pair is a candidate; the model ranks them.
     std::vector<Candidate> ranked;
     for (int t = 0; t < num_tiles(dtype); ++t) {
@@ -673,12 +679,17 @@ gett_status_t analyse(gett_plan_s &plan, gett_dtype_t dtype, const char *mC, con
         }
         // Persistent direct-load kernel (tiles that carry it): a contracted
         // set in one box, both operands gathered in vectors; its C stream is
-        // priced at dsbw of the HBM peak.
+        // priced at dsbw of the HBM peak when C's rows along y run at least a
+        // tile wide, else as the macro-kernel's (short runs: measured 1-7%
+        // slower than the macro-kernel on the fp64 6D contractions of
+        // Appendix A whose y set leads with one index of 24, 3-5% faster
+        // on those whose y set leads with a merged run of 384).
         if (c.dsbw > 0.0f && !slowGather && !(flags & GETT_FLAG_SCALAR) && !kSplitAhead &&
             b.nsteps == 1) {
+            const double dbw = cRunY >= c.nt ? c.dsbw : c.bw;
             const double tMem = (bytesC + bytesX + bytesY +
                                  0.05 * (bytesX * (ty - 1) + bytesY * (tx - 1))) /
-                                (8.0e12 * c.dsbw * cuShare);
+                                (8.0e12 * dbw * cuShare);
             Candidate cd;
             cd.tile = t;
             cd.kind = 5;
