@@ -1,10 +1,10 @@
-// direct.hpp -- the direct-load variant of the macro-kernel (device code).
+// direct.hpp -- the direct-load variants of the macro-kernel (device code).
 //
-// When both operands are gathered in 16-byte vectors (row or k vectors) and
-// every tile row and every K box lies inside the tensors, packing (Eq. 9-10)
-// needs no registers: the load unit copies each 16-byte piece from device
-// memory straight into LDS (global_load_lds_dwordx4: lane i of one
-// instruction fills bytes [16 i, 16 i + 16) after a wave-uniform LDS base).
+// When both operands are gathered in 16-byte vectors (row or k vectors),
+// packing (Eq. 9-10) needs no registers: the load unit copies each 16-byte
+// piece from device memory straight into LDS (global_load_lds_dwordx4: lane
+// i of one instruction fills bytes [16 i, 16 i + 16) after a wave-uniform LDS
+// base); a piece outside the tensors is written as zeros by its thread.
 // The LDS layout of an operand tile is then fixed by which piece each lane
 // loads:
 //   row-vector operand: [k][row], as the macro-kernel packs it (no padding);
@@ -31,6 +31,11 @@
 //     last step group.
 // Nothing is staged in registers but the fragments, so a workgroup of eight
 // wavefronts (two per SIMD) fits a 256 x 128 fp32 tile.
+//
+// The persistent variant (gett_direct_stream_kernel, contracted sets of one
+// box) walks several tiles per workgroup and copies the next tile's box into
+// the other buffer before storing the current tile's C, so the copy is not
+// queued behind those stores.
 #pragma once
 #include "kernel.hpp"
 
