@@ -3,9 +3,9 @@ is one K box; fp64 tile 64 x 128 x 24): every pair of vector gather modes, a
 whole box, a partial box and a short one, workgroups that walk several tiles
 (more tiles than resident workgroups), ragged tiles, the 6D x 4D structure of
 the write-only fp64 workload, every beta path, integer inputs (exact whatever
-the order of the additions), and the calls that run the tile's macro-kernel
-instead (alpha = 0, operands not 16-byte aligned, a contracted set of two
-boxes), against the oracle."""
+the order of the additions), C unaligned or gapped (single-element stores),
+and the calls that run the tile's macro-kernel instead (alpha = 0, operands
+not 16-byte aligned, a contracted set of two boxes), against the oracle."""
 import json
 
 import numpy as np
@@ -112,3 +112,20 @@ def test_direct_stream_fallbacks(gpu, forced):
     ext2 = {"a": 256, "b": 256, "k": 48}
     assert describe(modes, ext2)["kernel"] == "macro"
     check_case(gpu, rng, modes, shapes(modes, ext2), np.float64, 1.0, 0.5)
+
+
+@pytest.mark.parametrize("beta", [0.0, 1.5])
+def test_direct_stream_unaligned_or_gapped_c(gpu, forced, beta):
+    """C whose base is not 16-byte aligned, or C with gaps between its rows:
+    the persistent kernel still runs (its operands are aligned) and stores
+    single elements (whole tiles: every store issued, no offset checks)."""
+    modes = MODE_CASES["ab-ak-kb"][0]
+    ext = {"a": 1024, "b": 768, "k": 24}
+    assert describe(modes, ext)["kernel"] == "direct-stream"
+    rng = np.random.default_rng(77)
+    check_case(gpu, rng, modes, shapes(modes, ext), np.float64, 1.0, beta, offsets=(1, 0, 0))
+    check_case(gpu, rng, modes, shapes(modes, ext), np.float64, -0.5, beta,
+               kinds=("gapped", "dense", "dense"))
+    got, ref = check_case(gpu, rng, modes, shapes(modes, ext), np.float64, 1.0, beta,
+                          dist="int", offsets=(1, 0, 0))
+    np.testing.assert_array_equal(got.astype(np.float64), ref.out64)
